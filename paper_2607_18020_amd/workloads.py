@@ -1,0 +1,262 @@
+"""Seeded synthetic workloads for the five FD residual operators.
+
+This module holds the operator registry (op ids, field/const names, grid
+spacings, PDE coefficients) and the seeded input generators.  It contains none
+of the residual or adjoint arithmetic: only sums of Fourier modes and Gaussian
+noise that stand in for the grid-aligned network outputs the operator consumes
+(the paper feeds the operator with fields produced by a neural field generator,
+Sec. 2 intro; its trained fields are not available, so seeded fields of the same
+shape and smoothness are used instead).
+
+Every generator is a pure function of (config, seed, shape): it draws all of its
+random numbers from ``numpy.random.default_rng(seed)``, evaluates the fields in
+float64 and rounds them once to float32.  The float32 arrays are the canonical
+inputs; the CPU oracle receives them widened exactly to float64.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+# Operator ids shared by the C ABI and the oracle (numbers only).
+BURGERS_1DT = 1
+HELMHOLTZ_2D = 2
+HEAT_3D_BE = 3
+NS_2D_STEADY = 4
+NS_3D_BE = 5
+
+OP_NAMES = {
+    BURGERS_1DT: "burgers_1dt",
+    HELMHOLTZ_2D: "helmholtz_2d",
+    HEAT_3D_BE: "heat_3d_be",
+    NS_2D_STEADY: "ns_2d_steady",
+    NS_3D_BE: "ns_3d_be",
+}
+
+
+@dataclasses.dataclass(frozen=True)
+class OpSpec:
+    """Static description of one operator: which arrays it reads and writes."""
+
+    op: int
+    ndim: int
+    fields: Tuple[str, ...]      # differentiated inputs, in ABI order
+    consts: Tuple[str, ...]      # non-differentiated inputs, in ABI order
+    residuals: Tuple[str, ...]   # residual equations, in ABI order
+
+
+OPS: Dict[int, OpSpec] = {
+    BURGERS_1DT: OpSpec(BURGERS_1DT, 2, ("u",), (), ("R",)),
+    HELMHOLTZ_2D: OpSpec(HELMHOLTZ_2D, 2, ("u",), ("f",), ("R",)),
+    HEAT_3D_BE: OpSpec(HEAT_3D_BE, 3, ("u",), ("u0",), ("R",)),
+    NS_2D_STEADY: OpSpec(NS_2D_STEADY, 2, ("u", "v", "p"), (), ("R_u", "R_v", "R_c")),
+    NS_3D_BE: OpSpec(NS_3D_BE, 3, ("u", "v", "w", "p"), ("u_prev", "v_prev", "w_prev"),
+                     ("R_u", "R_v", "R_w", "R_c")),
+}
+
+
+@dataclasses.dataclass(frozen=True)
+class Coeffs:
+    """PDE coefficients; an operator ignores the members it does not use."""
+
+    nu: float = 0.0
+    k: float = 0.0
+    dt: float = 1.0
+    alpha: float = 0.0
+
+
+@dataclasses.dataclass
+class Workload:
+    """One concrete operator instance: arrays plus everything the ABI needs."""
+
+    name: str
+    op: int
+    shape: Tuple[int, ...]
+    h: Tuple[float, ...]
+    coeffs: Coeffs
+    fields: List[np.ndarray]   # float32, C-contiguous
+    consts: List[np.ndarray]   # float32, C-contiguous
+
+    @property
+    def spec(self) -> OpSpec:
+        return OPS[self.op]
+
+    @property
+    def n_points(self) -> int:
+        return int(np.prod(self.shape))
+
+    @property
+    def n_residual_points(self) -> int:
+        return int(np.prod([s - 2 for s in self.shape]))
+
+
+@dataclasses.dataclass(frozen=True)
+class Config:
+    """A named workload: operator, full-size grid, domain and coefficients."""
+
+    name: str
+    op: int
+    shape: Tuple[int, ...]
+    coeffs: Coeffs
+    description: str
+
+
+# The five workloads: 1D+t Burgers, 2D Helmholtz, one implicit 3D heat step,
+# 2D steady incompressible NS (the paper's worked ldc_2d example, Sec. 2.1) and
+# one backward-Euler step of 3D Taylor-Green NS.
+CONFIGS: Dict[str, Config] = {
+    "burgers_1dt": Config("burgers_1dt", BURGERS_1DT, (128, 256),
+                          Coeffs(nu=0.01 / math.pi),
+                          "1D viscous Burgers, space-time grid nt=128 x nx=256, t in [0,1], x in [-1,1]"),
+    "helmholtz_2d": Config("helmholtz_2d", HELMHOLTZ_2D, (1024, 1024),
+                           Coeffs(k=4.0 * math.pi),
+                           "2D Helmholtz 1024^2 on [0,1]^2, k=4pi, 5-point Laplacian"),
+    "heat_3d": Config("heat_3d", HEAT_3D_BE, (256, 256, 256),
+                      Coeffs(dt=1e-3, alpha=0.1),
+                      "3D heat, one implicit step, 256^3 on [0,1]^3, dt=1e-3, alpha=0.1"),
+    "ns_2d": Config("ns_2d", NS_2D_STEADY, (2048, 2048),
+                    Coeffs(nu=0.01),
+                    "2D steady incompressible NS (u,v,p), 2048^2 on [0,1]^2, nu=0.01"),
+    "ns_3d_tgv": Config("ns_3d_tgv", NS_3D_BE, (256, 256, 256),
+                        Coeffs(nu=0.01, dt=1e-2),
+                        "3D Taylor-Green NS (u,v,w,p), one backward-Euler step, 256^3 on [0,2pi)^3, nu=0.01, dt=1e-2"),
+}
+
+CONFIG_ORDER = ("burgers_1dt", "helmholtz_2d", "heat_3d", "ns_2d", "ns_3d_tgv")
+
+
+def spacing(cfg_name: str, shape: Sequence[int]) -> Tuple[float, ...]:
+    """Grid spacing per array axis for a config at a given shape.
+
+    Burgers: axis 0 is t on [0,1], axis 1 is x on [-1,1], endpoint-inclusive.
+    Helmholtz, heat, 2D NS: endpoint-inclusive nodes on [0,1] per axis.
+    3D TGV: periodic sampling x_i = 2*pi*i/n on [0,2pi).
+    """
+    if cfg_name == "burgers_1dt":
+        return (1.0 / (shape[0] - 1), 2.0 / (shape[1] - 1))
+    if cfg_name in ("helmholtz_2d", "heat_3d", "ns_2d"):
+        return tuple(1.0 / (s - 1) for s in shape)
+    if cfg_name == "ns_3d_tgv":
+        return tuple(2.0 * math.pi / s for s in shape)
+    raise KeyError(cfg_name)
+
+
+def _axes(cfg_name: str, shape: Sequence[int]) -> List[np.ndarray]:
+    """1-D node coordinates per axis (float64)."""
+    h = spacing(cfg_name, shape)
+    if cfg_name == "burgers_1dt":
+        return [np.arange(shape[0]) * h[0], -1.0 + np.arange(shape[1]) * h[1]]
+    return [np.arange(s) * hh for s, hh in zip(shape, h)]
+
+
+def _mesh(coords: List[np.ndarray]) -> List[np.ndarray]:
+    return np.meshgrid(*coords, indexing="ij", sparse=True)
+
+
+def _fourier_sum(rng, X, n_modes, kmax, trig_choice=False):
+    """sum over modes of (a/|kappa|) * trig(2 pi kappa.x + phi), kappa in {1..kmax}^d."""
+    d = len(X)
+    out = np.zeros(np.broadcast_shapes(*[x.shape for x in X]), dtype=np.float64)
+    for _ in range(n_modes):
+        kap = rng.integers(1, kmax + 1, size=d)
+        a = rng.standard_normal()
+        phi = rng.uniform(0.0, 2.0 * math.pi)
+        use_cos = bool(rng.integers(0, 2)) if trig_choice else False
+        arg = sum(2.0 * math.pi * float(kap[i]) * X[i] for i in range(d)) + phi
+        out += (a / float(np.linalg.norm(kap))) * (np.cos(arg) if use_cos else np.sin(arg))
+    return out
+
+
+def _f32(a: np.ndarray) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def make(cfg_name: str, seed: int = 42, shape: Optional[Sequence[int]] = None) -> Workload:
+    """Seeded synthetic inputs for one config (full size unless ``shape`` is given)."""
+    cfg = CONFIGS[cfg_name]
+    shape = tuple(int(s) for s in (shape if shape is not None else cfg.shape))
+    if len(shape) != OPS[cfg.op].ndim:
+        raise ValueError(f"{cfg_name}: shape {shape} has wrong rank")
+    rng = np.random.default_rng(seed)
+    X = _mesh(_axes(cfg_name, shape))
+    h = spacing(cfg_name, shape)
+    noise = lambda: 0.01 * rng.standard_normal(shape)  # N(0, 0.01^2): std 0.01
+
+    if cfg_name == "burgers_1dt":
+        t, x = X
+        u = np.zeros(shape)
+        for k in range(1, 9):
+            a = rng.standard_normal()
+            phi, psi = rng.uniform(0.0, 2.0 * math.pi, size=2)
+            m = int(rng.integers(0, 4))
+            u = u + (a / k) * np.sin(math.pi * k * x + phi) * np.cos(math.pi * m * t + psi)
+        u = u + noise()
+        fields, consts = [_f32(u)], []
+    elif cfg_name == "helmholtz_2d":
+        u = _fourier_sum(rng, X, 16, 8, trig_choice=True) + noise()
+        f = _fourier_sum(rng, X, 16, 8, trig_choice=True) + noise()
+        fields, consts = [_f32(u)], [_f32(f)]
+    elif cfg_name == "heat_3d":
+        u0 = _fourier_sum(rng, X, 8, 4)
+        u = u0 + noise()
+        fields, consts = [_f32(u)], [_f32(u0)]
+    elif cfg_name == "ns_2d":
+        # streamfunction psi = sum (a/|kappa|) sin(2 pi kappa.x + phi);
+        # u = d psi / d y (array axis 1), v = -d psi / d x (array axis 0), analytically.
+        x, y = X
+        u = np.zeros(shape)
+        v = np.zeros(shape)
+        for _ in range(16):
+            kap = rng.integers(1, 9, size=2)
+            a = rng.standard_normal()
+            phi = rng.uniform(0.0, 2.0 * math.pi)
+            amp = a / float(np.linalg.norm(kap))
+            c = np.cos(2.0 * math.pi * (kap[0] * x + kap[1] * y) + phi)
+            u = u + amp * 2.0 * math.pi * kap[1] * c
+            v = v - amp * 2.0 * math.pi * kap[0] * c
+        p = np.zeros(shape)
+        for _ in range(8):
+            kap = rng.integers(1, 9, size=2)
+            b = rng.standard_normal()
+            phi = rng.uniform(0.0, 2.0 * math.pi)
+            p = p + b * np.sin(2.0 * math.pi * (kap[0] * x + kap[1] * y) + phi)
+        fields, consts = [_f32(u), _f32(v), _f32(p)], []
+    elif cfg_name == "ns_3d_tgv":
+        x, y, z = X
+        u_ic = np.sin(x) * np.cos(y) * np.cos(z)
+        v_ic = -np.cos(x) * np.sin(y) * np.cos(z)
+        w_ic = np.zeros(shape)
+        p_ic = (np.cos(2.0 * x) + np.cos(2.0 * y)) * (np.cos(2.0 * z) + 2.0) / 16.0
+        u_ic = np.broadcast_to(u_ic, shape)
+        v_ic = np.broadcast_to(v_ic, shape)
+        p_ic = np.broadcast_to(p_ic, shape)
+        fields = [_f32(u_ic + noise()), _f32(v_ic + noise()), _f32(w_ic + noise()),
+                  _f32(p_ic + noise())]
+        consts = [_f32(u_ic), _f32(v_ic), _f32(w_ic)]
+    else:  # pragma: no cover
+        raise KeyError(cfg_name)
+
+    return Workload(cfg_name, cfg.op, shape, h, cfg.coeffs, fields, consts)
+
+
+def normal_fields(op: int, shape: Sequence[int], seed: int,
+                  h: Optional[Sequence[float]] = None,
+                  coeffs: Optional[Coeffs] = None) -> Workload:
+    """Standard-normal fields for every input (the paper's verification inputs,
+    App. A.7: N(0,1) samples, seeds 42-46)."""
+    spec = OPS[op]
+    shape = tuple(int(s) for s in shape)
+    rng = np.random.default_rng(seed)
+    fields = [_f32(rng.standard_normal(shape)) for _ in spec.fields]
+    consts = [_f32(rng.standard_normal(shape)) for _ in spec.consts]
+    if h is None:
+        h = tuple(1.0 / (s - 1) for s in shape)
+    if coeffs is None:
+        coeffs = {BURGERS_1DT: Coeffs(nu=0.01 / math.pi), HELMHOLTZ_2D: Coeffs(k=4 * math.pi),
+                  HEAT_3D_BE: Coeffs(dt=1e-3, alpha=0.1), NS_2D_STEADY: Coeffs(nu=0.01),
+                  NS_3D_BE: Coeffs(nu=0.01, dt=1e-2)}[op]
+    return Workload(f"normal_{OP_NAMES[op]}", op, shape, tuple(float(x) for x in h), coeffs,
+                    fields, consts)
