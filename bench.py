@@ -1,0 +1,202 @@
+"""Throughput of the differentiable FD residual operator on one MI355X.
+
+One step = the whole hot path on one batch of resident synthetic input:
+fpde_residual_fwd (fused stencil + loss) -> fpde_residual_bwd (interior
+adjoint) -> fpde_bc_correct (boundary shell), queued on one stream.
+
+Default workload: 3D Taylor-Green NS, one backward-Euler step, 256^3, 4 fields
+(u, v, w, p) + 3 previous velocities.  Prints ONE JSON line.
+
+Byte model (each input read once per pass, each output written once):
+  fwd reads every field and const (the loss write is 8 bytes); bwd + bc read
+  them again and write one gradient per field, so one step moves
+  (2 (NF + NC) + NF) * 4 bytes per grid node (72 B/node for the 3D NS case).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "grid-points/s and achieved HBM GB/s (% of peak) for residual fwd+bwd"
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--config", default="ns_3d_tgv")
+    p.add_argument("--seed", type=int, default=42)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-planes", type=int, default=0,
+                   help="planes of the oracle sample along axis 0 (0: sized automatically)")
+    return p.parse_args()
+
+
+def byte_model(wl):
+    nf, nc = len(wl.spec.fields), len(wl.spec.consts)
+    N, M = wl.n_points, wl.n_residual_points
+    return {
+        "step": (2 * (nf + nc) + nf) * 4 * N + 8,
+        "fwd": (nf + nc) * 4 * N + 8,
+        "bwd": (nf + nc) * 4 * N + nf * 4 * M,
+        "per_node": (2 * (nf + nc) + nf) * 4,
+    }
+
+
+def copy_gbps(torch, nbytes=1 << 30, reps=20):
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    b.synchronize()
+    s = a.elapsed_time(b) / 1e3 / reps
+    del src, dst
+    return 2 * nbytes / s / 1e9
+
+
+def cpu_baseline(W, wl_full, cfg, seed, planes):
+    """The oracle (single thread, float64) on a slab of the same workload."""
+    import numpy as np  # noqa: PLC0415
+    import oracle  # noqa: PLC0415  (CPU baseline leg only)
+    shape = wl_full.shape
+    if planes <= 0:
+        # about 10-30 s of oracle work on the host: size the slab by node count
+        per_plane = int(np.prod(shape[1:]))
+        target = {2: 4_000_000, 3: 8_000_000}[len(shape)]
+        planes = max(3, min(shape[0], target // per_plane))
+    sl = (slice(0, planes),) + tuple(slice(None) for _ in shape[1:])
+    fields = [np.ascontiguousarray(f[sl], dtype=np.float64) for f in wl_full.fields]
+    consts = [np.ascontiguousarray(c[sl], dtype=np.float64) for c in wl_full.consts]
+    sshape = fields[0].shape
+    t0 = time.perf_counter()
+    oracle.loss(wl_full.op, sshape, wl_full.h, wl_full.coeffs, fields, consts)
+    oracle.grad(wl_full.op, sshape, wl_full.h, wl_full.coeffs, fields, consts, dloss=1.0)
+    dt = time.perf_counter() - t0
+    npts = int(np.prod(sshape))
+    return {"value": npts / dt, "unit": "grid-points/s", "cores": 1, "kind": "oracle",
+            "sample": f"{cfg} seed {seed}: first {planes} planes along axis 0 "
+                      f"({'x'.join(map(str, sshape))} = {npts} nodes), loss + full gradient, "
+                      f"float64, single thread, {dt:.2f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the operator's multi-GPU slab decomposition is a design, not built)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch  # noqa: PLC0415
+
+    from paper_2607_18020_amd import binding as B  # noqa: PLC0415
+    from paper_2607_18020_amd import workloads as W  # noqa: PLC0415
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    B.lib()
+    cfg = args.config
+    wl = W.make(cfg, seed=args.seed)
+    dev = torch.device("cuda:0")
+    fields = [torch.from_numpy(f).to(dev) for f in wl.fields]
+    consts = [torch.from_numpy(c).to(dev) for c in wl.consts]
+    grads = [torch.empty_like(f) for f in fields]
+    loss = torch.empty((), dtype=torch.float64, device=dev)
+    dl = torch.ones((), dtype=torch.float64, device=dev)
+    stream = torch.cuda.current_stream()
+    op, h, co = wl.op, wl.h, wl.coeffs
+
+    def fwd():
+        B.fpde_residual_fwd(op, fields, consts, h, co, loss=loss, stream=stream)
+
+    def bwd():
+        B.fpde_residual_bwd(op, fields, consts, h, co, dl, grads=grads, stream=stream)
+
+    def bc():
+        B.fpde_bc_correct(op, fields, consts, h, co, dl, grads=grads, stream=stream)
+
+    for _ in range(args.warmup):
+        fwd(), bwd(), bc()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for k in range(K):
+        e = ev[k]
+        e[0].record(stream)
+        fwd()
+        e[1].record(stream)
+        bwd()
+        e[2].record(stream)
+        bc()
+        e[3].record(stream)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total_s = t_start.elapsed_time(t_end) / 1e3
+    per = {n: sum(ev[k][i].elapsed_time(ev[k][i + 1]) for k in range(K)) / K * 1e3
+           for i, n in enumerate(("fwd", "bwd", "bc"))}  # microseconds
+    L = float(loss.item())
+    if not (L == L) or L <= 0:
+        raise RuntimeError(f"bad loss {L}")
+
+    bm = byte_model(wl)
+    N = wl.n_points
+    ms = total_s / K * 1e3
+    gbps = bm["step"] * K / total_s / 1e9
+    dom = max(("fwd", "bwd"), key=lambda n: per[n])
+    achieved = bm[dom] / (per[dom] * 1e-6) / 1e9
+    roofline = {"bound": "hbm", "kernel": f"{dom} ({cfg})", "achieved": round(achieved, 1),
+                "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                "traffic": None,
+                "algorithmic_bytes_per_launch": bm[dom], "avg_launch_us": round(per[dom], 2)}
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(W, wl, cfg, args.seed, args.cpu_planes)
+    out = {
+        "metric": METRIC,
+        "value": N * K / total_s,
+        "unit": "grid-points/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg}: {W.CONFIGS[cfg].description}",
+                   "grid": list(wl.shape), "nodes": N,
+                   "fields": list(wl.spec.fields), "consts": list(wl.spec.consts),
+                   "seed": args.seed, "step": "fwd+loss, bwd, bc on one stream"},
+        "hbm_gbps": round(gbps, 1),
+        "hbm_frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4),
+        "bytes_per_step": bm["step"],
+        "kernel_us": {k: round(v, 2) for k, v in per.items()},
+        "copy_gbps": round(copy_gbps(torch), 1),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

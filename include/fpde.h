@@ -1,0 +1,150 @@
+/*
+ * fpde.h -- C ABI of libfpde: a differentiable finite-difference PDE residual
+ * operator for AMD Instinct MI355X (gfx950).
+ *
+ * The operator follows the three-part design of FlashPDE (Sec. 2): a fused
+ * forward stencil (Sec. 2.1), a discrete analytic-adjoint backward
+ * (Sec. 2.2, App. A.3) and a boundary-gradient correction (Sec. 2.3, App. A.5).
+ * Here the forward also reduces the mean-squared residual loss, and the
+ * backward recomputes the residuals it needs instead of reading an upstream
+ * sensitivity tensor, so one call sequence is
+ *     fpde_residual_fwd -> fpde_residual_bwd + fpde_bc_correct.
+ *
+ * Notation (used by every entry point):
+ *   - arrays are dense C-contiguous float32, shape n[0..ndim-1], last axis
+ *     fastest; h[a] is the node spacing along array axis a;
+ *   - the residual set is Omega = { nodes with 1 <= i_a <= n_a - 2 on every
+ *     axis }, M = prod_a (n_a - 2);
+ *   - D1_a q(m) = (q(m+e_a) - q(m-e_a)) / (2 h_a),
+ *     D2_a q(m) = (q(m+e_a) - 2 q(m) + q(m-e_a)) / h_a^2     (App. A.3);
+ *   - loss L = sum over equations b of (1/M) sum_{m in Omega} R_b(m)^2;
+ *   - the gradient written by bwd + bc is dloss * dL/dq for every node of
+ *     every differentiated field q (boundary nodes included).
+ *
+ * Operators (velocity component b lives on array axis b; pressure last):
+ *   FPDE_BURGERS_1DT  (ndim 2; axis 0 = t, axis 1 = x)   fields {u}        consts {}
+ *       R = D1_0 u + u D1_1 u - nu D2_1 u
+ *   FPDE_HELMHOLTZ_2D (ndim 2)                            fields {u}        consts {f}
+ *       R = D2_0 u + D2_1 u + k^2 u - f
+ *   FPDE_HEAT_3D_BE   (ndim 3; one implicit step)         fields {u}        consts {u0}
+ *       R = (u - u0)/dt - alpha (D2_0 + D2_1 + D2_2) u
+ *   FPDE_NS_2D_STEADY (ndim 2; the worked example of Sec. 2.1)
+ *                                                         fields {u, v, p}  consts {}
+ *       R_b = sum_a c_a D1_a c_b + D1_b p - nu sum_a D2_a c_b   (b = 0,1; c = (u,v))
+ *       R_div = sum_a D1_a c_a
+ *   FPDE_NS_3D_BE     (ndim 3; one backward-Euler step)   fields {u, v, w, p}
+ *                                                         consts {u_prev, v_prev, w_prev}
+ *       R_b = (c_b - c_b_prev)/dt + sum_a c_a D1_a c_b + D1_b p - nu sum_a D2_a c_b
+ *       R_div = sum_a D1_a c_a
+ *
+ * Common argument rules:
+ *   - `fields`, `consts`, `residual_out`, `grads` are HOST arrays holding
+ *     DEVICE pointers, one per array in the order listed above (`consts` may be
+ *     NULL for ops without consts).  Every device array is n[0]*...*n[ndim-1]
+ *     floats, 4-byte aligned, allocated on the current HIP device.
+ *   - The caller owns every buffer and keeps it alive until the work queued on
+ *     `stream` has completed.  The library allocates nothing and keeps no
+ *     global state; calls are reentrant.
+ *   - `stream` is a hipStream_t (NULL: the default stream).  All GPU work is
+ *     queued asynchronously on it; the host never synchronises.
+ *   - Arguments are validated on the host before anything is queued; on any
+ *     error the call returns a negative fpde_status and queues nothing.
+ *   - Output arrays must not overlap any input array (FPDE_ERR_ARG).
+ *   - NaN/Inf in the data are not checked; they propagate.
+ */
+#ifndef FPDE_H
+#define FPDE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum fpde_status {
+    FPDE_OK = 0,
+    FPDE_ERR_ARG = -1,         /* null pointer, unknown op, overlapping output */
+    FPDE_ERR_SHAPE = -2,       /* ndim differs from the op's, n_a < 3, or a size too large */
+    FPDE_ERR_SPACING = -3,     /* h_a <= 0 or not finite */
+    FPDE_ERR_COEFF = -4,       /* non-finite coefficient, or dt <= 0 for a time-stepping op */
+    FPDE_ERR_ALIGN = -5,       /* a device pointer not 4-byte aligned */
+    FPDE_ERR_HIP = -6,         /* the HIP runtime reported an error while queueing */
+    FPDE_ERR_UNSUPPORTED = -7  /* valid request this build does not implement (bc_mode != 0) */
+} fpde_status;
+
+typedef enum fpde_op {
+    FPDE_BURGERS_1DT = 1,
+    FPDE_HELMHOLTZ_2D = 2,
+    FPDE_HEAT_3D_BE = 3,
+    FPDE_NS_2D_STEADY = 4,
+    FPDE_NS_3D_BE = 5
+} fpde_op;
+
+/* Grid: rank, residual-set mode, sizes per array axis, spacings per axis.
+ * bc_mode 0 is the residual set Omega above; other values are rejected with
+ * FPDE_ERR_UNSUPPORTED.  Entries past ndim are ignored.
+ * Limits: every n_a >= 3; n[ndim-2]*n[ndim-1] < 2^31 and each n_a < 2^31. */
+typedef struct fpde_grid {
+    int32_t ndim;
+    int32_t bc_mode;
+    int64_t n[3];
+    double h[3];
+} fpde_grid;
+
+/* PDE coefficients in float64; an op ignores the members it does not use.
+ * The library derives 1/(2h), 1/h^2, nu/h^2, ... in float64 and rounds them
+ * once to float32 for the kernels. */
+typedef struct fpde_coeffs {
+    double nu;     /* viscosity (Burgers, NS) */
+    double k;      /* wave number (Helmholtz) */
+    double dt;     /* time step (heat, NS 3D); must be > 0 for those ops */
+    double alpha;  /* diffusivity (heat) */
+} fpde_coeffs;
+
+/* Static description of an op.  Any output pointer may be NULL.
+ * Returns FPDE_OK or FPDE_ERR_ARG (unknown op). */
+int fpde_op_info(int op, int* ndim, int* n_fields, int* n_consts, int* n_residuals);
+
+/* Fused forward stencil + mean-squared residual loss (Sec. 2.1).
+ *   loss          device pointer to one double; OVERWRITTEN with L (not accumulated).
+ *   residual_out  NULL, or a host array of n_residuals device pointers: R_b is
+ *                 written on Omega only; nodes off Omega are left untouched.
+ * Queues 2 kernels: a one-element fill that zeroes *loss, then the stencil
+ * kernel (one float64 atomic add per workgroup onto *loss). */
+int fpde_residual_fwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+                      const float* const* fields, const float* const* consts,
+                      float* const* residual_out, double* loss, void* stream);
+
+/* Interior analytic-adjoint backward, gather form (Sec. 2.2, App. A.3).
+ *   dloss  device pointer to one double: the upstream derivative of the
+ *          consumer's objective with respect to L (1.0 for L itself).
+ *   grads  host array of n_fields device pointers; OVERWRITTEN on the interior
+ *          nodes [1, n_a-2] of every axis with dloss * dL/dq.  Boundary-shell
+ *          nodes are not touched (fpde_bc_correct writes them).
+ * The residuals are recomputed from the fields; no sensitivity tensor is read.
+ * Queues 1 kernel; no atomics. */
+int fpde_residual_bwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+                      const float* const* fields, const float* const* consts,
+                      const double* dloss, float* const* grads, void* stream);
+
+/* Boundary-gradient correction (Sec. 2.3, App. A.5): a 1-D launch over the
+ * boundary shell (nodes with some i_a in {0, n_a-1}).  A node with exactly one
+ * boundary coordinate receives the single term from its inward neighbour's
+ * residuals; edge and corner nodes, which touch no residual node, receive 0.
+ * Arguments as fpde_residual_bwd; OVERWRITES grads on the shell only, so
+ * bwd and bc together write every node exactly once, in either order.
+ * Queues 1 kernel. */
+int fpde_bc_correct(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+                    const float* const* fields, const float* const* consts,
+                    const double* dloss, float* const* grads, void* stream);
+
+/* Static string naming a status code (never NULL). */
+const char* fpde_status_string(int status);
+
+/* Static version string of the library. */
+const char* fpde_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FPDE_H */

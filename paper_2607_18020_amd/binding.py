@@ -1,0 +1,190 @@
+"""ctypes binding of libfpde (include/fpde.h): argument marshalling only.
+
+Every computation runs in the library's HIP kernels; this module turns torch
+tensors into device pointers, grid/coefficient structs and a stream handle,
+calls the C entry point and raises on a non-zero status.  There is no CPU
+fallback: importing fails loudly when libfpde.so has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfpde.so")
+
+FPDE_OK = 0
+STATUS_NAMES = {0: "FPDE_OK", -1: "FPDE_ERR_ARG", -2: "FPDE_ERR_SHAPE", -3: "FPDE_ERR_SPACING",
+                -4: "FPDE_ERR_COEFF", -5: "FPDE_ERR_ALIGN", -6: "FPDE_ERR_HIP",
+                -7: "FPDE_ERR_UNSUPPORTED"}
+EXPORTED = ("fpde_op_info", "fpde_residual_fwd", "fpde_residual_bwd", "fpde_bc_correct",
+            "fpde_status_string", "fpde_version")
+
+
+class FpdeGrid(ctypes.Structure):
+    _fields_ = [("ndim", ctypes.c_int32), ("bc_mode", ctypes.c_int32),
+                ("n", ctypes.c_int64 * 3), ("h", ctypes.c_double * 3)]
+
+
+class FpdeCoeffs(ctypes.Structure):
+    _fields_ = [("nu", ctypes.c_double), ("k", ctypes.c_double), ("dt", ctypes.c_double),
+                ("alpha", ctypes.c_double)]
+
+
+class FpdeError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {_load().fpde_status_string(status).decode()} ({status})")
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2607_18020_amd.csrc.build`")
+        lib = ctypes.CDLL(LIB_PATH)
+        vp = ctypes.c_void_p
+        pp = ctypes.POINTER(ctypes.c_void_p)
+        gp, cp = ctypes.POINTER(FpdeGrid), ctypes.POINTER(FpdeCoeffs)
+        lib.fpde_op_info.argtypes = [ctypes.c_int] + [ctypes.POINTER(ctypes.c_int)] * 4
+        lib.fpde_residual_fwd.argtypes = [ctypes.c_int, gp, cp, pp, pp, pp, vp, vp]
+        lib.fpde_residual_bwd.argtypes = [ctypes.c_int, gp, cp, pp, pp, vp, pp, vp]
+        lib.fpde_bc_correct.argtypes = [ctypes.c_int, gp, cp, pp, pp, vp, pp, vp]
+        for name in ("fpde_op_info", "fpde_residual_fwd", "fpde_residual_bwd", "fpde_bc_correct"):
+            getattr(lib, name).restype = ctypes.c_int
+        lib.fpde_status_string.argtypes = [ctypes.c_int]
+        lib.fpde_status_string.restype = ctypes.c_char_p
+        lib.fpde_version.argtypes = []
+        lib.fpde_version.restype = ctypes.c_char_p
+        _lib = lib
+    return _lib
+
+
+def lib():
+    """The loaded ctypes library (raises ImportError if it is not built)."""
+    return _load()
+
+
+def op_info(op: int):
+    v = [ctypes.c_int() for _ in range(4)]
+    st = _load().fpde_op_info(int(op), *[ctypes.byref(x) for x in v])
+    if st != FPDE_OK:
+        raise FpdeError(st, "fpde_op_info")
+    return tuple(x.value for x in v)  # ndim, n_fields, n_consts, n_residuals
+
+
+def make_grid(shape: Sequence[int], h: Sequence[float], bc_mode: int = 0) -> FpdeGrid:
+    g = FpdeGrid()
+    g.ndim = len(shape)
+    g.bc_mode = int(bc_mode)
+    for a, (n, hh) in enumerate(zip(shape, h)):
+        g.n[a] = int(n)
+        g.h[a] = float(hh)
+    return g
+
+
+def make_coeffs(c) -> FpdeCoeffs:
+    return FpdeCoeffs(float(getattr(c, "nu", 0.0)), float(getattr(c, "k", 0.0)),
+                      float(getattr(c, "dt", 1.0)), float(getattr(c, "alpha", 0.0)))
+
+
+def _ptr_array(tensors):
+    arr = (ctypes.c_void_p * max(1, len(tensors)))()
+    for i, t in enumerate(tensors):
+        arr[i] = t.data_ptr()
+    return arr
+
+
+def _check_tensors(tensors, shape, what):
+    for t in tensors:
+        if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != torch.float32 \
+                or not t.is_contiguous() or tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{what}: need contiguous float32 CUDA tensors of shape {tuple(shape)}")
+
+
+def _stream(stream) -> int:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def fpde_residual_fwd(op: int, fields, consts, h, coeffs, *, residual_out=None,
+                      loss: Optional[torch.Tensor] = None, bc_mode: int = 0, stream=None):
+    """Queue the fused forward stencil + loss; returns the float64 loss tensor."""
+    shape = tuple(fields[0].shape)
+    _check_tensors(list(fields) + list(consts), shape, "fpde_residual_fwd")
+    dev = fields[0].device
+    if loss is None:
+        loss = torch.empty((), dtype=torch.float64, device=dev)
+    res_arr = None
+    if residual_out is not None:
+        _check_tensors(residual_out, shape, "fpde_residual_fwd residual_out")
+        res_arr = _ptr_array(residual_out)
+    g, c = make_grid(shape, h, bc_mode), make_coeffs(coeffs)
+    st = _load().fpde_residual_fwd(int(op), ctypes.byref(g), ctypes.byref(c), _ptr_array(fields),
+                                   _ptr_array(consts) if len(consts) else None, res_arr,
+                                   loss.data_ptr(), _stream(stream))
+    if st != FPDE_OK:
+        raise FpdeError(st, "fpde_residual_fwd")
+    return loss
+
+
+def _grad_call(fn, name, op, fields, consts, h, coeffs, dloss, grads, bc_mode, stream):
+    shape = tuple(fields[0].shape)
+    _check_tensors(list(fields) + list(consts), shape, name)
+    if grads is None:
+        grads = [torch.empty_like(f) for f in fields]
+    _check_tensors(grads, shape, name + " grads")
+    if not isinstance(dloss, torch.Tensor):
+        dloss = torch.tensor(float(dloss), dtype=torch.float64, device=fields[0].device)
+    if dloss.dtype != torch.float64 or not dloss.is_cuda or dloss.numel() != 1:
+        raise ValueError(f"{name}: dloss must be a one-element float64 CUDA tensor")
+    g, c = make_grid(shape, h, bc_mode), make_coeffs(coeffs)
+    st = fn(int(op), ctypes.byref(g), ctypes.byref(c), _ptr_array(fields),
+            _ptr_array(consts) if len(consts) else None, dloss.data_ptr(), _ptr_array(grads),
+            _stream(stream))
+    if st != FPDE_OK:
+        raise FpdeError(st, name)
+    return grads
+
+
+def fpde_residual_bwd(op: int, fields, consts, h, coeffs, dloss, *, grads=None, bc_mode: int = 0,
+                      stream=None):
+    """Queue the interior gather-form adjoint; returns the grads list."""
+    return _grad_call(_load().fpde_residual_bwd, "fpde_residual_bwd", op, fields, consts, h,
+                      coeffs, dloss, grads, bc_mode, stream)
+
+
+def fpde_bc_correct(op: int, fields, consts, h, coeffs, dloss, *, grads=None, bc_mode: int = 0,
+                    stream=None):
+    """Queue the boundary-shell correction; returns the grads list."""
+    return _grad_call(_load().fpde_bc_correct, "fpde_bc_correct", op, fields, consts, h,
+                      coeffs, dloss, grads, bc_mode, stream)
+
+
+class ResidualLoss(torch.autograd.Function):
+    """Drop-in differentiable loss op: forward = fused stencil + MSE loss,
+    backward = interior adjoint + boundary correction with dloss = grad_output.
+
+    Usage: ``loss = ResidualLoss.apply(op, h, coeffs, consts, *fields)``.
+    """
+
+    @staticmethod
+    def forward(ctx, op, h, coeffs, consts, *fields):
+        fields = [f.contiguous() for f in fields]
+        ctx.op, ctx.h, ctx.coeffs, ctx.consts = op, h, coeffs, consts
+        ctx.save_for_backward(*fields)
+        return fpde_residual_fwd(op, fields, consts, h, coeffs)
+
+    @staticmethod
+    def backward(ctx, gout):
+        fields = list(ctx.saved_tensors)
+        dl = gout.detach().to(torch.float64).reshape(()).contiguous()
+        grads = fpde_residual_bwd(ctx.op, fields, ctx.consts, ctx.h, ctx.coeffs, dl)
+        fpde_bc_correct(ctx.op, fields, ctx.consts, ctx.h, ctx.coeffs, dl, grads=grads)
+        return (None, None, None, None, *grads)

@@ -1,0 +1,321 @@
+// fpde.hip -- host side of libfpde: argument validation, launch geometry and
+// the exported C entry points declared in include/fpde.h.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "fpde.h"
+#include "fpde_engine.hpp"
+
+namespace fpde {
+namespace {
+
+struct OpDesc {
+    int ndim, nf, nc, nr;
+};
+
+bool op_desc(int op, OpDesc* d) {
+    switch (op) {
+    case FPDE_BURGERS_1DT: *d = {2, 1, 0, 1}; return true;
+    case FPDE_HELMHOLTZ_2D: *d = {2, 1, 1, 1}; return true;
+    case FPDE_HEAT_3D_BE: *d = {3, 1, 1, 1}; return true;
+    case FPDE_NS_2D_STEADY: *d = {2, 3, 0, 3}; return true;
+    case FPDE_NS_3D_BE: *d = {3, 4, 3, 4}; return true;
+    default: return false;
+    }
+}
+
+// Launch geometry.  3-D: 64 x 8 column tiles (512 threads, one wavefront per
+// x-row of 64 nodes).  2-D: 256-node row segments.  Chunks of planes along axis 0
+// are sized so that a launch has about kTargetBlocks workgroups.
+constexpr int kTX3 = 64, kTY3 = 8;
+constexpr int kTX2 = 256;
+constexpr int kTargetBlocks3 = 512;
+constexpr int kTargetBlocks2 = 1024;
+
+struct Req {
+    int op;
+    OpDesc d;
+    Dims dims;
+    KCoef K;
+    double inv_M, two_over_M;
+    long long N, M, shell;
+    Ptrs P;
+    hipStream_t stream;
+};
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+    const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+    return x < y + nb && y < x + na;
+}
+
+bool finite_pos(double v) { return isfinite(v) && v > 0.0; }
+
+// Validates everything except the outputs; fills req.
+int validate_common(int op, const fpde_grid* g, const fpde_coeffs* c, const float* const* fields,
+                    const float* const* consts, Req* r) {
+    if (!op_desc(op, &r->d)) return FPDE_ERR_ARG;
+    if (!g || !c || !fields) return FPDE_ERR_ARG;
+    if (r->d.nc > 0 && !consts) return FPDE_ERR_ARG;
+    for (int f = 0; f < r->d.nf; ++f)
+        if (!fields[f]) return FPDE_ERR_ARG;
+    for (int j = 0; j < r->d.nc; ++j)
+        if (!consts[j]) return FPDE_ERR_ARG;
+    if (g->bc_mode != 0 && g->bc_mode != 1) return FPDE_ERR_ARG;
+    if (g->ndim != r->d.ndim) return FPDE_ERR_SHAPE;
+    const int D = r->d.ndim;
+    long long N = 1, M = 1;
+    for (int a = 0; a < D; ++a) {
+        if (g->n[a] < 3 || g->n[a] >= (1LL << 31)) return FPDE_ERR_SHAPE;
+        if (N > (1LL << 62) / g->n[a]) return FPDE_ERR_SHAPE;
+        N *= g->n[a];
+        M *= g->n[a] - 2;
+    }
+    if (g->n[D - 2] * g->n[D - 1] >= (1LL << 31)) return FPDE_ERR_SHAPE;
+    for (int a = 0; a < D; ++a)
+        if (!finite_pos(g->h[a])) return FPDE_ERR_SPACING;
+    if (!isfinite(c->nu) || !isfinite(c->k) || !isfinite(c->dt) || !isfinite(c->alpha))
+        return FPDE_ERR_COEFF;
+    if ((op == FPDE_HEAT_3D_BE || op == FPDE_NS_3D_BE) && !(c->dt > 0.0)) return FPDE_ERR_COEFF;
+
+    // float32 kernel coefficients, derived in float64
+    KCoef K;
+    memset(&K, 0, sizeof K);
+    for (int a = 0; a < D; ++a) {
+        const double h = g->h[a];
+        K.i2h[a] = (float)(1.0 / (2.0 * h));
+        K.ih2[a] = (float)(1.0 / (h * h));
+        if (!isfinite(K.i2h[a]) || !isfinite(K.ih2[a]) || K.ih2[a] == 0.f) return FPDE_ERR_SPACING;
+    }
+    K.nu = (float)c->nu;
+    K.k2 = (float)(c->k * c->k);
+    K.inv_dt = (op == FPDE_HEAT_3D_BE || op == FPDE_NS_3D_BE) ? (float)(1.0 / c->dt) : 0.f;
+    K.alpha = (float)c->alpha;
+    if (!isfinite(K.nu) || !isfinite(K.k2) || !isfinite(K.inv_dt) || !isfinite(K.alpha))
+        return FPDE_ERR_COEFF;
+
+    for (int f = 0; f < r->d.nf; ++f)
+        if ((uintptr_t)fields[f] & 3u) return FPDE_ERR_ALIGN;
+    for (int j = 0; j < r->d.nc; ++j)
+        if ((uintptr_t)consts[j] & 3u) return FPDE_ERR_ALIGN;
+    if (g->bc_mode == 1) return FPDE_ERR_UNSUPPORTED;
+
+    r->op = op;
+    r->K = K;
+    r->N = N;
+    r->M = M;
+    r->inv_M = 1.0 / (double)M;
+    r->two_over_M = 2.0 / (double)M;
+    memset(&r->P, 0, sizeof r->P);
+    for (int f = 0; f < r->d.nf; ++f) r->P.f[f] = fields[f];
+    for (int j = 0; j < r->d.nc; ++j) r->P.c[j] = consts[j];
+
+    Dims& dm = r->dims;
+    if (D == 3) {
+        dm.nz = (int)g->n[0];
+        dm.ny = (int)g->n[1];
+        dm.nx = (int)g->n[2];
+        dm.tiles_x = (dm.nx + kTX3 - 1) / kTX3;
+        dm.tiles_y = (dm.ny + kTY3 - 1) / kTY3;
+        r->shell = N - M;
+    } else {
+        dm.nz = (int)g->n[0];
+        dm.ny = 1;
+        dm.nx = (int)g->n[1];
+        dm.tiles_x = (dm.nx + kTX2 - 1) / kTX2;
+        dm.tiles_y = 1;
+        r->shell = N - M;
+    }
+    const long long tiles = (long long)dm.tiles_x * dm.tiles_y;
+    const long long target = (D == 3) ? kTargetBlocks3 : kTargetBlocks2;
+    const int nplanes = dm.nz - 2;
+    long long nch = (target + tiles - 1) / tiles;
+    if (nch < 1) nch = 1;
+    if (nch > nplanes) nch = nplanes;
+    dm.zc = (int)((nplanes + nch - 1) / nch);
+    nch = (nplanes + dm.zc - 1) / dm.zc;
+    if (tiles * nch >= (1LL << 31)) return FPDE_ERR_SHAPE;
+    dm.nblocks = (int)(tiles * nch);
+    return FPDE_OK;
+}
+
+int check_outputs(const Req& r, const fpde_grid*, const float* const* fields,
+                  const float* const* consts, float* const* outs, int nout, const void* extra,
+                  size_t extra_bytes) {
+    const size_t bytes = (size_t)r.N * sizeof(float);
+    for (int o = 0; o < nout; ++o) {
+        if (!outs[o]) return FPDE_ERR_ARG;
+        if ((uintptr_t)outs[o] & 3u) return FPDE_ERR_ALIGN;
+        for (int f = 0; f < r.d.nf; ++f)
+            if (overlaps(outs[o], bytes, fields[f], bytes)) return FPDE_ERR_ARG;
+        for (int j = 0; j < r.d.nc; ++j)
+            if (overlaps(outs[o], bytes, consts[j], bytes)) return FPDE_ERR_ARG;
+        for (int p = 0; p < o; ++p)
+            if (overlaps(outs[o], bytes, outs[p], bytes)) return FPDE_ERR_ARG;
+        if (extra && overlaps(outs[o], bytes, extra, extra_bytes)) return FPDE_ERR_ARG;
+    }
+    return FPDE_OK;
+}
+
+int hip_status() {
+    const hipError_t e = hipGetLastError();
+    return e == hipSuccess ? FPDE_OK : FPDE_ERR_HIP;
+}
+
+// ---- launches, per op type
+
+template <class OP, int TX, int TY>
+int launch_fwd(const Req& r, bool store, double* loss) {
+    hipLaunchKernelGGL(fill_f64_kernel, dim3(1), dim3(1), 0, r.stream, loss, 0.0);
+    if (store)
+        hipLaunchKernelGGL((fwd_kernel<OP, TX, TY, true>), dim3(r.dims.nblocks), dim3(TX * TY), 0,
+                           r.stream, r.P, r.dims, r.K, r.inv_M, loss);
+    else
+        hipLaunchKernelGGL((fwd_kernel<OP, TX, TY, false>), dim3(r.dims.nblocks), dim3(TX * TY), 0,
+                           r.stream, r.P, r.dims, r.K, r.inv_M, loss);
+    return hip_status();
+}
+
+template <class OP, int TX, int TY>
+int launch_bwd(const Req& r, const double* dloss) {
+    hipLaunchKernelGGL((bwd_kernel<OP, TX, TY>), dim3(r.dims.nblocks), dim3(TX * TY), 0, r.stream,
+                       r.P, r.dims, r.K, dloss, r.two_over_M);
+    return hip_status();
+}
+
+template <class OP>
+int launch_bc(const Req& r, const double* dloss) {
+    long long nb = (r.shell + 255) / 256;
+    if (nb > 65535LL * 16) nb = 65535LL * 16;
+    hipLaunchKernelGGL((bc_kernel<OP>), dim3((unsigned)nb), dim3(256), 0, r.stream, r.P, r.dims,
+                       r.K, dloss, r.two_over_M, r.shell);
+    return hip_status();
+}
+
+template <class OP>
+int dispatch_fwd3(const Req& r, bool store, double* loss) {
+    return launch_fwd<OP, kTX3, kTY3>(r, store, loss);
+}
+template <class OP>
+int dispatch_fwd2(const Req& r, bool store, double* loss) {
+    return launch_fwd<OP, kTX2, 1>(r, store, loss);
+}
+
+int run_fwd(const Req& r, bool store, double* loss) {
+    switch (r.op) {
+    case FPDE_BURGERS_1DT: return dispatch_fwd2<OpBurgers>(r, store, loss);
+    case FPDE_HELMHOLTZ_2D: return dispatch_fwd2<OpHelmholtz>(r, store, loss);
+    case FPDE_HEAT_3D_BE: return dispatch_fwd3<OpHeat>(r, store, loss);
+    case FPDE_NS_2D_STEADY: return dispatch_fwd2<OpNS2>(r, store, loss);
+    case FPDE_NS_3D_BE: return dispatch_fwd3<OpNS3>(r, store, loss);
+    }
+    return FPDE_ERR_ARG;
+}
+
+int run_bwd(const Req& r, const double* dloss) {
+    switch (r.op) {
+    case FPDE_BURGERS_1DT: return launch_bwd<OpBurgers, kTX2, 1>(r, dloss);
+    case FPDE_HELMHOLTZ_2D: return launch_bwd<OpHelmholtz, kTX2, 1>(r, dloss);
+    case FPDE_HEAT_3D_BE: return launch_bwd<OpHeat, kTX3, kTY3>(r, dloss);
+    case FPDE_NS_2D_STEADY: return launch_bwd<OpNS2, kTX2, 1>(r, dloss);
+    case FPDE_NS_3D_BE: return launch_bwd<OpNS3, kTX3, kTY3>(r, dloss);
+    }
+    return FPDE_ERR_ARG;
+}
+
+int run_bc(const Req& r, const double* dloss) {
+    switch (r.op) {
+    case FPDE_BURGERS_1DT: return launch_bc<OpBurgers>(r, dloss);
+    case FPDE_HELMHOLTZ_2D: return launch_bc<OpHelmholtz>(r, dloss);
+    case FPDE_HEAT_3D_BE: return launch_bc<OpHeat>(r, dloss);
+    case FPDE_NS_2D_STEADY: return launch_bc<OpNS2>(r, dloss);
+    case FPDE_NS_3D_BE: return launch_bc<OpNS3>(r, dloss);
+    }
+    return FPDE_ERR_ARG;
+}
+
+int prepare_grad_call(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+                      const float* const* fields, const float* const* consts, const double* dloss,
+                      float* const* grads, void* stream, Req* r) {
+    int st = validate_common(op, grid, coeffs, fields, consts, r);
+    if (st != FPDE_OK) return st;
+    if (!dloss || !grads) return FPDE_ERR_ARG;
+    if ((uintptr_t)dloss & 7u) return FPDE_ERR_ALIGN;
+    st = check_outputs(*r, grid, fields, consts, grads, r->d.nf, dloss, sizeof(double));
+    if (st != FPDE_OK) return st;
+    for (int f = 0; f < r->d.nf; ++f) r->P.out[f] = grads[f];
+    r->stream = (hipStream_t)stream;
+    return FPDE_OK;
+}
+
+}  // namespace
+}  // namespace fpde
+
+using namespace fpde;
+
+extern "C" int fpde_op_info(int op, int* ndim, int* n_fields, int* n_consts, int* n_residuals) {
+    OpDesc d;
+    if (!op_desc(op, &d)) return FPDE_ERR_ARG;
+    if (ndim) *ndim = d.ndim;
+    if (n_fields) *n_fields = d.nf;
+    if (n_consts) *n_consts = d.nc;
+    if (n_residuals) *n_residuals = d.nr;
+    return FPDE_OK;
+}
+
+extern "C" int fpde_residual_fwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+                                 const float* const* fields, const float* const* consts,
+                                 float* const* residual_out, double* loss, void* stream) {
+    Req r;
+    int st = validate_common(op, grid, coeffs, fields, consts, &r);
+    if (st != FPDE_OK) return st;
+    if (!loss) return FPDE_ERR_ARG;
+    if ((uintptr_t)loss & 7u) return FPDE_ERR_ALIGN;
+    const size_t bytes = (size_t)r.N * sizeof(float);
+    for (int f = 0; f < r.d.nf; ++f)
+        if (overlaps(loss, sizeof(double), fields[f], bytes)) return FPDE_ERR_ARG;
+    for (int j = 0; j < r.d.nc; ++j)
+        if (overlaps(loss, sizeof(double), consts[j], bytes)) return FPDE_ERR_ARG;
+    if (residual_out) {
+        st = check_outputs(r, grid, fields, consts, residual_out, r.d.nr, loss, sizeof(double));
+        if (st != FPDE_OK) return st;
+        for (int b = 0; b < r.d.nr; ++b) r.P.out[b] = residual_out[b];
+    }
+    r.stream = (hipStream_t)stream;
+    return run_fwd(r, residual_out != nullptr, loss);
+}
+
+extern "C" int fpde_residual_bwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+                                 const float* const* fields, const float* const* consts,
+                                 const double* dloss, float* const* grads, void* stream) {
+    Req r;
+    const int st = prepare_grad_call(op, grid, coeffs, fields, consts, dloss, grads, stream, &r);
+    if (st != FPDE_OK) return st;
+    return run_bwd(r, dloss);
+}
+
+extern "C" int fpde_bc_correct(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+                               const float* const* fields, const float* const* consts,
+                               const double* dloss, float* const* grads, void* stream) {
+    Req r;
+    const int st = prepare_grad_call(op, grid, coeffs, fields, consts, dloss, grads, stream, &r);
+    if (st != FPDE_OK) return st;
+    return run_bc(r, dloss);
+}
+
+extern "C" const char* fpde_status_string(int status) {
+    switch (status) {
+    case FPDE_OK: return "FPDE_OK";
+    case FPDE_ERR_ARG: return "FPDE_ERR_ARG: null pointer, unknown op or overlapping output";
+    case FPDE_ERR_SHAPE: return "FPDE_ERR_SHAPE: wrong rank, n_a < 3 or size too large";
+    case FPDE_ERR_SPACING: return "FPDE_ERR_SPACING: grid spacing not positive and finite";
+    case FPDE_ERR_COEFF: return "FPDE_ERR_COEFF: non-finite coefficient or dt <= 0";
+    case FPDE_ERR_ALIGN: return "FPDE_ERR_ALIGN: misaligned device pointer";
+    case FPDE_ERR_HIP: return "FPDE_ERR_HIP: HIP runtime error while queueing work";
+    case FPDE_ERR_UNSUPPORTED: return "FPDE_ERR_UNSUPPORTED: bc_mode not implemented";
+    default: return "unknown fpde status";
+    }
+}
+
+extern "C" const char* fpde_version(void) { return "fpde 0.1 gfx950"; }

@@ -1,0 +1,200 @@
+// fpde_ops.hpp -- per-operator point arithmetic for the gfx950 kernels.
+//
+// Each operator is a struct with compile-time sizes and three device
+// functions, all in float32:
+//   residual(f, c, K, R)    R_b at one node from the 2*DIM+1-point star of every
+//                           stencil field and the point values of the consts
+//                           (the fused forward stencil, Sec. 2.1);
+//   gather(f, r, K, g)      sum over the star of node n of R_b(m) dR_b(m)/dq(n):
+//                           the transpose-Jacobian action in gather form
+//                           (Sec. 2.2; the printed dL/du of the 2D NS operator is
+//                           the NS case with DIM = 2), without the 2 dloss / M
+//                           factor that the caller applies;
+//   bc_term<AX>(f, c, K, t, g)
+//                           for a boundary-face node n = m + t e_AX whose only
+//                           residual neighbour is m: R_b(m) dR_b(m)/dq(n)
+//                           (the boundary-gradient correction, Sec. 2.3).
+// Star values are indexed by array axis: m[a] / p[a] hold q(n - e_a) / q(n + e_a).
+//
+// Evaluation order: second differences are formed as ((q+ - q) + (q- - q)) / h^2,
+// differences first, and the viscous / diffusive term is kept separate from the
+// advective products.  Smooth float32 fields make neighbouring values close, so
+// the differences are exact and the only rounding is in the small sums; the
+// algebraically equal grouped form (q+ - 2q + q-) or coefficient grouping such as
+// g * (u_x + 2 nu/h^2) loses several digits on fine grids.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+namespace fpde {
+
+struct Star {
+    float c;
+    float m[3];
+    float p[3];
+};
+
+// Float32 coefficients derived on the host in float64 and rounded once.
+struct KCoef {
+    float i2h[3];  // 1 / (2 h_a)
+    float ih2[3];  // 1 / h_a^2
+    float nu;
+    float k2;      // k^2
+    float inv_dt;  // 1 / dt
+    float alpha;
+};
+
+__device__ __forceinline__ float d1(const Star& s, int a, const KCoef& K) {
+    return (s.p[a] - s.m[a]) * K.i2h[a];
+}
+
+template <int DIM>
+__device__ __forceinline__ float lap(const Star& s, const KCoef& K) {
+    float l = 0.f;
+#pragma unroll
+    for (int a = 0; a < DIM; ++a) l += ((s.p[a] - s.c) + (s.m[a] - s.c)) * K.ih2[a];
+    return l;
+}
+
+// ---------------------------------------------------------------------------
+// Burgers on a space-time grid: axis 0 = t, axis 1 = x.
+//   R = u_t + u u_x - nu u_xx
+struct OpBurgers {
+    static constexpr int DIM = 2, NF = 1, NC = 0, NR = 1;
+
+    __device__ static void residual(const Star* f, const float*, const KCoef& K, float* R) {
+        const Star& u = f[0];
+        const float uxx = ((u.p[1] - u.c) + (u.m[1] - u.c)) * K.ih2[1];
+        R[0] = d1(u, 0, K) + u.c * d1(u, 1, K) - K.nu * uxx;
+    }
+
+    // dL/du(n): time neighbours (R(n-e_t) - R(n+e_t))/(2dt); advective
+    // R(n) u_x(n) + (R(n-e_x) u(n-e_x) - R(n+e_x) u(n+e_x))/(2dx); viscous -nu D2_x R.
+    __device__ static void gather(const Star* f, const Star* r, const KCoef& K, float* g) {
+        const Star& u = f[0];
+        const Star& R = r[0];
+        float acc = (R.m[0] - R.p[0]) * K.i2h[0];
+        acc += R.c * d1(u, 1, K);
+        acc += (R.m[1] * u.m[1] - R.p[1] * u.p[1]) * K.i2h[1];
+        acc -= K.nu * (((R.p[1] - R.c) + (R.m[1] - R.c)) * K.ih2[1]);
+        g[0] = acc;
+    }
+
+    template <int AX>
+    __device__ static void bc_term(const Star* f, const float* c, const KCoef& K, float t, float* g) {
+        float R[1];
+        residual(f, c, K, R);
+        g[0] = (AX == 0) ? R[0] * t * K.i2h[0]
+                         : R[0] * (t * f[0].c * K.i2h[1] - K.nu * K.ih2[1]);
+    }
+};
+
+// ---------------------------------------------------------------------------
+// Helmholtz: R = lap u + k^2 u - f   (self-adjoint: dL/du = k^2 R + lap R).
+struct OpHelmholtz {
+    static constexpr int DIM = 2, NF = 1, NC = 1, NR = 1;
+
+    __device__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
+        R[0] = lap<2>(f[0], K) + K.k2 * f[0].c - c[0];
+    }
+
+    __device__ static void gather(const Star*, const Star* r, const KCoef& K, float* g) {
+        g[0] = K.k2 * r[0].c + lap<2>(r[0], K);
+    }
+
+    template <int AX>
+    __device__ static void bc_term(const Star* f, const float* c, const KCoef& K, float, float* g) {
+        float R[1];
+        residual(f, c, K, R);
+        g[0] = R[0] * K.ih2[AX];
+    }
+};
+
+// ---------------------------------------------------------------------------
+// One implicit heat step: R = (u - u0)/dt - alpha lap u.
+struct OpHeat {
+    static constexpr int DIM = 3, NF = 1, NC = 1, NR = 1;
+
+    __device__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
+        R[0] = (f[0].c - c[0]) * K.inv_dt - K.alpha * lap<3>(f[0], K);
+    }
+
+    __device__ static void gather(const Star*, const Star* r, const KCoef& K, float* g) {
+        g[0] = r[0].c * K.inv_dt - K.alpha * lap<3>(r[0], K);
+    }
+
+    template <int AX>
+    __device__ static void bc_term(const Star* f, const float* c, const KCoef& K, float, float* g) {
+        float R[1];
+        residual(f, c, K, R);
+        g[0] = -R[0] * K.alpha * K.ih2[AX];
+    }
+};
+
+// ---------------------------------------------------------------------------
+// Incompressible NS; velocity component b on array axis b, pressure last.
+//   R_b = [(c_b - c_b_prev)/dt] + sum_a c_a D1_a c_b + D1_b p - nu lap c_b
+//   R_div = sum_a D1_a c_a
+// UNSTEADY selects the backward-Euler time term (consts = previous velocities).
+template <int D, bool UNSTEADY>
+struct OpNS {
+    static constexpr int DIM = D, NF = D + 1, NC = UNSTEADY ? D : 0, NR = D + 1;
+
+    __device__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
+        float div = 0.f;
+#pragma unroll
+        for (int b = 0; b < D; ++b) {
+            float adv = 0.f;
+#pragma unroll
+            for (int a = 0; a < D; ++a) adv += f[a].c * d1(f[b], a, K);
+            float r = adv + d1(f[D], b, K);
+            if (UNSTEADY) r += (f[b].c - c[b]) * K.inv_dt;
+            R[b] = r - K.nu * lap<D>(f[b], K);
+            div += d1(f[b], b, K);
+        }
+        R[D] = div;
+    }
+
+    // dL/dc_q(n) = sum_b R_b(n) D1_q c_b(n) + [R_q(n)/dt]
+    //            + sum_a (R_q(n-e_a) c_a(n-e_a) - R_q(n+e_a) c_a(n+e_a)) / (2 h_a)
+    //            + (R_div(n-e_q) - R_div(n+e_q)) / (2 h_q) - nu lap R_q(n)
+    // dL/dp(n)   = sum_b (R_b(n-e_b) - R_b(n+e_b)) / (2 h_b)
+    __device__ static void gather(const Star* f, const Star* r, const KCoef& K, float* g) {
+        float gp = 0.f;
+#pragma unroll
+        for (int q = 0; q < D; ++q) {
+            float acc = 0.f;
+#pragma unroll
+            for (int b = 0; b < D; ++b) acc += r[b].c * d1(f[b], q, K);
+            if (UNSTEADY) acc += r[q].c * K.inv_dt;
+            float nbr = 0.f;
+#pragma unroll
+            for (int a = 0; a < D; ++a)
+                nbr += (r[q].m[a] * f[a].m[a] - r[q].p[a] * f[a].p[a]) * K.i2h[a];
+            acc += nbr;
+            acc += (r[D].m[q] - r[D].p[q]) * K.i2h[q];
+            g[q] = acc - K.nu * lap<D>(r[q], K);
+            gp += (r[q].m[q] - r[q].p[q]) * K.i2h[q];
+        }
+        g[D] = gp;
+    }
+
+    // n = m + t e_AX: only the neighbour terms of R_b(m) reach n.
+    template <int AX>
+    __device__ static void bc_term(const Star* f, const float* c, const KCoef& K, float t, float* g) {
+        float R[NR];
+        residual(f, c, K, R);
+#pragma unroll
+        for (int q = 0; q < D; ++q) {
+            float v = R[q] * (t * f[AX].c * K.i2h[AX] - K.nu * K.ih2[AX]);
+            if (q == AX) v += R[D] * t * K.i2h[AX];
+            g[q] = v;
+        }
+        g[D] = R[AX] * t * K.i2h[AX];
+    }
+};
+
+using OpNS2 = OpNS<2, false>;
+using OpNS3 = OpNS<3, true>;
+
+}  // namespace fpde

@@ -1,0 +1,62 @@
+"""Helpers shared by the GPU parity tests: run the HIP path, compare with the oracle."""
+from __future__ import annotations
+
+import numpy as np
+
+# parity bar: residuals and loss within 1e-5 * max|ref|, gradients within 1e-4 * max|ref|
+TOL_RES = 1e-5
+TOL_GRAD = 1e-4
+
+
+def interior(a):
+    return a[tuple(slice(1, n - 1) for n in a.shape)]
+
+
+def shell_mask(shape):
+    m = np.ones(shape, bool)
+    m[tuple(slice(1, n - 1) for n in shape)] = False
+    return m
+
+
+def run_gpu(wl, dloss=1.0, store_residual=True, order=("bwd", "bc")):
+    """fwd (+ residuals) then bwd and bc on cuda:0; outputs pre-filled with NaN so
+    that untouched nodes are visible.  Returns numpy (R list, loss, grads list)."""
+    import torch  # noqa: PLC0415
+    from paper_2607_18020_amd import binding as B  # noqa: PLC0415
+    dev = torch.device("cuda:0")
+    fields = [torch.from_numpy(f).to(dev) for f in wl.fields]
+    consts = [torch.from_numpy(c).to(dev) for c in wl.consts]
+    R = None
+    if store_residual:
+        R = [torch.full_like(fields[0], float("nan")) for _ in wl.spec.residuals]
+    loss = B.fpde_residual_fwd(wl.op, fields, consts, wl.h, wl.coeffs, residual_out=R)
+    dl = torch.tensor(float(dloss), dtype=torch.float64, device=dev)
+    grads = [torch.full_like(f, float("nan")) for f in fields]
+    for step in order:
+        fn = B.fpde_residual_bwd if step == "bwd" else B.fpde_bc_correct
+        fn(wl.op, fields, consts, wl.h, wl.coeffs, dl, grads=grads)
+    torch.cuda.synchronize()
+    Rn = [r.cpu().numpy() for r in R] if R is not None else None
+    return Rn, float(loss.item()), [g.cpu().numpy() for g in grads]
+
+
+def max_rel_err(got, ref):
+    scale = float(np.abs(ref).max())
+    err = float(np.abs(got.astype(np.float64) - ref).max())
+    return err / scale if scale > 0 else err
+
+
+def assert_parity(wl, R_gpu, L_gpu, g_gpu, R_ref, L_ref, g_ref, what=""):
+    """Element-by-element comparison on the same float32 inputs."""
+    sm = shell_mask(wl.shape)
+    if R_gpu is not None:
+        for b, (rg, rr) in enumerate(zip(R_gpu, R_ref)):
+            assert np.all(np.isnan(rg[sm])), f"{what}: residual {b} written off the residual set"
+            e = max_rel_err(interior(rg), interior(rr))
+            assert e <= TOL_RES, f"{what}: residual {b} rel err {e:.3e}"
+    eL = abs(L_gpu - L_ref) / abs(L_ref)
+    assert eL <= TOL_RES, f"{what}: loss {L_gpu!r} vs {L_ref!r} (rel {eL:.3e})"
+    for f, (gg, gr) in enumerate(zip(g_gpu, g_ref)):
+        assert np.all(np.isfinite(gg)), f"{what}: grad {f} has unwritten nodes"
+        e = max_rel_err(gg, gr)
+        assert e <= TOL_GRAD, f"{what}: grad {f} rel err {e:.3e}"

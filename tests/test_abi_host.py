@@ -1,0 +1,168 @@
+"""Host-side checks of the C ABI (no GPU): exports, op table, validation.
+
+Every call here is invalid in at least one argument, so the library returns
+before queueing any GPU work; the fake device addresses are never touched.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_18020_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fpde.h")
+
+
+@pytest.fixture(scope="module")
+def B():
+    from paper_2607_18020_amd import binding  # noqa: PLC0415
+    try:
+        binding.lib()
+    except ImportError as e:  # pragma: no cover
+        pytest.fail(f"libfpde.so missing: {e}")
+    return binding
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(fpde_\w+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol(B):
+    decl = _declared_functions()
+    assert set(decl) == set(B.EXPORTED)
+    lib = B.lib()
+    for name in decl:
+        assert hasattr(lib, name), name
+
+
+def test_op_info_matches_workload_registry(B):
+    for op, spec in W.OPS.items():
+        ndim, nf, nc, nr = B.op_info(op)
+        assert (ndim, nf, nc, nr) == (spec.ndim, len(spec.fields), len(spec.consts), len(spec.residuals))
+    with pytest.raises(B.FpdeError):
+        B.op_info(0)
+    with pytest.raises(B.FpdeError):
+        B.op_info(6)
+
+
+def test_status_strings_and_version(B):
+    lib = B.lib()
+    for code, name in B.STATUS_NAMES.items():
+        assert lib.fpde_status_string(code).decode().startswith(name)
+    assert b"unknown" in lib.fpde_status_string(12345)
+    assert b"gfx950" in lib.fpde_version()
+
+
+# fake, 256-byte-aligned "device" addresses: never dereferenced (every call below is invalid)
+BASE = 0x7F0000000000
+STRIDE = 1 << 32
+
+
+def _addr(i, off=0):
+    return BASE + i * STRIDE + off
+
+
+def _arr(vals):
+    a = (ctypes.c_void_p * max(1, len(vals)))()
+    for i, v in enumerate(vals):
+        a[i] = v
+    return a
+
+
+def _call(B, fn, op, shape, h=None, coef=W.Coeffs(nu=0.01, k=1.0, dt=0.1, alpha=0.1),
+          fields=None, consts=None, outs=None, scalar=None, bc_mode=0, ndim=None):
+    lib = B.lib()
+    spec = W.OPS[op]
+    h = h if h is not None else (0.1,) * len(shape)
+    g = B.make_grid(shape, h, bc_mode)
+    if ndim is not None:
+        g.ndim = ndim
+    c = B.make_coeffs(coef)
+    nf, nc, nr = len(spec.fields), len(spec.consts), len(spec.residuals)
+    fields = fields if fields is not None else [_addr(i) for i in range(nf)]
+    consts = consts if consts is not None else [_addr(10 + j) for j in range(nc)]
+    scalar = _addr(30) if scalar is None else scalar
+    if fn == "fwd":
+        outs = outs if outs is not None else None
+        return lib.fpde_residual_fwd(op, ctypes.byref(g), ctypes.byref(c), _arr(fields),
+                                     _arr(consts) if nc else None,
+                                     _arr(outs) if outs is not None else None, scalar, None)
+    outs = outs if outs is not None else [_addr(20 + i) for i in range(nf)]
+    f = lib.fpde_residual_bwd if fn == "bwd" else lib.fpde_bc_correct
+    return f(op, ctypes.byref(g), ctypes.byref(c), _arr(fields), _arr(consts) if nc else None,
+             scalar, _arr(outs), None)
+
+
+ARG, SHAPE, SPACING, COEFF, ALIGN, UNSUP = -1, -2, -3, -4, -5, -7
+
+
+@pytest.mark.parametrize("fn", ["fwd", "bwd", "bc"])
+def test_validation_status_codes(B, fn):
+    op3, op2 = W.NS_3D_BE, W.NS_2D_STEADY
+    s3 = (8, 9, 10)
+    lib = B.lib()
+    g = B.make_grid(s3, (0.1,) * 3)
+    c = B.make_coeffs(W.Coeffs())
+    z = _arr([_addr(0)] * 4)
+    if fn == "fwd":  # unknown op, null grid
+        assert lib.fpde_residual_fwd(0, ctypes.byref(g), ctypes.byref(c), z, z, None, _addr(30), None) == ARG
+        assert lib.fpde_residual_fwd(op3, None, ctypes.byref(c), z, z, None, _addr(30), None) == ARG
+    # wrong rank, too small, bad spacing, bad coefficients
+    assert _call(B, fn, op3, s3, ndim=2) == SHAPE
+    assert _call(B, fn, op3, (2, 9, 10)) == SHAPE
+    assert _call(B, fn, op2, (9, 2)) == SHAPE
+    assert _call(B, fn, op3, s3, h=(0.1, 0.0, 0.1)) == SPACING
+    assert _call(B, fn, op3, s3, h=(0.1, float("nan"), 0.1)) == SPACING
+    assert _call(B, fn, op3, s3, h=(0.1, 0.1, -1.0)) == SPACING
+    assert _call(B, fn, op3, s3, coef=W.Coeffs(nu=0.01, dt=0.0)) == COEFF
+    assert _call(B, fn, op3, s3, coef=W.Coeffs(nu=float("inf"), dt=0.1)) == COEFF
+    assert _call(B, fn, W.HEAT_3D_BE, s3, coef=W.Coeffs(dt=-1.0, alpha=0.1)) == COEFF
+    # null field / const pointers
+    assert _call(B, fn, op3, s3, fields=[_addr(0), 0, _addr(2), _addr(3)]) == ARG
+    assert _call(B, fn, op3, s3, consts=[_addr(10), _addr(11), 0]) == ARG
+    # misaligned field
+    assert _call(B, fn, op3, s3, fields=[_addr(0), _addr(1, 2), _addr(2), _addr(3)]) == ALIGN
+    # periodic mode is reserved
+    assert _call(B, fn, op3, s3, bc_mode=1) == UNSUP
+    assert _call(B, fn, op3, s3, bc_mode=7) == ARG
+
+
+def test_output_checks(B):
+    op = W.NS_3D_BE
+    s3 = (8, 9, 10)
+    nbytes = 8 * 9 * 10 * 4
+    # fwd: null loss, misaligned loss, loss inside a field, residual aliasing a field
+    assert _call(B, "fwd", op, s3, scalar=0) == ARG
+    assert _call(B, "fwd", op, s3, scalar=_addr(30, 4)) == ALIGN
+    assert _call(B, "fwd", op, s3, scalar=_addr(2, 64)) == ARG
+    assert _call(B, "fwd", op, s3, outs=[_addr(20), _addr(21), _addr(1, 4 * 10), _addr(23)]) == ARG
+    assert _call(B, "fwd", op, s3, outs=[_addr(20), 0, _addr(22), _addr(23)]) == ARG
+    assert _call(B, "fwd", op, s3, outs=[_addr(20), _addr(20, nbytes - 4), _addr(22), _addr(23)]) == ARG
+    for fn in ("bwd", "bc"):
+        # null / misaligned dloss, grads aliasing fields, consts, each other or dloss
+        assert _call(B, fn, op, s3, scalar=0) == ARG
+        assert _call(B, fn, op, s3, scalar=_addr(30, 4)) == ALIGN
+        assert _call(B, fn, op, s3, outs=[_addr(20), _addr(0), _addr(22), _addr(23)]) == ARG
+        assert _call(B, fn, op, s3, outs=[_addr(20), _addr(21), _addr(11, 8), _addr(23)]) == ARG
+        assert _call(B, fn, op, s3, outs=[_addr(20), _addr(21), _addr(21), _addr(23)]) == ARG
+        assert _call(B, fn, op, s3, outs=[_addr(20), _addr(21), _addr(22), _addr(30, 0)],
+                     scalar=_addr(30, 16)) == ARG
+        assert _call(B, fn, op, s3, outs=[_addr(20), _addr(21), _addr(22), _addr(23, 2)]) == ALIGN
+
+
+def test_product_path_shares_nothing_with_the_oracle():
+    """The HIP path neither imports, includes nor links the oracle."""
+    pkg = os.path.join(ROOT, "paper_2607_18020_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for fn in files:
+            if fn.endswith((".py", ".hip", ".hpp", ".h", ".cpp")):
+                src = open(os.path.join(dirpath, fn)).read()
+                assert not re.search(r"^\s*(from|import)\s+oracle\b", src, re.M), fn
+                assert "fpde_oracle" not in src, fn
+                assert "orc_" not in src, fn

@@ -1,0 +1,173 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Small and ragged grids are compared element by element over every node
+(residuals on the residual set, the loss, and the gradient on every node,
+boundary shell included).  Full-size grids run in the same launch
+configuration the benchmark times; there the loss is compared with the oracle
+on the whole grid, and residuals and gradients on windows that the oracle
+evaluates on a sub-grid (corners, edges, faces and the middle of the domain).
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from paper_2607_18020_amd import workloads as W
+from tests import gpu_helpers as H
+
+pytestmark = pytest.mark.gpu
+
+# (config, shape): several tiles along every axis plus ragged tails (2-D rows are
+# 256-node segments; 3-D tiles are 64 x 8 columns; chunks of planes along axis 0)
+SMALL = [
+    ("burgers_1dt", (3, 3)), ("burgers_1dt", (5, 7)), ("burgers_1dt", (41, 300)),
+    ("burgers_1dt", (128, 256)),
+    ("helmholtz_2d", (3, 3)), ("helmholtz_2d", (4, 259)), ("helmholtz_2d", (67, 513)),
+    ("helmholtz_2d", (130, 1000)),
+    ("heat_3d", (3, 3, 3)), ("heat_3d", (5, 6, 7)), ("heat_3d", (19, 21, 70)),
+    ("heat_3d", (33, 40, 130)),
+    ("ns_2d", (3, 3)), ("ns_2d", (6, 257)), ("ns_2d", (71, 600)), ("ns_2d", (300, 257)),
+    ("ns_3d_tgv", (3, 3, 3)), ("ns_3d_tgv", (4, 9, 66)), ("ns_3d_tgv", (19, 21, 70)),
+    ("ns_3d_tgv", (40, 17, 129)),
+]
+
+
+@pytest.fixture(scope="module")
+def oracle_mod():
+    import oracle  # noqa: PLC0415
+    return oracle
+
+
+@pytest.mark.parametrize("cfg,shape", SMALL, ids=[f"{c}-{'x'.join(map(str, s))}" for c, s in SMALL])
+def test_parity_small_and_ragged(oracle_mod, cfg, shape):
+    wl = W.make(cfg, seed=42, shape=shape)
+    print(f"case {cfg} {shape}", flush=True)
+    R, L, g = H.run_gpu(wl, dloss=1.0)
+    Rr, Lr, gr = oracle_mod.on_workload(wl, dloss=1.0)
+    H.assert_parity(wl, R, L, g, Rr, Lr, gr, what=f"{cfg}{shape}")
+
+
+@pytest.mark.parametrize("op", sorted(W.OPS))
+@pytest.mark.parametrize("seed", [42, 43, 44, 45, 46])
+def test_parity_normal_inputs_seeds(oracle_mod, op, seed):
+    """The paper's verification inputs (App. A.7): N(0,1) fields, seeds 42-46."""
+    shape = (37, 291) if W.OPS[op].ndim == 2 else (13, 19, 75)
+    wl = W.normal_fields(op, shape, seed)
+    print(f"case op={op} seed={seed} {shape}", flush=True)
+    R, L, g = H.run_gpu(wl, dloss=1.0)
+    Rr, Lr, gr = oracle_mod.on_workload(wl, dloss=1.0)
+    H.assert_parity(wl, R, L, g, Rr, Lr, gr, what=f"op{op} seed{seed}")
+
+
+@pytest.mark.parametrize("cfg", ["ns_2d", "ns_3d_tgv", "burgers_1dt"])
+def test_dloss_scaling_and_call_order(oracle_mod, cfg):
+    """dloss scales the gradient; bwd and bc write disjoint nodes (either order)."""
+    shape = (23, 300) if W.OPS[W.CONFIGS[cfg].op].ndim == 2 else (11, 18, 67)
+    wl = W.make(cfg, seed=44, shape=shape)
+    dloss = -0.37
+    _, L, g = H.run_gpu(wl, dloss=dloss, store_residual=False, order=("bc", "bwd"))
+    gr = oracle_mod.grad(wl.op, wl.shape, wl.h, wl.coeffs, wl.fields, wl.consts, dloss=dloss)
+    for a, b in zip(g, gr):
+        assert H.max_rel_err(a, b) <= H.TOL_GRAD
+
+
+def test_bwd_and_bc_cover_disjoint_node_sets():
+    import torch  # noqa: PLC0415
+    from paper_2607_18020_amd import binding as B  # noqa: PLC0415
+    for cfg, shape in (("ns_3d_tgv", (9, 12, 70)), ("ns_2d", (9, 260))):
+        wl = W.make(cfg, seed=45, shape=shape)
+        fields = [torch.from_numpy(f).cuda() for f in wl.fields]
+        consts = [torch.from_numpy(c).cuda() for c in wl.consts]
+        dl = torch.ones((), dtype=torch.float64, device="cuda")
+        sm = torch.from_numpy(H.shell_mask(shape)).cuda()
+        g = [torch.full_like(f, float("nan")) for f in fields]
+        B.fpde_residual_bwd(wl.op, fields, consts, wl.h, wl.coeffs, dl, grads=g)
+        torch.cuda.synchronize()
+        for x in g:
+            assert torch.isnan(x[sm]).all() and torch.isfinite(x[~sm]).all()
+        g = [torch.full_like(f, float("nan")) for f in fields]
+        B.fpde_bc_correct(wl.op, fields, consts, wl.h, wl.coeffs, dl, grads=g)
+        torch.cuda.synchronize()
+        for x in g:
+            assert torch.isfinite(x[sm]).all() and torch.isnan(x[~sm]).all()
+
+
+def test_gradients_are_deterministic():
+    """Gather form, no atomics: two runs give bitwise-identical gradients."""
+    wl = W.make("ns_3d_tgv", seed=46, shape=(40, 33, 100))
+    _, L1, g1 = H.run_gpu(wl, store_residual=False)
+    _, L2, g2 = H.run_gpu(wl, store_residual=False)
+    for a, b in zip(g1, g2):
+        assert np.array_equal(a, b)
+    assert abs(L1 - L2) <= 1e-12 * abs(L1)
+
+
+def test_autograd_function_matches_abi(oracle_mod):
+    import torch  # noqa: PLC0415
+    from paper_2607_18020_amd import binding as B  # noqa: PLC0415
+    wl = W.make("ns_3d_tgv", seed=43, shape=(12, 20, 70))
+    fields = [torch.from_numpy(f).cuda().requires_grad_() for f in wl.fields]
+    consts = [torch.from_numpy(c).cuda() for c in wl.consts]
+    loss = B.ResidualLoss.apply(wl.op, wl.h, wl.coeffs, consts, *fields)
+    (2.5 * loss).backward()
+    gr = oracle_mod.grad(wl.op, wl.shape, wl.h, wl.coeffs, wl.fields, wl.consts, dloss=2.5)
+    for f, ref in zip(fields, gr):
+        assert H.max_rel_err(f.grad.cpu().numpy(), ref) <= H.TOL_GRAD
+    Lr = oracle_mod.loss(wl.op, wl.shape, wl.h, wl.coeffs, wl.fields, wl.consts)
+    assert abs(loss.item() - Lr) <= H.TOL_RES * Lr
+
+
+# --------------------------------------------------------------------------- full size
+
+
+def _windows(shape, w):
+    """Sub-grid boxes: every corner, the middle of every edge/face, the centre."""
+    picks = []
+    for n in shape:
+        picks.append(sorted({0, max(0, n // 2 - w // 2), n - w}))
+    boxes = []
+    import itertools  # noqa: PLC0415
+    for starts in itertools.product(*picks):
+        boxes.append(tuple(slice(s, s + w) for s in starts))
+    return boxes
+
+
+def _window_check(oracle_mod, wl, R, g, dloss, w):
+    M_full = wl.n_residual_points
+    for box in _windows(wl.shape, w):
+        sub_f = [np.ascontiguousarray(f[box]) for f in wl.fields]
+        sub_c = [np.ascontiguousarray(c[box]) for c in wl.consts]
+        sshape = sub_f[0].shape
+        Rs = oracle_mod.residual(wl.op, sshape, wl.h, wl.coeffs, sub_f, sub_c)
+        # residuals on the sub-grid interior equal the full-grid residuals there
+        for b in range(len(Rs)):
+            e = H.max_rel_err(H.interior(R[b][box]), H.interior(Rs[b]))
+            assert e <= H.TOL_RES, (box, b, e)
+        # gradients: G = 2 dloss R / M with the full-grid M; exact on nodes at least
+        # two nodes away from every cut (non-boundary) face of the box
+        Gs = [2.0 * dloss * r / M_full for r in Rs]
+        gs = oracle_mod.vjp(wl.op, sshape, wl.h, wl.coeffs, sub_f, sub_c, Gs)
+        valid = []
+        for a, sl in enumerate(box):
+            lo = 0 if sl.start == 0 else 2
+            hi = sshape[a] if sl.stop == wl.shape[a] else sshape[a] - 2
+            valid.append(slice(lo, hi))
+        valid = tuple(valid)
+        for f in range(len(gs)):
+            e = H.max_rel_err(g[f][box][valid], gs[f][valid])
+            assert e <= H.TOL_GRAD, (box, f, e)
+
+
+@pytest.mark.parametrize("cfg", list(W.CONFIG_ORDER))
+def test_parity_full_size(oracle_mod, cfg):
+    wl = W.make(cfg, seed=42)
+    print(f"case full {cfg} {wl.shape}", flush=True)
+    R, L, g = H.run_gpu(wl, dloss=1.0)
+    Lr = oracle_mod.loss(wl.op, wl.shape, wl.h, wl.coeffs, wl.fields, wl.consts)
+    assert abs(L - Lr) <= H.TOL_RES * abs(Lr), (L, Lr)
+    sm = H.shell_mask(wl.shape)
+    for r in R:
+        assert np.all(np.isnan(r[sm]))
+    for x in g:
+        assert np.all(np.isfinite(x))
+    _window_check(oracle_mod, wl, R, g, 1.0, w=24 if len(wl.shape) == 3 else 96)
