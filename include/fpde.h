@@ -118,9 +118,13 @@ int fpde_residual_fwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
 /* Interior analytic-adjoint backward, gather form (Sec. 2.2, App. A.3).
  *   dloss  device pointer to one double: the upstream derivative of the
  *          consumer's objective with respect to L (1.0 for L itself).
- *   grads  host array of n_fields device pointers; OVERWRITTEN on the interior
- *          nodes [1, n_a-2] of every axis with dloss * dL/dq.  Boundary-shell
- *          nodes are not touched (fpde_bc_correct writes them).
+ *   grads  host array of n_fields device pointers; OVERWRITTEN with
+ *          dloss * dL/dq on every node of the planes 1 <= i_0 <= n_0 - 2 of
+ *          array axis 0 (the planes the kernel marches over), boundary columns
+ *          of those planes included: there the transposed stencil is evaluated
+ *          with the residuals off Omega taken as zero, which is their exact
+ *          boundary term.  The end planes i_0 = 0 and i_0 = n_0 - 1 are not
+ *          touched (fpde_bc_correct writes them).
  * The residuals are recomputed from the fields; no sensitivity tensor is read.
  * Queues 1 kernel; no atomics. */
 int fpde_residual_bwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
@@ -128,12 +132,13 @@ int fpde_residual_bwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
                       const double* dloss, float* const* grads, void* stream);
 
 /* Boundary-gradient correction (Sec. 2.3, App. A.5): a 1-D launch over the
- * boundary shell (nodes with some i_a in {0, n_a-1}).  A node with exactly one
- * boundary coordinate receives the single term from its inward neighbour's
- * residuals; edge and corner nodes, which touch no residual node, receive 0.
- * Arguments as fpde_residual_bwd; OVERWRITES grads on the shell only, so
- * bwd and bc together write every node exactly once, in either order.
- * Queues 1 kernel. */
+ * boundary nodes the backward march does not visit, the end planes i_0 = 0 and
+ * i_0 = n_0 - 1.  A node whose only boundary coordinate is i_0 receives the
+ * terms of its single inward neighbour's residuals; a node with a second
+ * boundary coordinate (an edge or corner) touches no residual node and
+ * receives 0.  Arguments as fpde_residual_bwd; OVERWRITES grads on those two
+ * planes only, so bwd and bc together write every node exactly once, in
+ * either order.  Queues 1 kernel. */
 int fpde_bc_correct(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
                     const float* const* fields, const float* const* consts,
                     const double* dloss, float* const* grads, void* stream);

@@ -40,7 +40,7 @@ struct Req {
     Dims dims;
     KCoef K;
     double inv_M, two_over_M;
-    long long N, M, shell;
+    long long N, M;
     Ptrs P;
     hipStream_t stream;
 };
@@ -84,6 +84,7 @@ int validate_common(int op, const fpde_grid* g, const fpde_coeffs* c, const floa
     memset(&K, 0, sizeof K);
     for (int a = 0; a < D; ++a) {
         const double h = g->h[a];
+        K.i2hd[a] = 1.0 / (2.0 * h);
         K.i2h[a] = (float)(1.0 / (2.0 * h));
         K.ih2[a] = (float)(1.0 / (h * h));
         if (!isfinite(K.i2h[a]) || !isfinite(K.ih2[a]) || K.ih2[a] == 0.f) return FPDE_ERR_SPACING;
@@ -118,14 +119,12 @@ int validate_common(int op, const fpde_grid* g, const fpde_coeffs* c, const floa
         dm.nx = (int)g->n[2];
         dm.tiles_x = (dm.nx + kTX3 - 1) / kTX3;
         dm.tiles_y = (dm.ny + kTY3 - 1) / kTY3;
-        r->shell = N - M;
     } else {
         dm.nz = (int)g->n[0];
         dm.ny = 1;
         dm.nx = (int)g->n[1];
         dm.tiles_x = (dm.nx + kTX2 - 1) / kTX2;
         dm.tiles_y = 1;
-        r->shell = N - M;
     }
     const long long tiles = (long long)dm.tiles_x * dm.tiles_y;
     const long long target = (D == 3) ? kTargetBlocks3 : kTargetBlocks2;
@@ -186,10 +185,11 @@ int launch_bwd(const Req& r, const double* dloss) {
 
 template <class OP>
 int launch_bc(const Req& r, const double* dloss) {
-    long long nb = (r.shell + 255) / 256;
+    const long long nodes = 2LL * r.dims.ny * r.dims.nx;  // the two end planes of axis 0
+    long long nb = (nodes + 255) / 256;
     if (nb > 65535LL * 16) nb = 65535LL * 16;
     hipLaunchKernelGGL((bc_kernel<OP>), dim3((unsigned)nb), dim3(256), 0, r.stream, r.P, r.dims,
-                       r.K, dloss, r.two_over_M, r.shell);
+                       r.K, dloss, r.two_over_M);
     return hip_status();
 }
 

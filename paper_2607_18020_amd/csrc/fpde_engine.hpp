@@ -20,9 +20,12 @@
 // gather for plane z reads R(z) (in-plane star, LDS), R(z+1) (LDS) and R(z-1)
 // (register queue).  Field planes live in a 4-slot LDS ring (tile plus a
 // two-node halo); the next plane is prefetched into registers one step ahead.
-// Each interior node is written exactly once; no atomics.
+// Every node of the visited planes 1..nz-2 is written exactly once (boundary
+// columns included: there the residuals off the residual set are zero, which
+// the LDS tiles already hold); no atomics.
 //
-// Boundary correction: a 1-D launch over the boundary shell (Sec. 2.3).
+// Boundary correction: a 1-D launch over the two end planes of axis 0, the
+// boundary nodes the march does not visit (Sec. 2.3).
 //
 // Workgroup-to-tile order is XCD-aware: consecutive workgroup ids are spread
 // round-robin over the 8 XCDs, so the id is remapped such that each XCD gets a
@@ -163,11 +166,23 @@ __global__ __launch_bounds__(TX* TY) void fwd_kernel(Ptrs P, Dims D, KCoef K, do
     const bool ring_in = has_ring && rgx >= 0 && rgx < D.nx && rgy >= 0 && rgy < D.ny;
     const int rcol = ring_in ? rgy * D.nx + rgx : 0;
 
-    float q[NF][3];
+    // register queue of the own column (planes z-1, z, z+1), the ring value of the
+    // current plane, the consts of the current plane, and their prefetched successors
+    float q[NF][3], qn[NF], rc[NF], rn[NF];
+    float cc[NC > 0 ? NC : 1], cn[NC > 0 ? NC : 1];
 #pragma unroll
     for (int f = 0; f < NF; ++f) {
         q[f][0] = inarr ? P.f[f][(long long)(tc.z0 - 1) * plane + col] : 0.f;
         q[f][1] = inarr ? P.f[f][(long long)tc.z0 * plane + col] : 0.f;
+        q[f][2] = inarr ? P.f[f][(long long)(tc.z0 + 1) * plane + col] : 0.f;
+        rc[f] = ring_in ? P.f[f][(long long)tc.z0 * plane + rcol] : 0.f;
+        qn[f] = 0.f;
+        rn[f] = 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < NC; ++j) {
+        cc[j] = interior ? P.c[j][(long long)tc.z0 * plane + col] : 0.f;
+        cn[j] = 0.f;
     }
 
     double acc = 0.0;
@@ -175,14 +190,18 @@ __global__ __launch_bounds__(TX* TY) void fwd_kernel(Ptrs P, Dims D, KCoef K, do
     for (int z = tc.z0; z < tc.z1; ++z) {
         const long long zo = (long long)z * plane;
 #pragma unroll
-        for (int f = 0; f < NF; ++f) q[f][2] = inarr ? P.f[f][zo + plane + col] : 0.f;
-        float cc[NC > 0 ? NC : 1];
-#pragma unroll
-        for (int j = 0; j < NC; ++j) cc[j] = interior ? P.c[j][zo + col] : 0.f;
-#pragma unroll
         for (int f = 0; f < NF; ++f) {
             sF[buf][f][ty + HY][tx + 1] = q[f][1];
-            if (has_ring) sF[buf][f][rly][rlx] = ring_in ? P.f[f][zo + rcol] : 0.f;
+            if (has_ring) sF[buf][f][rly][rlx] = rc[f];
+        }
+        if (z + 1 < tc.z1) {  // prefetch plane z+1's ring and consts, plane z+2's column
+#pragma unroll
+            for (int f = 0; f < NF; ++f) {
+                qn[f] = inarr ? P.f[f][zo + 2 * plane + col] : 0.f;
+                rn[f] = ring_in ? P.f[f][zo + plane + rcol] : 0.f;
+            }
+#pragma unroll
+            for (int j = 0; j < NC; ++j) cn[j] = interior ? P.c[j][zo + plane + col] : 0.f;
         }
         __syncthreads();
         if (interior) {
@@ -213,7 +232,11 @@ __global__ __launch_bounds__(TX* TY) void fwd_kernel(Ptrs P, Dims D, KCoef K, do
         for (int f = 0; f < NF; ++f) {
             q[f][0] = q[f][1];
             q[f][1] = q[f][2];
+            q[f][2] = qn[f];
+            rc[f] = rn[f];
         }
+#pragma unroll
+        for (int j = 0; j < NC; ++j) cc[j] = cn[j];
         buf ^= 1;
     }
     block_atomic_sum<NT>(acc * inv_M, loss);
@@ -376,7 +399,7 @@ __global__ __launch_bounds__(TX* TY) void bwd_kernel(Ptrs P, Dims D, KCoef K,
         __syncthreads();
         r_tile(z + 1, z & 3, (z + 1) & 3, (z + 2) & 3, (z + 1) & 1);
         __syncthreads();
-        if (interior) {
+        if (inarr) {
             const int sc = z & 3, sp = (z + 1) & 3, rc = z & 1, rp = (z + 1) & 1;
             const int fy = ty + HY, fx = tx + 2, ry = ty + RHY, rx = tx + 1;
             Star fs[NF], rs[NR];
@@ -418,22 +441,21 @@ __global__ __launch_bounds__(TX* TY) void bwd_kernel(Ptrs P, Dims D, KCoef K,
 }
 
 // ---------------------------------------------------------------------------
-// Boundary-gradient correction over the shell.
-//
-// Shell enumeration (3-D): faces of axis 0 (i0 in {0, nz-1}, all i1, i2), then
-// faces of axis 1 (i0 interior, i1 in {0, ny-1}, all i2), then faces of axis 2
-// (i0, i1 interior, i2 in {0, nx-1}).  2-D: faces of axis 0, then of axis 1.
-// A node with more than one boundary coordinate touches no residual node and
-// gets 0.
+// Boundary-gradient correction: the two end planes of axis 0 (i0 = 0 and
+// i0 = nz - 1), which the march never visits.  A node whose only boundary
+// coordinate is i0 receives the terms of its inward neighbour's residuals; a
+// node with another boundary coordinate as well (an edge or corner) touches no
+// residual node and gets 0.  (Boundary nodes of the other axes lie on visited
+// planes: the march evaluates the same transposed stencil there with the
+// residuals taken as zero off the residual set, which is exactly their
+// correction term.)
 
-// One boundary-face node n with boundary axis AX: n = m + t e_AX, with m the
-// inward neighbour (on the residual set).
-template <class OP, int AX>
-__device__ __forceinline__ void bc_node(const Ptrs& P, const KCoef& K, const long long* i,
-                                        const long long* str, long long node, float* g) {
+template <class OP>
+__device__ __forceinline__ void bc_node0(const Ptrs& P, const KCoef& K, const long long* str,
+                                         long long node, bool low, float* g) {
     constexpr int DIM = OP::DIM, NF = OP::NF, NC = OP::NC;
-    const float t = (i[AX] == 0) ? -1.f : 1.f;
-    const long long m = (i[AX] == 0) ? node + str[AX] : node - str[AX];
+    const float t = low ? -1.f : 1.f;  // node = m + t e_0
+    const long long m = low ? node + str[0] : node - str[0];
     Star s[NF];
 #pragma unroll
     for (int f = 0; f < NF; ++f) {
@@ -448,77 +470,30 @@ __device__ __forceinline__ void bc_node(const Ptrs& P, const KCoef& K, const lon
     float cc[NC > 0 ? NC : 1];
 #pragma unroll
     for (int j = 0; j < NC; ++j) cc[j] = P.c[j][m];
-    OP::template bc_term<AX>(s, cc, K, t, g);
+    OP::template bc_term<0>(s, cc, K, t, g);
 }
 
 template <class OP>
 __global__ __launch_bounds__(256) void bc_kernel(Ptrs P, Dims D, KCoef K, const double* dloss,
-                                                 double two_over_M, long long total) {
+                                                 double two_over_M) {
     constexpr int DIM = OP::DIM, NF = OP::NF;
     const float scale = (float)(two_over_M * (*dloss));
     const long long nz = D.nz, ny = D.ny, nx = D.nx;
     const long long plane = ny * nx;
+    const long long total = 2 * plane;
+    const long long str[3] = {plane, (DIM == 3) ? nx : 1, 1};
     for (long long idx = blockIdx.x * 256LL + threadIdx.x; idx < total;
          idx += (long long)gridDim.x * 256LL) {
-        long long i[3] = {0, 0, 0};  // (axis 0, axis 1, axis 2) for 3-D; (axis 0, axis 1) for 2-D
-        long long r = idx;
-        if (DIM == 3) {
-            const long long sa = 2 * ny * nx, sb = 2 * (nz - 2) * nx;
-            if (r < sa) {
-                i[0] = (r / plane) ? nz - 1 : 0;
-                r %= plane;
-                i[1] = r / nx;
-                i[2] = r % nx;
-            } else if ((r -= sa) < sb) {
-                const long long half = (nz - 2) * nx;
-                i[1] = (r / half) ? ny - 1 : 0;
-                r %= half;
-                i[0] = 1 + r / nx;
-                i[2] = r % nx;
-            } else {
-                r -= sb;
-                const long long half = (nz - 2) * (ny - 2);
-                i[2] = (r / half) ? nx - 1 : 0;
-                r %= half;
-                i[0] = 1 + r / (ny - 2);
-                i[1] = 1 + r % (ny - 2);
-            }
-        } else {
-            const long long sa = 2 * nx;
-            if (r < sa) {
-                i[0] = (r / nx) ? nz - 1 : 0;
-                i[1] = r % nx;
-            } else {
-                r -= sa;
-                i[1] = (r / (nz - 2)) ? nx - 1 : 0;
-                i[0] = 1 + r % (nz - 2);
-            }
-        }
-        const long long n[3] = {nz, (DIM == 3) ? ny : nx, nx};
-        int nb = 0, ax = 0;
-#pragma unroll
-        for (int a = 0; a < DIM; ++a) {
-            if (i[a] == 0 || i[a] == n[a] - 1) {
-                ++nb;
-                ax = a;
-            }
-        }
-        long long str[3];
-        if (DIM == 3) {
-            str[0] = plane; str[1] = nx; str[2] = 1;
-        } else {
-            str[0] = nx; str[1] = 1; str[2] = 0;
-        }
-        long long node = 0;
-#pragma unroll
-        for (int a = 0; a < DIM; ++a) node += i[a] * str[a];
+        const bool low = idx < plane;
+        const long long r = low ? idx : idx - plane;
+        const long long node = (low ? 0 : (nz - 1) * plane) + r;
+        const long long i1 = (DIM == 3) ? r / nx : r;
+        const long long i2 = r % nx;
+        const bool edge = (DIM == 3) ? (i1 == 0 || i1 == ny - 1 || i2 == 0 || i2 == nx - 1)
+                                     : (i1 == 0 || i1 == nx - 1);
         float g[NF];
-        if (nb == 1) {
-            switch (ax) {
-            case 0: bc_node<OP, 0>(P, K, i, str, node, g); break;
-            case 1: bc_node<OP, 1>(P, K, i, str, node, g); break;
-            default: bc_node<OP, (DIM == 3) ? 2 : 1>(P, K, i, str, node, g); break;
-            }
+        if (!edge) {
+            bc_node0<OP>(P, K, str, node, low, g);
 #pragma unroll
             for (int f = 0; f < NF; ++f) g[f] *= scale;
         } else {

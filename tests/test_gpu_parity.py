@@ -72,24 +72,27 @@ def test_dloss_scaling_and_call_order(oracle_mod, cfg):
 
 
 def test_bwd_and_bc_cover_disjoint_node_sets():
+    """bwd writes every node of planes 1..n0-2 of axis 0; bc writes planes 0 and n0-1."""
     import torch  # noqa: PLC0415
     from paper_2607_18020_amd import binding as B  # noqa: PLC0415
-    for cfg, shape in (("ns_3d_tgv", (9, 12, 70)), ("ns_2d", (9, 260))):
+    for cfg, shape in (("ns_3d_tgv", (9, 12, 70)), ("ns_2d", (9, 260)), ("heat_3d", (3, 3, 3))):
         wl = W.make(cfg, seed=45, shape=shape)
         fields = [torch.from_numpy(f).cuda() for f in wl.fields]
         consts = [torch.from_numpy(c).cuda() for c in wl.consts]
         dl = torch.ones((), dtype=torch.float64, device="cuda")
-        sm = torch.from_numpy(H.shell_mask(shape)).cuda()
+        ends = torch.zeros(shape, dtype=torch.bool, device="cuda")
+        ends[0] = True
+        ends[-1] = True
         g = [torch.full_like(f, float("nan")) for f in fields]
         B.fpde_residual_bwd(wl.op, fields, consts, wl.h, wl.coeffs, dl, grads=g)
         torch.cuda.synchronize()
         for x in g:
-            assert torch.isnan(x[sm]).all() and torch.isfinite(x[~sm]).all()
+            assert torch.isnan(x[ends]).all() and torch.isfinite(x[~ends]).all()
         g = [torch.full_like(f, float("nan")) for f in fields]
         B.fpde_bc_correct(wl.op, fields, consts, wl.h, wl.coeffs, dl, grads=g)
         torch.cuda.synchronize()
         for x in g:
-            assert torch.isfinite(x[sm]).all() and torch.isnan(x[~sm]).all()
+            assert torch.isfinite(x[ends]).all() and torch.isnan(x[~ends]).all()
 
 
 def test_gradients_are_deterministic():
