@@ -29,10 +29,31 @@ bool op_desc(int op, OpDesc* d) {
 // Launch geometry.  3-D: 64 x 8 column tiles (512 threads, one wavefront per
 // x-row of 64 nodes).  2-D: 256-node row segments.  Chunks of planes along axis 0
 // are sized so that a launch has about kTargetBlocks workgroups.
-constexpr int kTX3 = 64, kTY3 = 8;
-constexpr int kTX2 = 256;
-constexpr int kTargetBlocks3 = 512;
-constexpr int kTargetBlocks2 = 1024;
+#ifndef FPDE_TX3
+#define FPDE_TX3 64
+#endif
+#ifndef FPDE_TY3
+#define FPDE_TY3 8
+#endif
+#ifndef FPDE_TY3_BWD
+#define FPDE_TY3_BWD 8
+#endif
+#ifndef FPDE_TX2
+#define FPDE_TX2 256
+#endif
+#ifndef FPDE_BLOCKS3
+#define FPDE_BLOCKS3 512
+#endif
+#ifndef FPDE_BLOCKS3_BWD
+#define FPDE_BLOCKS3_BWD 512
+#endif
+#ifndef FPDE_BLOCKS2
+#define FPDE_BLOCKS2 1024
+#endif
+constexpr int kTX3 = FPDE_TX3, kTY3 = FPDE_TY3, kTY3b = FPDE_TY3_BWD;
+constexpr int kTX2 = FPDE_TX2;
+constexpr int kTargetBlocks3 = FPDE_BLOCKS3, kTargetBlocks3b = FPDE_BLOCKS3_BWD;
+constexpr int kTargetBlocks2 = FPDE_BLOCKS2;
 
 struct Req {
     int op;
@@ -112,31 +133,31 @@ int validate_common(int op, const fpde_grid* g, const fpde_coeffs* c, const floa
     for (int f = 0; f < r->d.nf; ++f) r->P.f[f] = fields[f];
     for (int j = 0; j < r->d.nc; ++j) r->P.c[j] = consts[j];
 
-    Dims& dm = r->dims;
-    if (D == 3) {
-        dm.nz = (int)g->n[0];
-        dm.ny = (int)g->n[1];
-        dm.nx = (int)g->n[2];
-        dm.tiles_x = (dm.nx + kTX3 - 1) / kTX3;
-        dm.tiles_y = (dm.ny + kTY3 - 1) / kTY3;
-    } else {
-        dm.nz = (int)g->n[0];
-        dm.ny = 1;
-        dm.nx = (int)g->n[1];
-        dm.tiles_x = (dm.nx + kTX2 - 1) / kTX2;
-        dm.tiles_y = 1;
-    }
+    Dims& dm = r->dims;  // sizes only; tiles and chunks are set per launch
+    dm.nz = (int)g->n[0];
+    dm.ny = (D == 3) ? (int)g->n[1] : 1;
+    dm.nx = (int)g->n[D - 1];
+    dm.tiles_x = dm.tiles_y = dm.zc = dm.nblocks = 0;
+    // every launch shape used below must have fewer than 2^31 workgroups
+    if ((long long)(dm.nx / 32 + 1) * (dm.ny + 1) * (dm.nz + 1) >= (1LL << 31)) return FPDE_ERR_SHAPE;
+    return FPDE_OK;
+}
+
+// Tiles of TX x TY columns and chunks of planes along axis 0 such that a launch
+// has about `target` workgroups (each chunk at least one plane).
+Dims launch_dims(const Dims& n, int TX, int TY, int target) {
+    Dims dm = n;
+    dm.tiles_x = (dm.nx + TX - 1) / TX;
+    dm.tiles_y = (dm.ny + TY - 1) / TY;
     const long long tiles = (long long)dm.tiles_x * dm.tiles_y;
-    const long long target = (D == 3) ? kTargetBlocks3 : kTargetBlocks2;
     const int nplanes = dm.nz - 2;
     long long nch = (target + tiles - 1) / tiles;
     if (nch < 1) nch = 1;
     if (nch > nplanes) nch = nplanes;
     dm.zc = (int)((nplanes + nch - 1) / nch);
     nch = (nplanes + dm.zc - 1) / dm.zc;
-    if (tiles * nch >= (1LL << 31)) return FPDE_ERR_SHAPE;
     dm.nblocks = (int)(tiles * nch);
-    return FPDE_OK;
+    return dm;
 }
 
 int check_outputs(const Req& r, const fpde_grid*, const float* const* fields,
@@ -165,21 +186,23 @@ int hip_status() {
 // ---- launches, per op type
 
 template <class OP, int TX, int TY>
-int launch_fwd(const Req& r, bool store, double* loss) {
+int launch_fwd(const Req& r, bool store, double* loss, int target) {
+    const Dims dm = launch_dims(r.dims, TX, TY, target);
     hipLaunchKernelGGL(fill_f64_kernel, dim3(1), dim3(1), 0, r.stream, loss, 0.0);
     if (store)
-        hipLaunchKernelGGL((fwd_kernel<OP, TX, TY, true>), dim3(r.dims.nblocks), dim3(TX * TY), 0,
-                           r.stream, r.P, r.dims, r.K, r.inv_M, loss);
+        hipLaunchKernelGGL((fwd_kernel<OP, TX, TY, true>), dim3(dm.nblocks), dim3(TX * TY), 0,
+                           r.stream, r.P, dm, r.K, r.inv_M, loss);
     else
-        hipLaunchKernelGGL((fwd_kernel<OP, TX, TY, false>), dim3(r.dims.nblocks), dim3(TX * TY), 0,
-                           r.stream, r.P, r.dims, r.K, r.inv_M, loss);
+        hipLaunchKernelGGL((fwd_kernel<OP, TX, TY, false>), dim3(dm.nblocks), dim3(TX * TY), 0,
+                           r.stream, r.P, dm, r.K, r.inv_M, loss);
     return hip_status();
 }
 
 template <class OP, int TX, int TY>
-int launch_bwd(const Req& r, const double* dloss) {
-    hipLaunchKernelGGL((bwd_kernel<OP, TX, TY>), dim3(r.dims.nblocks), dim3(TX * TY), 0, r.stream,
-                       r.P, r.dims, r.K, dloss, r.two_over_M);
+int launch_bwd(const Req& r, const double* dloss, int target) {
+    const Dims dm = launch_dims(r.dims, TX, TY, target);
+    hipLaunchKernelGGL((bwd_kernel<OP, TX, TY>), dim3(dm.nblocks), dim3(TX * TY), 0, r.stream,
+                       r.P, dm, r.K, dloss, r.two_over_M);
     return hip_status();
 }
 
@@ -195,11 +218,11 @@ int launch_bc(const Req& r, const double* dloss) {
 
 template <class OP>
 int dispatch_fwd3(const Req& r, bool store, double* loss) {
-    return launch_fwd<OP, kTX3, kTY3>(r, store, loss);
+    return launch_fwd<OP, kTX3, kTY3>(r, store, loss, kTargetBlocks3);
 }
 template <class OP>
 int dispatch_fwd2(const Req& r, bool store, double* loss) {
-    return launch_fwd<OP, kTX2, 1>(r, store, loss);
+    return launch_fwd<OP, kTX2, 1>(r, store, loss, kTargetBlocks2);
 }
 
 int run_fwd(const Req& r, bool store, double* loss) {
@@ -215,11 +238,11 @@ int run_fwd(const Req& r, bool store, double* loss) {
 
 int run_bwd(const Req& r, const double* dloss) {
     switch (r.op) {
-    case FPDE_BURGERS_1DT: return launch_bwd<OpBurgers, kTX2, 1>(r, dloss);
-    case FPDE_HELMHOLTZ_2D: return launch_bwd<OpHelmholtz, kTX2, 1>(r, dloss);
-    case FPDE_HEAT_3D_BE: return launch_bwd<OpHeat, kTX3, kTY3>(r, dloss);
-    case FPDE_NS_2D_STEADY: return launch_bwd<OpNS2, kTX2, 1>(r, dloss);
-    case FPDE_NS_3D_BE: return launch_bwd<OpNS3, kTX3, kTY3>(r, dloss);
+    case FPDE_BURGERS_1DT: return launch_bwd<OpBurgers, kTX2, 1>(r, dloss, kTargetBlocks2);
+    case FPDE_HELMHOLTZ_2D: return launch_bwd<OpHelmholtz, kTX2, 1>(r, dloss, kTargetBlocks2);
+    case FPDE_HEAT_3D_BE: return launch_bwd<OpHeat, kTX3, kTY3b>(r, dloss, kTargetBlocks3b);
+    case FPDE_NS_2D_STEADY: return launch_bwd<OpNS2, kTX2, 1>(r, dloss, kTargetBlocks2);
+    case FPDE_NS_3D_BE: return launch_bwd<OpNS3, kTX3, kTY3b>(r, dloss, kTargetBlocks3b);
     }
     return FPDE_ERR_ARG;
 }
