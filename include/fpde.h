@@ -83,7 +83,8 @@ typedef enum fpde_op {
 /* Grid: rank, residual-set mode, sizes per array axis, spacings per axis.
  * bc_mode 0 is the residual set Omega above; other values are rejected with
  * FPDE_ERR_UNSUPPORTED.  Entries past ndim are ignored.
- * Limits: every n_a >= 3; n[ndim-2]*n[ndim-1] < 2^31 and each n_a < 2^31. */
+ * Limits: every n_a >= 3 and n_a < 2^31; a plane of the non-marching axes
+ * (n[1]*n[2] for ndim 3, n[1] for ndim 2) holds fewer than 2^29 nodes. */
 typedef struct fpde_grid {
     int32_t ndim;
     int32_t bc_mode;

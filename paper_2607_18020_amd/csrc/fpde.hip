@@ -35,6 +35,9 @@ bool op_desc(int op, OpDesc* d) {
 #ifndef FPDE_TY3
 #define FPDE_TY3 8
 #endif
+#ifndef FPDE_TX3_BWD
+#define FPDE_TX3_BWD 64
+#endif
 #ifndef FPDE_TY3_BWD
 #define FPDE_TY3_BWD 8
 #endif
@@ -45,12 +48,12 @@ bool op_desc(int op, OpDesc* d) {
 #define FPDE_BLOCKS3 512
 #endif
 #ifndef FPDE_BLOCKS3_BWD
-#define FPDE_BLOCKS3_BWD 512
+#define FPDE_BLOCKS3_BWD 1024
 #endif
 #ifndef FPDE_BLOCKS2
 #define FPDE_BLOCKS2 1024
 #endif
-constexpr int kTX3 = FPDE_TX3, kTY3 = FPDE_TY3, kTY3b = FPDE_TY3_BWD;
+constexpr int kTX3 = FPDE_TX3, kTY3 = FPDE_TY3, kTX3b = FPDE_TX3_BWD, kTY3b = FPDE_TY3_BWD;
 constexpr int kTX2 = FPDE_TX2;
 constexpr int kTargetBlocks3 = FPDE_BLOCKS3, kTargetBlocks3b = FPDE_BLOCKS3_BWD;
 constexpr int kTargetBlocks2 = FPDE_BLOCKS2;
@@ -93,7 +96,8 @@ int validate_common(int op, const fpde_grid* g, const fpde_coeffs* c, const floa
         N *= g->n[a];
         M *= g->n[a] - 2;
     }
-    if (g->n[D - 2] * g->n[D - 1] >= (1LL << 31)) return FPDE_ERR_SHAPE;
+    // plane of the last two axes (one row for 2-D grids) addressed with 32-bit byte offsets
+    if ((D == 3 ? g->n[1] * g->n[2] : g->n[1]) >= (1LL << 29)) return FPDE_ERR_SHAPE;
     for (int a = 0; a < D; ++a)
         if (!finite_pos(g->h[a])) return FPDE_ERR_SPACING;
     if (!isfinite(c->nu) || !isfinite(c->k) || !isfinite(c->dt) || !isfinite(c->alpha))
@@ -240,9 +244,9 @@ int run_bwd(const Req& r, const double* dloss) {
     switch (r.op) {
     case FPDE_BURGERS_1DT: return launch_bwd<OpBurgers, kTX2, 1>(r, dloss, kTargetBlocks2);
     case FPDE_HELMHOLTZ_2D: return launch_bwd<OpHelmholtz, kTX2, 1>(r, dloss, kTargetBlocks2);
-    case FPDE_HEAT_3D_BE: return launch_bwd<OpHeat, kTX3, kTY3b>(r, dloss, kTargetBlocks3b);
+    case FPDE_HEAT_3D_BE: return launch_bwd<OpHeat, kTX3b, kTY3b>(r, dloss, kTargetBlocks3b);
     case FPDE_NS_2D_STEADY: return launch_bwd<OpNS2, kTX2, 1>(r, dloss, kTargetBlocks2);
-    case FPDE_NS_3D_BE: return launch_bwd<OpNS3, kTX3, kTY3b>(r, dloss, kTargetBlocks3b);
+    case FPDE_NS_3D_BE: return launch_bwd<OpNS3, kTX3b, kTY3b>(r, dloss, kTargetBlocks3b);
     }
     return FPDE_ERR_ARG;
 }

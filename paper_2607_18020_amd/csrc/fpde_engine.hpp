@@ -36,6 +36,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "fpde_ops.hpp"
 
 namespace fpde {
@@ -138,12 +140,45 @@ __device__ __forceinline__ TileCoord tile_coord(const Dims& D) {
 }
 
 // ---------------------------------------------------------------------------
+// Global-memory access in the marching kernels: one raw buffer resource per
+// plane (base = the plane's first byte, built in SGPRs) and a 32-bit per-thread
+// byte offset, so a load is a single buffer_load_dword with no per-lane
+// address arithmetic.  num_records is the plane size: an offset past it reads 0.
+// Positions outside the array use offset 0 and a select to zero.
+
+template <int V>
+using IC = std::integral_constant<int, V>;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t plane_rsrc(const float* p, int z,
+                                                             uint32_t pbytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(reinterpret_cast<const char*>(p) + (uint64_t)z * pbytes), (short)0, (int)pbytes,
+        0x00020000);
+}
+
+__device__ __forceinline__ float bld(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
+}
+
+__device__ __forceinline__ void bst(__amdgpu_buffer_rsrc_t r, uint32_t off, float v) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)off, 0, 0);
+}
+
+// ---------------------------------------------------------------------------
 // Forward: residuals of one chunk of planes + fused sum of squares.
 
+#ifndef FPDE_FWD_MINW
+#define FPDE_FWD_MINW 1
+#endif
+#ifndef FPDE_BWD_MINW
+#define FPDE_BWD_MINW 1
+#endif
+
 template <class OP, int TX, int TY, bool STORE_R>
-__global__ __launch_bounds__(TX* TY) void fwd_kernel(Ptrs P, Dims D, KCoef K, double inv_M,
+__global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims D, KCoef K, double inv_M,
                                                      double* loss) {
     constexpr int DIM = OP::DIM, NF = OP::NF, NC = OP::NC, NR = OP::NR, NT = TX * TY;
+    constexpr int NC1 = NC > 0 ? NC : 1;
     constexpr int HY = (DIM == 3) ? 1 : 0;
     constexpr int LY = TY + 2 * HY, LX = TX + 2;
     static_assert(DIM == 3 || TY == 1, "2-D grids use one-row tiles");
@@ -152,11 +187,12 @@ __global__ __launch_bounds__(TX* TY) void fwd_kernel(Ptrs P, Dims D, KCoef K, do
 
     const int t = threadIdx.x, tx = t % TX, ty = t / TX;
     const TileCoord tc = tile_coord<TX, TY>(D);
+    const int z0 = tc.z0, z1 = tc.z1;
     const int gx = tc.gx0 + tx, gy = (DIM == 3) ? tc.gy0 + ty : 0;
-    const long long plane = (long long)D.ny * D.nx;
+    const uint32_t pbytes = (uint32_t)D.ny * (uint32_t)D.nx * 4u;
     const bool inarr = gx < D.nx && gy < D.ny;
     const bool interior = gx >= 1 && gx <= D.nx - 2 && (DIM == 2 || (gy >= 1 && gy <= D.ny - 2));
-    const int col = gy * D.nx + gx;
+    const uint32_t cb = inarr ? (uint32_t)(gy * D.nx + gx) * 4u : 0u;
 
     // fixed halo-ring slot of this thread (if any)
     const bool has_ring = t < Ring<TX, TY, DIM>::COUNT;
@@ -164,86 +200,99 @@ __global__ __launch_bounds__(TX* TY) void fwd_kernel(Ptrs P, Dims D, KCoef K, do
     if (has_ring) Ring<TX, TY, DIM>::pos(t, rly, rlx);
     const int rgy = (DIM == 3) ? tc.gy0 - 1 + rly : 0, rgx = tc.gx0 - 1 + rlx;
     const bool ring_in = has_ring && rgx >= 0 && rgx < D.nx && rgy >= 0 && rgy < D.ny;
-    const int rcol = ring_in ? rgy * D.nx + rgx : 0;
+    const uint32_t rb = ring_in ? (uint32_t)(rgy * D.nx + rgx) * 4u : 0u;
 
-    // register queue of the own column (planes z-1, z, z+1), the ring value of the
-    // current plane, the consts of the current plane, and their prefetched successors
-    float q[NF][3], qn[NF], rc[NF], rn[NF];
-    float cc[NC > 0 ? NC : 1], cn[NC > 0 ? NC : 1];
+    // Register queue of the own column: planes z-1, z, z+1 and the prefetched
+    // z+2 live in q[(j)&3], q[(j+1)&3], q[(j+2)&3], q[(j+3)&3] at step j = z - z0;
+    // the ring values and consts of plane z (and prefetched z+1) alternate.
+    float q[4][NF], rv[2][NF], cv[2][NC1];
 #pragma unroll
     for (int f = 0; f < NF; ++f) {
-        q[f][0] = inarr ? P.f[f][(long long)(tc.z0 - 1) * plane + col] : 0.f;
-        q[f][1] = inarr ? P.f[f][(long long)tc.z0 * plane + col] : 0.f;
-        q[f][2] = inarr ? P.f[f][(long long)(tc.z0 + 1) * plane + col] : 0.f;
-        rc[f] = ring_in ? P.f[f][(long long)tc.z0 * plane + rcol] : 0.f;
-        qn[f] = 0.f;
-        rn[f] = 0.f;
+        const float a = bld(plane_rsrc(P.f[f], z0 - 1, pbytes), cb);
+        const float b = bld(plane_rsrc(P.f[f], z0, pbytes), cb);
+        const float c = bld(plane_rsrc(P.f[f], z0 + 1, pbytes), cb);
+        const float r = bld(plane_rsrc(P.f[f], z0, pbytes), rb);
+        q[0][f] = inarr ? a : 0.f;
+        q[1][f] = inarr ? b : 0.f;
+        q[2][f] = inarr ? c : 0.f;
+        q[3][f] = 0.f;
+        rv[0][f] = ring_in ? r : 0.f;
+        rv[1][f] = 0.f;
     }
 #pragma unroll
-    for (int j = 0; j < NC; ++j) {
-        cc[j] = interior ? P.c[j][(long long)tc.z0 * plane + col] : 0.f;
-        cn[j] = 0.f;
+    for (int j = 0; j < NC1; ++j) {
+        cv[0][j] = NC ? bld(plane_rsrc(P.c[j], z0, pbytes), cb) : 0.f;
+        cv[1][j] = 0.f;
     }
 
     double acc = 0.0;
-    int buf = 0;
-    for (int z = tc.z0; z < tc.z1; ++z) {
-        const long long zo = (long long)z * plane;
+    auto step = [&](auto jc, int z) __attribute__((always_inline)) {
+        constexpr int J = decltype(jc)::value;
+        constexpr int QM = J & 3, QZ = (J + 1) & 3, QP = (J + 2) & 3, QN = (J + 3) & 3;
+        constexpr int CUR = J & 1, NXT = (J + 1) & 1, BUF = J & 1;
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
-            sF[buf][f][ty + HY][tx + 1] = q[f][1];
-            if (has_ring) sF[buf][f][rly][rlx] = rc[f];
+            sF[BUF][f][ty + HY][tx + 1] = q[QZ][f];
+            if (has_ring) sF[BUF][f][rly][rlx] = rv[CUR][f];
         }
-        if (z + 1 < tc.z1) {  // prefetch plane z+1's ring and consts, plane z+2's column
+        if (z + 1 < z1) {  // prefetch plane z+2 of the own column, ring and consts of z+1
 #pragma unroll
             for (int f = 0; f < NF; ++f) {
-                qn[f] = inarr ? P.f[f][zo + 2 * plane + col] : 0.f;
-                rn[f] = ring_in ? P.f[f][zo + plane + rcol] : 0.f;
+                // branch-free: threads without a ring node load a valid address too
+                const float v = bld(plane_rsrc(P.f[f], z + 2, pbytes), cb);
+                const float w = bld(plane_rsrc(P.f[f], z + 1, pbytes), rb);
+                q[QN][f] = inarr ? v : 0.f;
+                rv[NXT][f] = ring_in ? w : 0.f;
             }
 #pragma unroll
-            for (int j = 0; j < NC; ++j) cn[j] = interior ? P.c[j][zo + plane + col] : 0.f;
+            for (int j = 0; j < NC; ++j) cv[NXT][j] = bld(plane_rsrc(P.c[j], z + 1, pbytes), cb);
         }
         __syncthreads();
-        if (interior) {
-            Star s[NF];
-#pragma unroll
-            for (int f = 0; f < NF; ++f) {
-                s[f].c = q[f][1];
-                s[f].m[0] = q[f][0];
-                s[f].p[0] = q[f][2];
-                s[f].m[DIM - 1] = sF[buf][f][ty + HY][tx];
-                s[f].p[DIM - 1] = sF[buf][f][ty + HY][tx + 2];
-                if (DIM == 3) {
-                    s[f].m[1] = sF[buf][f][ty][tx + 1];
-                    s[f].p[1] = sF[buf][f][ty + 2][tx + 1];
-                }
-            }
-            float R[NR];
-            OP::residual(s, cc, K, R);
-            float ss = 0.f;
-#pragma unroll
-            for (int b = 0; b < NR; ++b) {
-                ss += R[b] * R[b];
-                if (STORE_R) P.out[b][zo + col] = R[b];
-            }
-            acc += (double)ss;
-        }
+        Star s[NF];
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
-            q[f][0] = q[f][1];
-            q[f][1] = q[f][2];
-            q[f][2] = qn[f];
-            rc[f] = rn[f];
+            s[f].c = q[QZ][f];
+            s[f].m[0] = q[QM][f];
+            s[f].p[0] = q[QP][f];
+            s[f].m[DIM - 1] = sF[BUF][f][ty + HY][tx];
+            s[f].p[DIM - 1] = sF[BUF][f][ty + HY][tx + 2];
+            if (DIM == 3) {
+                s[f].m[1] = sF[BUF][f][ty][tx + 1];
+                s[f].p[1] = sF[BUF][f][ty + 2][tx + 1];
+            }
         }
+        float R[NR];
+        OP::residual(s, cv[CUR], K, R);
+        float ss = 0.f;
 #pragma unroll
-        for (int j = 0; j < NC; ++j) cc[j] = cn[j];
-        buf ^= 1;
+        for (int b = 0; b < NR; ++b) ss = fmaf(R[b], R[b], ss);
+        acc += (double)(interior ? ss : 0.f);
+        if (STORE_R && interior) {
+#pragma unroll
+            for (int b = 0; b < NR; ++b) bst(plane_rsrc(P.out[b], z, pbytes), cb, R[b]);
+        }
+    };
+
+    int z = z0;
+    for (; z + 4 <= z1; z += 4) {  // four steps bring the queue and the buffers back
+        step(IC<0>{}, z);
+        step(IC<1>{}, z + 1);
+        step(IC<2>{}, z + 2);
+        step(IC<3>{}, z + 3);
     }
+    if (z < z1) step(IC<0>{}, z);
+    if (z + 1 < z1) step(IC<1>{}, z + 1);
+    if (z + 2 < z1) step(IC<2>{}, z + 2);
     block_atomic_sum<NT>(acc * inv_M, loss);
 }
 
 // ---------------------------------------------------------------------------
 // Backward: gather-form transposed stencil with residual recompute.
+//
+// Per step z: plane z+3 is queued from memory straight into the LDS slot of
+// plane z-1; R(z+1) is evaluated on the tile and its one-node ring into an LDS
+// tile; the gather at plane z reads the in-plane neighbours of R(z) from LDS and
+// R(z-1), R(z), R(z+1) of its own column from a register queue; one barrier.
 
 template <class OP, int TX, int TY>
 struct BwdGeo {
@@ -257,187 +306,229 @@ struct BwdGeo {
 };
 
 template <class OP, int TX, int TY>
-__global__ __launch_bounds__(TX* TY) void bwd_kernel(Ptrs P, Dims D, KCoef K,
+__global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims D, KCoef K,
                                                      const double* dloss, double two_over_M) {
     using G = BwdGeo<OP, TX, TY>;
     constexpr int DIM = OP::DIM, NF = OP::NF, NC = OP::NC, NR = OP::NR, NT = G::NT;
+    constexpr int NC1 = NC > 0 ? NC : 1;
     constexpr int HY = G::HY, FLY = G::FLY, FLX = G::FLX, RHY = G::RHY, RLY = G::RLY,
                   RLX = G::RLX, FSZ = G::FSZ, KP = G::KP;
     static_assert(DIM == 3 || TY == 1, "2-D grids use one-row tiles");
     static_assert(Ring<TX, TY, DIM>::COUNT <= NT, "ring larger than the workgroup");
+    // field planes in a 4-slot ring: plane pz lives in slot (pz - z0 + 1) & 3
     __shared__ float sF[4][NF][FLY][FLX];
+    // residual tiles: R(zr) lives in buffer (zr - z0) & 1
     __shared__ float sR[2][NR][RLY][RLX];
 
     const int t = threadIdx.x, tx = t % TX, ty = t / TX;
     const TileCoord tc = tile_coord<TX, TY>(D);
+    const int z0 = tc.z0, z1 = tc.z1;
     const int gx = tc.gx0 + tx, gy = (DIM == 3) ? tc.gy0 + ty : 0;
-    const long long plane = (long long)D.ny * D.nx;
+    const uint32_t pbytes = (uint32_t)D.ny * (uint32_t)D.nx * 4u;
     const bool inarr = gx < D.nx && gy < D.ny;
-    const bool interior = gx >= 1 && gx <= D.nx - 2 && (DIM == 2 || (gy >= 1 && gy <= D.ny - 2));
-    const int col = gy * D.nx + gx;
+    const uint32_t cb = inarr ? (uint32_t)(gy * D.nx + gx) * 4u : 0u;
     const float scale = (float)(two_over_M * (*dloss));
 
-    // Per-thread prefetch slots of a field plane (tile + 2-node halo).
-    int pofs[KP];
-    bool pok[KP];
+    // This thread's share of a field plane (tile + 2-node halo): element
+    // i = t + k*NT of the slot, in slot order, so that the 64 lanes of a wave
+    // fill 64 consecutive LDS words.  Planes go straight from memory into LDS
+    // (buffer_load_dword ... lds); a position outside the array gets an offset
+    // past the descriptor's range, which the buffer unit reads as 0.
+    constexpr uint32_t kOff = 0x80000000u;
+    uint32_t poff[KP];
 #pragma unroll
     for (int k = 0; k < KP; ++k) {
         const int i = t + k * NT;
         const int ly = i / FLX, lx = i % FLX;
         const int py = (DIM == 3) ? tc.gy0 - HY + ly : 0, px = tc.gx0 - 2 + lx;
-        pok[k] = i < FSZ && px >= 0 && px < D.nx && py >= 0 && py < D.ny;
-        pofs[k] = pok[k] ? py * D.nx + px : 0;
+        const bool ok = i < FSZ && px >= 0 && px < D.nx && py >= 0 && py < D.ny;
+        poff[k] = ok ? (uint32_t)(py * D.nx + px) * 4u : kOff;
     }
-    float pre[NF][KP];
-    auto load_plane = [&](int z) {
-        const bool zok = z >= 0 && z < D.nz;
-        const long long zo = (long long)(zok ? z : 0) * plane;
+    const int wbase = t & ~63;  // first element of this wave in each round
+    // queue plane pz (uniform) into LDS slot `slot`; planes outside the grid read as 0
+    auto load_plane = [&](int pz, int slot) __attribute__((always_inline)) {
+        const bool zok = pz >= 0 && pz < D.nz;
 #pragma unroll
-        for (int f = 0; f < NF; ++f)
+        for (int f = 0; f < NF; ++f) {
+            const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+                (void*)(reinterpret_cast<const char*>(P.f[f]) +
+                        (uint64_t)(zok ? pz : 0) * pbytes),
+                (short)0, zok ? (int)pbytes : 0, 0x00020000);
 #pragma unroll
-            for (int k = 0; k < KP; ++k) pre[f][k] = (zok && pok[k]) ? P.f[f][zo + pofs[k]] : 0.f;
-    };
-    auto store_plane = [&](int slot) {
-#pragma unroll
-        for (int k = 0; k < KP; ++k) {
-            const int i = t + k * NT;
-            if (i < FSZ) {
-#pragma unroll
-                for (int f = 0; f < NF; ++f) (&sF[slot][f][0][0])[i] = pre[f][k];
+            for (int k = 0; k < KP; ++k) {
+                if (KP * NT == FSZ || t + k * NT < FSZ) {
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                        r, (__attribute__((address_space(3))) void*)(&sF[slot][f][0][0] + wbase + k * NT),
+                        4, (int)poff[k], 0, 0, 0);
+                }
             }
         }
     };
 
-    // Residuals at plane zr on R-tile position (ly, lx) -> sR[dst].
-    auto r_at = [&](int zr, int sm, int sc, int sp, int dst, int ly, int lx) {
-        const int ry = (DIM == 3) ? tc.gy0 - RHY + ly : 0, rx = tc.gx0 - 1 + lx;
-        const bool om = zr >= 1 && zr <= D.nz - 2 && rx >= 1 && rx <= D.nx - 2 &&
-                        (DIM == 2 || (ry >= 1 && ry <= D.ny - 2));
-        float R[NR];
-        if (om) {
-            const int fy = ly + (HY - RHY), fx = lx + 1;
-            Star s[NF];
-#pragma unroll
-            for (int f = 0; f < NF; ++f) {
-                s[f].c = sF[sc][f][fy][fx];
-                s[f].m[0] = sF[sm][f][fy][fx];
-                s[f].p[0] = sF[sp][f][fy][fx];
-                s[f].m[DIM - 1] = sF[sc][f][fy][fx - 1];
-                s[f].p[DIM - 1] = sF[sc][f][fy][fx + 1];
-                if (DIM == 3) {
-                    s[f].m[1] = sF[sc][f][fy - 1][fx];
-                    s[f].p[1] = sF[sc][f][fy + 1][fx];
-                }
-            }
-            float cc[NC > 0 ? NC : 1];
-            const long long o = (long long)zr * plane + ry * D.nx + rx;
-#pragma unroll
-            for (int j = 0; j < NC; ++j) cc[j] = P.c[j][o];
-            OP::residual(s, cc, K, R);
-        } else {
-#pragma unroll
-            for (int b = 0; b < NR; ++b) R[b] = 0.f;
-        }
-#pragma unroll
-        for (int b = 0; b < NR; ++b) sR[dst][b][ly][lx] = R[b];
-    };
+    // residual positions of this thread on the R tile: its own column and, for
+    // the first threads, one node of the ring; their in-plane part of the
+    // residual-set test and their const offsets are fixed for the whole march
+    const int oly = ty + RHY, olx = tx + 1;
+    const bool own_om = gx >= 1 && gx <= D.nx - 2 && (DIM == 2 || (gy >= 1 && gy <= D.ny - 2));
     const bool has_ring = t < Ring<TX, TY, DIM>::COUNT;
     int rly = 0, rlx = 0;
     if (has_ring) Ring<TX, TY, DIM>::pos(t, rly, rlx);
-    auto r_tile = [&](int zr, int sm, int sc, int sp, int dst) {
-        r_at(zr, sm, sc, sp, dst, ty + RHY, tx + 1);
-        if (has_ring) r_at(zr, sm, sc, sp, dst, rly, rlx);
+    const int rgy = (DIM == 3) ? tc.gy0 - RHY + rly : 0, rgx = tc.gx0 - 1 + rlx;
+    const bool ring_om = has_ring && rgx >= 1 && rgx <= D.nx - 2 &&
+                         (DIM == 2 || (rgy >= 1 && rgy <= D.ny - 2));
+    const uint32_t rcb = ring_om ? (uint32_t)(rgy * D.nx + rgx) * 4u : 0u;
+
+    // R(zr) at R-tile position (ly, lx) from field slots sm (zr-1), sc (zr), sp (zr+1);
+    // written to sR[dst] and returned in R (zero off the residual set)
+    auto r_at = [&](int zr, int sm, int sc, int sp, int dst, int ly, int lx, bool om_xy,
+                    const float* cc, float* R) __attribute__((always_inline)) {
+        const int fy = ly + (HY - RHY), fx = lx + 1;
+        Star s[NF];
+#pragma unroll
+        for (int f = 0; f < NF; ++f) {
+            s[f].c = sF[sc][f][fy][fx];
+            s[f].m[0] = sF[sm][f][fy][fx];
+            s[f].p[0] = sF[sp][f][fy][fx];
+            s[f].m[DIM - 1] = sF[sc][f][fy][fx - 1];
+            s[f].p[DIM - 1] = sF[sc][f][fy][fx + 1];
+            if (DIM == 3) {
+                s[f].m[1] = sF[sc][f][fy - 1][fx];
+                s[f].p[1] = sF[sc][f][fy + 1][fx];
+            }
+        }
+        OP::residual(s, cc, K, R);
+        const bool om = om_xy && zr >= 1 && zr <= D.nz - 2;
+#pragma unroll
+        for (int b = 0; b < NR; ++b) {
+            R[b] = om ? R[b] : 0.f;
+            sR[dst][b][ly][lx] = R[b];
+        }
+    };
+    // consts of the R-tile positions, for the plane whose residuals come next
+    // (loaded one step ahead so that their latency hides behind a step)
+    float cown[NC1], cring[NC1];
+    auto load_consts = [&](int zr) __attribute__((always_inline)) {  // zr uniform, in range
+#pragma unroll
+        for (int j = 0; j < NC; ++j) {
+            const __amdgpu_buffer_rsrc_t r = plane_rsrc(P.c[j], zr, pbytes);
+            cown[j] = bld(r, cb);
+            cring[j] = bld(r, rcb);
+        }
+    };
+    // R(zr) on the whole R tile; the own column's values are returned in Rown
+    auto r_tile = [&](int zr, int sm, int sc, int sp, int dst, float* Rown)
+                      __attribute__((always_inline)) {
+        r_at(zr, sm, sc, sp, dst, oly, olx, own_om, cown, Rown);
+        if (has_ring) {
+            float Rr[NR];
+            r_at(zr, sm, sc, sp, dst, rly, rlx, ring_om, cring, Rr);
+        }
     };
 
-    // ---- prologue: planes z0-1, z0, z0+1 in LDS; R(z0) tile; R(z0-1) own column
-    const int z0 = tc.z0, z1 = tc.z1;
-    for (int pz = z0 - 1; pz <= z0 + 1; ++pz) {
-        load_plane(pz);
-        store_plane(pz & 3);
-    }
-    float fzm[NF], rzm[NR];
+    // ---- prologue: planes z0-1 .. z0+2 in slots 0..3; R(z0) tile; the own
+    // column's R(z0-1), R(z0) and fields of plane z0-1 in registers
+    for (int j = 0; j < 4; ++j) load_plane(z0 - 1 + j, j);
     float fzm2[NF];
 #pragma unroll
-    for (int f = 0; f < NF; ++f)
-        fzm2[f] = (inarr && z0 >= 2) ? P.f[f][(long long)(z0 - 2) * plane + col] : 0.f;
+    for (int f = 0; f < NF; ++f) {
+        const float v = bld(plane_rsrc(P.f[f], z0 >= 2 ? z0 - 2 : 0, pbytes), cb);
+        fzm2[f] = (inarr && z0 >= 2) ? v : 0.f;
+    }
+    load_consts(z0);
     __syncthreads();
-    r_tile(z0, (z0 - 1) & 3, z0 & 3, (z0 + 1) & 3, z0 & 1);
+    float fzm[NF], rzm[NR], rzc[NR], rzp[NR];
+    r_tile(z0, 0, 1, 2, 0, rzc);
     {
-        const int s1 = (z0 - 1) & 3, s0 = z0 & 3;
         const int fy = ty + HY, fx = tx + 2;
+        Star s[NF];
 #pragma unroll
-        for (int f = 0; f < NF; ++f) fzm[f] = sF[s1][f][fy][fx];
-        if (interior && z0 - 1 >= 1) {
-            Star s[NF];
-#pragma unroll
-            for (int f = 0; f < NF; ++f) {
-                s[f].c = sF[s1][f][fy][fx];
-                s[f].m[0] = fzm2[f];
-                s[f].p[0] = sF[s0][f][fy][fx];
-                s[f].m[DIM - 1] = sF[s1][f][fy][fx - 1];
-                s[f].p[DIM - 1] = sF[s1][f][fy][fx + 1];
-                if (DIM == 3) {
-                    s[f].m[1] = sF[s1][f][fy - 1][fx];
-                    s[f].p[1] = sF[s1][f][fy + 1][fx];
-                }
+        for (int f = 0; f < NF; ++f) {
+            s[f].c = sF[0][f][fy][fx];
+            s[f].m[0] = fzm2[f];
+            s[f].p[0] = sF[1][f][fy][fx];
+            s[f].m[DIM - 1] = sF[0][f][fy][fx - 1];
+            s[f].p[DIM - 1] = sF[0][f][fy][fx + 1];
+            if (DIM == 3) {
+                s[f].m[1] = sF[0][f][fy - 1][fx];
+                s[f].p[1] = sF[0][f][fy + 1][fx];
             }
-            float cc[NC > 0 ? NC : 1];
-#pragma unroll
-            for (int j = 0; j < NC; ++j) cc[j] = P.c[j][(long long)(z0 - 1) * plane + col];
-            OP::residual(s, cc, K, rzm);
-        } else {
-#pragma unroll
-            for (int b = 0; b < NR; ++b) rzm[b] = 0.f;
+            fzm[f] = s[f].c;
         }
+        float cc[NC1];
+#pragma unroll
+        for (int j = 0; j < NC; ++j) cc[j] = bld(plane_rsrc(P.c[j], z0 - 1, pbytes), cb);
+        OP::residual(s, cc, K, rzm);
+        const bool om = own_om && z0 - 1 >= 1;
+#pragma unroll
+        for (int b = 0; b < NR; ++b) rzm[b] = om ? rzm[b] : 0.f;
     }
-    load_plane(z0 + 2);
+    load_consts(z0 + 1);
+    __syncthreads();
 
-    // ---- march
-    for (int z = z0; z < z1; ++z) {
-        store_plane((z + 2) & 3);
-        if (z + 1 < z1) load_plane(z + 3);
-        __syncthreads();
-        r_tile(z + 1, z & 3, (z + 1) & 3, (z + 2) & 3, (z + 1) & 1);
-        __syncthreads();
-        if (inarr) {
-            const int sc = z & 3, sp = (z + 1) & 3, rc = z & 1, rp = (z + 1) & 1;
-            const int fy = ty + HY, fx = tx + 2, ry = ty + RHY, rx = tx + 1;
-            Star fs[NF], rs[NR];
+    // ---- march.  Step z: issue the loads of plane z+3; R(z+1) on the R tile; the
+    // gather at plane z; plane z+3 into the slot of plane z-1; one barrier.  Every
+    // LDS buffer a step writes was last read before the previous step's barrier.
+    auto step = [&](auto jc, int z) __attribute__((always_inline)) {
+        constexpr int J = decltype(jc)::value;  // (z - z0) & 3
+        // field slots of planes z-1 (reused for z+3), z, z+1, z+2; R tiles of R(z), R(z+1)
+        constexpr int SM = J & 3, SC = (J + 1) & 3, SP = (J + 2) & 3, SQ = (J + 3) & 3;
+        constexpr int RC = J & 1, RP = (J + 1) & 1;
+        const bool more = z + 1 < z1;
+        if (more) load_plane(z + 3, SM);  // the slot of plane z-1, unread in this step
+        r_tile(z + 1, SC, SP, SQ, RP, rzp);
+        if (more) load_consts(z + 2);
+        const int fy = ty + HY, fx = tx + 2, ry = ty + RHY, rx = tx + 1;
+        Star fs[NF], rs[NR];
 #pragma unroll
-            for (int f = 0; f < NF; ++f) {
-                fs[f].c = sF[sc][f][fy][fx];
-                fs[f].m[0] = fzm[f];
-                fs[f].p[0] = sF[sp][f][fy][fx];
-                fs[f].m[DIM - 1] = sF[sc][f][fy][fx - 1];
-                fs[f].p[DIM - 1] = sF[sc][f][fy][fx + 1];
-                if (DIM == 3) {
-                    fs[f].m[1] = sF[sc][f][fy - 1][fx];
-                    fs[f].p[1] = sF[sc][f][fy + 1][fx];
-                }
+        for (int f = 0; f < NF; ++f) {
+            fs[f].c = sF[SC][f][fy][fx];
+            fs[f].m[0] = fzm[f];
+            fs[f].p[0] = sF[SP][f][fy][fx];
+            fs[f].m[DIM - 1] = sF[SC][f][fy][fx - 1];
+            fs[f].p[DIM - 1] = sF[SC][f][fy][fx + 1];
+            if (DIM == 3) {
+                fs[f].m[1] = sF[SC][f][fy - 1][fx];
+                fs[f].p[1] = sF[SC][f][fy + 1][fx];
             }
-#pragma unroll
-            for (int b = 0; b < NR; ++b) {
-                rs[b].c = sR[rc][b][ry][rx];
-                rs[b].m[0] = rzm[b];
-                rs[b].p[0] = sR[rp][b][ry][rx];
-                rs[b].m[DIM - 1] = sR[rc][b][ry][rx - 1];
-                rs[b].p[DIM - 1] = sR[rc][b][ry][rx + 1];
-                if (DIM == 3) {
-                    rs[b].m[1] = sR[rc][b][ry - 1][rx];
-                    rs[b].p[1] = sR[rc][b][ry + 1][rx];
-                }
-            }
-            float g[NF];
-            OP::gather(fs, rs, K, g);
-            const long long o = (long long)z * plane + col;
-#pragma unroll
-            for (int f = 0; f < NF; ++f) P.out[f][o] = scale * g[f];
-#pragma unroll
-            for (int f = 0; f < NF; ++f) fzm[f] = fs[f].c;
-#pragma unroll
-            for (int b = 0; b < NR; ++b) rzm[b] = rs[b].c;
         }
+#pragma unroll
+        for (int b = 0; b < NR; ++b) {
+            rs[b].c = rzc[b];
+            rs[b].m[0] = rzm[b];
+            rs[b].p[0] = rzp[b];
+            rs[b].m[DIM - 1] = sR[RC][b][ry][rx - 1];
+            rs[b].p[DIM - 1] = sR[RC][b][ry][rx + 1];
+            if (DIM == 3) {
+                rs[b].m[1] = sR[RC][b][ry - 1][rx];
+                rs[b].p[1] = sR[RC][b][ry + 1][rx];
+            }
+        }
+        float g[NF];
+        OP::gather(fs, rs, K, g);
+        if (inarr) {
+#pragma unroll
+            for (int f = 0; f < NF; ++f) bst(plane_rsrc(P.out[f], z, pbytes), cb, scale * g[f]);
+        }
+#pragma unroll
+        for (int f = 0; f < NF; ++f) fzm[f] = fs[f].c;
+#pragma unroll
+        for (int b = 0; b < NR; ++b) {
+            rzm[b] = rzc[b];
+            rzc[b] = rzp[b];
+        }
+        __syncthreads();  // (waits for the plane loads into LDS as well)
+    };
+
+    int z = z0;
+    for (; z + 4 <= z1; z += 4) {  // slot and buffer indices are constants in each copy
+        step(IC<0>{}, z);
+        step(IC<1>{}, z + 1);
+        step(IC<2>{}, z + 2);
+        step(IC<3>{}, z + 3);
     }
+    if (z < z1) step(IC<0>{}, z);
+    if (z + 1 < z1) step(IC<1>{}, z + 1);
+    if (z + 2 < z1) step(IC<2>{}, z + 2);
 }
 
 // ---------------------------------------------------------------------------

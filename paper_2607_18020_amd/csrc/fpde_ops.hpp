@@ -67,7 +67,7 @@ __device__ __forceinline__ float lap(const Star& s, const KCoef& K) {
 struct OpBurgers {
     static constexpr int DIM = 2, NF = 1, NC = 0, NR = 1;
 
-    __device__ static void residual(const Star* f, const float*, const KCoef& K, float* R) {
+    __device__ __forceinline__ static void residual(const Star* f, const float*, const KCoef& K, float* R) {
         const Star& u = f[0];
         const float uxx = ((u.p[1] - u.c) + (u.m[1] - u.c)) * K.ih2[1];
         R[0] = d1(u, 0, K) + u.c * d1(u, 1, K) - K.nu * uxx;
@@ -75,7 +75,7 @@ struct OpBurgers {
 
     // dL/du(n): time neighbours (R(n-e_t) - R(n+e_t))/(2dt); advective
     // R(n) u_x(n) + (R(n-e_x) u(n-e_x) - R(n+e_x) u(n+e_x))/(2dx); viscous -nu D2_x R.
-    __device__ static void gather(const Star* f, const Star* r, const KCoef& K, float* g) {
+    __device__ __forceinline__ static void gather(const Star* f, const Star* r, const KCoef& K, float* g) {
         const Star& u = f[0];
         const Star& R = r[0];
         float acc = (R.m[0] - R.p[0]) * K.i2h[0];
@@ -86,7 +86,7 @@ struct OpBurgers {
     }
 
     template <int AX>
-    __device__ static void bc_term(const Star* f, const float* c, const KCoef& K, float t, float* g) {
+    __device__ __forceinline__ static void bc_term(const Star* f, const float* c, const KCoef& K, float t, float* g) {
         float R[1];
         residual(f, c, K, R);
         g[0] = (AX == 0) ? R[0] * t * K.i2h[0]
@@ -99,16 +99,16 @@ struct OpBurgers {
 struct OpHelmholtz {
     static constexpr int DIM = 2, NF = 1, NC = 1, NR = 1;
 
-    __device__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
+    __device__ __forceinline__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
         R[0] = lap<2>(f[0], K) + K.k2 * f[0].c - c[0];
     }
 
-    __device__ static void gather(const Star*, const Star* r, const KCoef& K, float* g) {
+    __device__ __forceinline__ static void gather(const Star*, const Star* r, const KCoef& K, float* g) {
         g[0] = K.k2 * r[0].c + lap<2>(r[0], K);
     }
 
     template <int AX>
-    __device__ static void bc_term(const Star* f, const float* c, const KCoef& K, float, float* g) {
+    __device__ __forceinline__ static void bc_term(const Star* f, const float* c, const KCoef& K, float, float* g) {
         float R[1];
         residual(f, c, K, R);
         g[0] = R[0] * K.ih2[AX];
@@ -120,16 +120,16 @@ struct OpHelmholtz {
 struct OpHeat {
     static constexpr int DIM = 3, NF = 1, NC = 1, NR = 1;
 
-    __device__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
+    __device__ __forceinline__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
         R[0] = (f[0].c - c[0]) * K.inv_dt - K.alpha * lap<3>(f[0], K);
     }
 
-    __device__ static void gather(const Star*, const Star* r, const KCoef& K, float* g) {
+    __device__ __forceinline__ static void gather(const Star*, const Star* r, const KCoef& K, float* g) {
         g[0] = r[0].c * K.inv_dt - K.alpha * lap<3>(r[0], K);
     }
 
     template <int AX>
-    __device__ static void bc_term(const Star* f, const float* c, const KCoef& K, float, float* g) {
+    __device__ __forceinline__ static void bc_term(const Star* f, const float* c, const KCoef& K, float, float* g) {
         float R[1];
         residual(f, c, K, R);
         g[0] = -R[0] * K.alpha * K.ih2[AX];
@@ -145,16 +145,19 @@ template <int D, bool UNSTEADY>
 struct OpNS {
     static constexpr int DIM = D, NF = D + 1, NC = UNSTEADY ? D : 0, NR = D + 1;
 
-    __device__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
+    __device__ __forceinline__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
+        float cs[D];  // c_a / (2 h_a), shared by the D momentum equations
+#pragma unroll
+        for (int a = 0; a < D; ++a) cs[a] = f[a].c * K.i2h[a];
         double div = 0.0;
 #pragma unroll
         for (int b = 0; b < D; ++b) {
-            float adv = 0.f;
+            float r = cs[0] * (f[b].p[0] - f[b].m[0]);
 #pragma unroll
-            for (int a = 0; a < D; ++a) adv += f[a].c * d1(f[b], a, K);
-            float r = adv + d1(f[D], b, K);
-            if (UNSTEADY) r += (f[b].c - c[b]) * K.inv_dt;
-            R[b] = r - K.nu * lap<D>(f[b], K);
+            for (int a = 1; a < D; ++a) r = fmaf(cs[a], f[b].p[a] - f[b].m[a], r);
+            r = fmaf(f[D].p[b] - f[D].m[b], K.i2h[b], r);
+            if (UNSTEADY) r = fmaf(f[b].c - c[b], K.inv_dt, r);
+            R[b] = fmaf(-K.nu, lap<D>(f[b], K), r);
             div = fma((double)f[b].p[b] - (double)f[b].m[b], K.i2hd[b], div);
         }
         R[D] = (float)div;
@@ -164,29 +167,28 @@ struct OpNS {
     //            + sum_a (R_q(n-e_a) c_a(n-e_a) - R_q(n+e_a) c_a(n+e_a)) / (2 h_a)
     //            + (R_div(n-e_q) - R_div(n+e_q)) / (2 h_q) - nu lap R_q(n)
     // dL/dp(n)   = sum_b (R_b(n-e_b) - R_b(n+e_b)) / (2 h_b)
-    __device__ static void gather(const Star* f, const Star* r, const KCoef& K, float* g) {
+    __device__ __forceinline__ static void gather(const Star* f, const Star* r, const KCoef& K, float* g) {
         float gp = 0.f;
 #pragma unroll
         for (int q = 0; q < D; ++q) {
-            float acc = 0.f;
+            float loc = r[0].c * (f[0].p[q] - f[0].m[q]);
 #pragma unroll
-            for (int b = 0; b < D; ++b) acc += r[b].c * d1(f[b], q, K);
-            if (UNSTEADY) acc += r[q].c * K.inv_dt;
-            float nbr = 0.f;
+            for (int b = 1; b < D; ++b) loc = fmaf(r[b].c, f[b].p[q] - f[b].m[q], loc);
+            float acc = loc * K.i2h[q];
+            if (UNSTEADY) acc = fmaf(r[q].c, K.inv_dt, acc);
 #pragma unroll
             for (int a = 0; a < D; ++a)
-                nbr += (r[q].m[a] * f[a].m[a] - r[q].p[a] * f[a].p[a]) * K.i2h[a];
-            acc += nbr;
-            acc += (r[D].m[q] - r[D].p[q]) * K.i2h[q];
-            g[q] = acc - K.nu * lap<D>(r[q], K);
-            gp += (r[q].m[q] - r[q].p[q]) * K.i2h[q];
+                acc = fmaf(fmaf(r[q].m[a], f[a].m[a], -(r[q].p[a] * f[a].p[a])), K.i2h[a], acc);
+            acc = fmaf(r[D].m[q] - r[D].p[q], K.i2h[q], acc);
+            g[q] = fmaf(-K.nu, lap<D>(r[q], K), acc);
+            gp = fmaf(r[q].m[q] - r[q].p[q], K.i2h[q], gp);
         }
         g[D] = gp;
     }
 
     // n = m + t e_AX: only the neighbour terms of R_b(m) reach n.
     template <int AX>
-    __device__ static void bc_term(const Star* f, const float* c, const KCoef& K, float t, float* g) {
+    __device__ __forceinline__ static void bc_term(const Star* f, const float* c, const KCoef& K, float t, float* g) {
         float R[NR];
         residual(f, c, K, R);
 #pragma unroll
