@@ -26,37 +26,53 @@ bool op_desc(int op, OpDesc* d) {
     }
 }
 
-// Launch geometry.  3-D: 64 x 8 column tiles (512 threads, one wavefront per
-// x-row of 64 nodes).  2-D: 256-node row segments.  Chunks of planes along axis 0
-// are sized so that a launch has about kTargetBlocks workgroups.
+// Launch geometry.  A workgroup owns a TX x TY column tile (TY = 1 for 2-D
+// grids, where a "plane" is one row) and marches a chunk of planes of axis 0.
+// 3-D grids: the chunk length is chosen once per call from the backward's
+// tiling (at least kMinBwdBlocks workgroups) and shared by the forward and the
+// backward, so that the backward, which marches each chunk top down, starts on
+// the planes the forward read last (still in the memory-side infinity cache).
+// 2-D grids: chunks sized for about kTargetBlocks2 workgroups per launch.
 #ifndef FPDE_TX3
 #define FPDE_TX3 64
 #endif
-#ifndef FPDE_TY3
-#define FPDE_TY3 8
+#ifndef FPDE_NS3_FWD_TY
+#define FPDE_NS3_FWD_TY 8
 #endif
-#ifndef FPDE_TX3_BWD
-#define FPDE_TX3_BWD 64
+#ifndef FPDE_NS3_BWD_TY
+#define FPDE_NS3_BWD_TY 16
 #endif
-#ifndef FPDE_TY3_BWD
-#define FPDE_TY3_BWD 8
+#ifndef FPDE_NS3_MIN_BWD_BLOCKS
+#define FPDE_NS3_MIN_BWD_BLOCKS 256
+#endif
+#ifndef FPDE_HEAT_FWD_TY
+#define FPDE_HEAT_FWD_TY 8
+#endif
+#ifndef FPDE_HEAT_BWD_TY
+#define FPDE_HEAT_BWD_TY 8
+#endif
+#ifndef FPDE_HEAT_MIN_BWD_BLOCKS
+#define FPDE_HEAT_MIN_BWD_BLOCKS 1024
 #endif
 #ifndef FPDE_TX2
 #define FPDE_TX2 256
 #endif
-#ifndef FPDE_BLOCKS3
-#define FPDE_BLOCKS3 512
-#endif
-#ifndef FPDE_BLOCKS3_BWD
-#define FPDE_BLOCKS3_BWD 1024
-#endif
 #ifndef FPDE_BLOCKS2
 #define FPDE_BLOCKS2 1024
 #endif
-constexpr int kTX3 = FPDE_TX3, kTY3 = FPDE_TY3, kTX3b = FPDE_TX3_BWD, kTY3b = FPDE_TY3_BWD;
-constexpr int kTX2 = FPDE_TX2;
-constexpr int kTargetBlocks3 = FPDE_BLOCKS3, kTargetBlocks3b = FPDE_BLOCKS3_BWD;
-constexpr int kTargetBlocks2 = FPDE_BLOCKS2;
+// The backward marches each chunk top-down (see above).
+#ifndef FPDE_BWD_REVERSE
+#define FPDE_BWD_REVERSE 1
+#endif
+constexpr int kTX3 = FPDE_TX3, kTX2 = FPDE_TX2, kTargetBlocks2 = FPDE_BLOCKS2;
+constexpr bool kBwdReverse = FPDE_BWD_REVERSE != 0;
+
+template <int TYF, int TYB, int MINB>
+struct Geo3 {
+    static constexpr int TXF = kTX3, TYf = TYF, TXB = kTX3, TYb = TYB, MIN_BWD_BLOCKS = MINB;
+};
+using GeoNS3 = Geo3<FPDE_NS3_FWD_TY, FPDE_NS3_BWD_TY, FPDE_NS3_MIN_BWD_BLOCKS>;
+using GeoHeat = Geo3<FPDE_HEAT_FWD_TY, FPDE_HEAT_BWD_TY, FPDE_HEAT_MIN_BWD_BLOCKS>;
 
 struct Req {
     int op;
@@ -147,21 +163,27 @@ int validate_common(int op, const fpde_grid* g, const fpde_coeffs* c, const floa
     return FPDE_OK;
 }
 
-// Tiles of TX x TY columns and chunks of planes along axis 0 such that a launch
-// has about `target` workgroups (each chunk at least one plane).
-Dims launch_dims(const Dims& n, int TX, int TY, int target) {
+// Tiles of TX x TY columns; chunks of zc planes along axis 0.
+Dims tile_dims(const Dims& n, int TX, int TY, int zc) {
     Dims dm = n;
     dm.tiles_x = (dm.nx + TX - 1) / TX;
     dm.tiles_y = (dm.ny + TY - 1) / TY;
-    const long long tiles = (long long)dm.tiles_x * dm.tiles_y;
     const int nplanes = dm.nz - 2;
+    dm.zc = zc;
+    const long long nch = (nplanes + zc - 1) / zc;
+    dm.nblocks = (int)((long long)dm.tiles_x * dm.tiles_y * nch);
+    return dm;
+}
+
+// Chunk length giving a launch with TX x TY tiles about `target` workgroups
+// (each chunk at least one plane).
+int chunk_planes(const Dims& n, int TX, int TY, int target) {
+    const long long tiles = (long long)((n.nx + TX - 1) / TX) * ((n.ny + TY - 1) / TY);
+    const int nplanes = n.nz - 2;
     long long nch = (target + tiles - 1) / tiles;
     if (nch < 1) nch = 1;
     if (nch > nplanes) nch = nplanes;
-    dm.zc = (int)((nplanes + nch - 1) / nch);
-    nch = (nplanes + dm.zc - 1) / dm.zc;
-    dm.nblocks = (int)(tiles * nch);
-    return dm;
+    return (int)((nplanes + nch - 1) / nch);
 }
 
 int check_outputs(const Req& r, const fpde_grid*, const float* const* fields,
@@ -190,8 +212,8 @@ int hip_status() {
 // ---- launches, per op type
 
 template <class OP, int TX, int TY>
-int launch_fwd(const Req& r, bool store, double* loss, int target) {
-    const Dims dm = launch_dims(r.dims, TX, TY, target);
+int launch_fwd(const Req& r, bool store, double* loss, int zc) {
+    const Dims dm = tile_dims(r.dims, TX, TY, zc);
     hipLaunchKernelGGL(fill_f64_kernel, dim3(1), dim3(1), 0, r.stream, loss, 0.0);
     if (store)
         hipLaunchKernelGGL((fwd_kernel<OP, TX, TY, true>), dim3(dm.nblocks), dim3(TX * TY), 0,
@@ -203,12 +225,19 @@ int launch_fwd(const Req& r, bool store, double* loss, int target) {
 }
 
 template <class OP, int TX, int TY>
-int launch_bwd(const Req& r, const double* dloss, int target) {
-    const Dims dm = launch_dims(r.dims, TX, TY, target);
-    hipLaunchKernelGGL((bwd_kernel<OP, TX, TY>), dim3(dm.nblocks), dim3(TX * TY), 0, r.stream,
-                       r.P, dm, r.K, dloss, r.two_over_M);
+int launch_bwd(const Req& r, const double* dloss, int zc) {
+    const Dims dm = tile_dims(r.dims, TX, TY, zc);
+    hipLaunchKernelGGL((bwd_kernel<OP, TX, TY, kBwdReverse>), dim3(dm.nblocks), dim3(TX * TY), 0,
+                       r.stream, r.P, dm, r.K, dloss, r.two_over_M);
     return hip_status();
 }
+
+// 3-D: the chunk length shared by the forward and the backward
+template <class GEO>
+int zc3(const Req& r) {
+    return chunk_planes(r.dims, GEO::TXB, GEO::TYb, GEO::MIN_BWD_BLOCKS);
+}
+int zc2(const Req& r) { return chunk_planes(r.dims, kTX2, 1, kTargetBlocks2); }
 
 template <class OP>
 int launch_bc(const Req& r, const double* dloss) {
@@ -220,33 +249,28 @@ int launch_bc(const Req& r, const double* dloss) {
     return hip_status();
 }
 
-template <class OP>
-int dispatch_fwd3(const Req& r, bool store, double* loss) {
-    return launch_fwd<OP, kTX3, kTY3>(r, store, loss, kTargetBlocks3);
-}
-template <class OP>
-int dispatch_fwd2(const Req& r, bool store, double* loss) {
-    return launch_fwd<OP, kTX2, 1>(r, store, loss, kTargetBlocks2);
-}
-
 int run_fwd(const Req& r, bool store, double* loss) {
     switch (r.op) {
-    case FPDE_BURGERS_1DT: return dispatch_fwd2<OpBurgers>(r, store, loss);
-    case FPDE_HELMHOLTZ_2D: return dispatch_fwd2<OpHelmholtz>(r, store, loss);
-    case FPDE_HEAT_3D_BE: return dispatch_fwd3<OpHeat>(r, store, loss);
-    case FPDE_NS_2D_STEADY: return dispatch_fwd2<OpNS2>(r, store, loss);
-    case FPDE_NS_3D_BE: return dispatch_fwd3<OpNS3>(r, store, loss);
+    case FPDE_BURGERS_1DT: return launch_fwd<OpBurgers, kTX2, 1>(r, store, loss, zc2(r));
+    case FPDE_HELMHOLTZ_2D: return launch_fwd<OpHelmholtz, kTX2, 1>(r, store, loss, zc2(r));
+    case FPDE_HEAT_3D_BE:
+        return launch_fwd<OpHeat, GeoHeat::TXF, GeoHeat::TYf>(r, store, loss, zc3<GeoHeat>(r));
+    case FPDE_NS_2D_STEADY: return launch_fwd<OpNS2, kTX2, 1>(r, store, loss, zc2(r));
+    case FPDE_NS_3D_BE:
+        return launch_fwd<OpNS3, GeoNS3::TXF, GeoNS3::TYf>(r, store, loss, zc3<GeoNS3>(r));
     }
     return FPDE_ERR_ARG;
 }
 
 int run_bwd(const Req& r, const double* dloss) {
     switch (r.op) {
-    case FPDE_BURGERS_1DT: return launch_bwd<OpBurgers, kTX2, 1>(r, dloss, kTargetBlocks2);
-    case FPDE_HELMHOLTZ_2D: return launch_bwd<OpHelmholtz, kTX2, 1>(r, dloss, kTargetBlocks2);
-    case FPDE_HEAT_3D_BE: return launch_bwd<OpHeat, kTX3b, kTY3b>(r, dloss, kTargetBlocks3b);
-    case FPDE_NS_2D_STEADY: return launch_bwd<OpNS2, kTX2, 1>(r, dloss, kTargetBlocks2);
-    case FPDE_NS_3D_BE: return launch_bwd<OpNS3, kTX3b, kTY3b>(r, dloss, kTargetBlocks3b);
+    case FPDE_BURGERS_1DT: return launch_bwd<OpBurgers, kTX2, 1>(r, dloss, zc2(r));
+    case FPDE_HELMHOLTZ_2D: return launch_bwd<OpHelmholtz, kTX2, 1>(r, dloss, zc2(r));
+    case FPDE_HEAT_3D_BE:
+        return launch_bwd<OpHeat, GeoHeat::TXB, GeoHeat::TYb>(r, dloss, zc3<GeoHeat>(r));
+    case FPDE_NS_2D_STEADY: return launch_bwd<OpNS2, kTX2, 1>(r, dloss, zc2(r));
+    case FPDE_NS_3D_BE:
+        return launch_bwd<OpNS3, GeoNS3::TXB, GeoNS3::TYb>(r, dloss, zc3<GeoNS3>(r));
     }
     return FPDE_ERR_ARG;
 }

@@ -40,6 +40,15 @@
 
 #include "fpde_ops.hpp"
 
+// Minimum waves per SIMD requested from the compiler for the marching kernels
+// (bounds their VGPR budget; 1 leaves the compiler free).
+#ifndef FPDE_FWD_MINW
+#define FPDE_FWD_MINW 1
+#endif
+#ifndef FPDE_BWD_MINW
+#define FPDE_BWD_MINW 1
+#endif
+
 namespace fpde {
 
 struct Ptrs {
@@ -165,100 +174,135 @@ __device__ __forceinline__ void bst(__amdgpu_buffer_rsrc_t r, uint32_t off, floa
 }
 
 // ---------------------------------------------------------------------------
-// Forward: residuals of one chunk of planes + fused sum of squares.
+// Streaming a plane region straight into LDS.  A workgroup's slot holds the
+// region's FSZ elements (tile plus halo, row-major) padded to a multiple of 64,
+// and element i is loaded by thread i mod NT in round i / NT: the 64 lanes of a
+// wave fill 64 consecutive LDS words (buffer_load_dword ... lds, M0 = the
+// wave's base).  Whether a wave takes part in a round is uniform across the
+// wave.  Elements outside the array, and the padding, carry an offset past the
+// descriptor's range and read as 0; so does a whole plane outside the grid.
 
-#ifndef FPDE_FWD_MINW
-#define FPDE_FWD_MINW 1
-#endif
-#ifndef FPDE_BWD_MINW
-#define FPDE_BWD_MINW 1
-#endif
+template <int FSZ, int NT>
+struct PlaneStream {
+    static constexpr int FSZP = (FSZ + 63) / 64 * 64;  // padded slot size (elements)
+    static constexpr int KP = (FSZP + NT - 1) / NT;     // load rounds
+    static constexpr uint32_t kOff = 0x80000000u;
+    uint32_t off[KP];  // byte offset of this thread's element in each round
+    uint32_t wl;       // first element of this wave (uniform)
+
+    // node_of(i, lin): in-plane linear node index of element i; false if outside the array
+    template <class F>
+    __device__ __forceinline__ void init(int t, F node_of) {
+        wl = __builtin_amdgcn_readfirstlane((uint32_t)(t & ~63));
+#pragma unroll
+        for (int k = 0; k < KP; ++k) {
+            const int i = t + k * NT;
+            int lin = 0;
+            const bool ok = i < FSZ && node_of(i, lin);
+            off[k] = ok ? (uint32_t)lin * 4u : kOff;
+        }
+    }
+    // queue plane pz (uniform) of the NF arrays src[0..NF) into slot base pointers
+    template <int NF>
+    __device__ __forceinline__ void load(const float* const* src, int pz, int nz, uint32_t pbytes,
+                                         float* const* dst) const {
+        const bool zok = pz >= 0 && pz < nz;
+        const uint64_t zoff = zok ? (uint64_t)pz * pbytes : 0;
+        const int nrec = zok ? (int)pbytes : 0;
+        __amdgpu_buffer_rsrc_t r[NF];
+#pragma unroll
+        for (int f = 0; f < NF; ++f)
+            r[f] = __builtin_amdgcn_make_buffer_rsrc(
+                (void*)(reinterpret_cast<const char*>(src[f]) + zoff), (short)0, nrec, 0x00020000);
+#pragma unroll
+        for (int k = 0; k < KP; ++k) {
+            // every wave takes part in the rounds that the slot fills completely
+            if ((k + 1) * NT <= FSZP || wl + k * NT < (uint32_t)FSZP) {
+#pragma unroll
+                for (int f = 0; f < NF; ++f)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                        r[f], (__attribute__((address_space(3))) void*)(dst[f] + wl + k * NT), 4,
+                        (int)off[k], 0, 0, 0);
+            }
+        }
+    }
+};
+
+// ---------------------------------------------------------------------------
+// Forward: residuals of one chunk of planes + fused sum of squares.  Each plane
+// (tile + one-node halo) streams from memory straight into a 4-slot LDS ring;
+// the 7-point star of every field is read from the slots of planes z-1, z, z+1.
+// One barrier per step: plane z+2 streams into the slot of plane z-2 while
+// plane z is evaluated.  The sum of squares is accumulated per thread in
+// float64, reduced with DPP across the wavefront and through LDS across waves,
+// then added with ONE float64 atomic per workgroup.
 
 template <class OP, int TX, int TY, bool STORE_R>
-__global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims D, KCoef K, double inv_M,
-                                                     double* loss) {
+__global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims D, KCoef K,
+                                                                    double inv_M, double* loss) {
     constexpr int DIM = OP::DIM, NF = OP::NF, NC = OP::NC, NR = OP::NR, NT = TX * TY;
     constexpr int NC1 = NC > 0 ? NC : 1;
     constexpr int HY = (DIM == 3) ? 1 : 0;
     constexpr int LY = TY + 2 * HY, LX = TX + 2;
+    using PS = PlaneStream<LY * LX, NT>;
     static_assert(DIM == 3 || TY == 1, "2-D grids use one-row tiles");
-    static_assert(Ring<TX, TY, DIM>::COUNT <= NT, "ring larger than the workgroup");
-    __shared__ float sF[2][NF][LY][LX];
+    __shared__ float sF[4][NF][PS::FSZP];
 
     const int t = threadIdx.x, tx = t % TX, ty = t / TX;
     const TileCoord tc = tile_coord<TX, TY>(D);
-    const int z0 = tc.z0, z1 = tc.z1;
+    const int z0 = tc.z0, z1 = tc.z1, L = z1 - z0;
     const int gx = tc.gx0 + tx, gy = (DIM == 3) ? tc.gy0 + ty : 0;
     const uint32_t pbytes = (uint32_t)D.ny * (uint32_t)D.nx * 4u;
     const bool inarr = gx < D.nx && gy < D.ny;
     const bool interior = gx >= 1 && gx <= D.nx - 2 && (DIM == 2 || (gy >= 1 && gy <= D.ny - 2));
     const uint32_t cb = inarr ? (uint32_t)(gy * D.nx + gx) * 4u : 0u;
 
-    // fixed halo-ring slot of this thread (if any)
-    const bool has_ring = t < Ring<TX, TY, DIM>::COUNT;
-    int rly = 0, rlx = 0;
-    if (has_ring) Ring<TX, TY, DIM>::pos(t, rly, rlx);
-    const int rgy = (DIM == 3) ? tc.gy0 - 1 + rly : 0, rgx = tc.gx0 - 1 + rlx;
-    const bool ring_in = has_ring && rgx >= 0 && rgx < D.nx && rgy >= 0 && rgy < D.ny;
-    const uint32_t rb = ring_in ? (uint32_t)(rgy * D.nx + rgx) * 4u : 0u;
-
-    // Register queue of the own column: planes z-1, z, z+1 and the prefetched
-    // z+2 live in q[(j)&3], q[(j+1)&3], q[(j+2)&3], q[(j+3)&3] at step j = z - z0;
-    // the ring values and consts of plane z (and prefetched z+1) alternate.
-    float q[4][NF], rv[2][NF], cv[2][NC1];
+    PS ps;
+    ps.init(t, [&](int i, int& lin) {
+        const int py = (DIM == 3) ? tc.gy0 - HY + i / LX : 0, px = tc.gx0 - 1 + i % LX;
+        lin = py * D.nx + px;
+        return px >= 0 && px < D.nx && py >= 0 && py < D.ny;
+    });
+    auto load_plane = [&](int pz, int slot) __attribute__((always_inline)) {
+        float* dst[NF];
 #pragma unroll
-    for (int f = 0; f < NF; ++f) {
-        const float a = bld(plane_rsrc(P.f[f], z0 - 1, pbytes), cb);
-        const float b = bld(plane_rsrc(P.f[f], z0, pbytes), cb);
-        const float c = bld(plane_rsrc(P.f[f], z0 + 1, pbytes), cb);
-        const float r = bld(plane_rsrc(P.f[f], z0, pbytes), rb);
-        q[0][f] = inarr ? a : 0.f;
-        q[1][f] = inarr ? b : 0.f;
-        q[2][f] = inarr ? c : 0.f;
-        q[3][f] = 0.f;
-        rv[0][f] = ring_in ? r : 0.f;
-        rv[1][f] = 0.f;
-    }
+        for (int f = 0; f < NF; ++f) dst[f] = &sF[slot][f][0];
+        ps.template load<NF>(P.f, pz, D.nz, pbytes, dst);
+    };
+    float cv[2][NC1];
+    auto load_consts = [&](int pz, float* c) __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < NC1; ++j) {
-        cv[0][j] = NC ? bld(plane_rsrc(P.c[j], z0, pbytes), cb) : 0.f;
-        cv[1][j] = 0.f;
-    }
+        for (int j = 0; j < NC; ++j) c[j] = bld(plane_rsrc(P.c[j], pz, pbytes), cb);
+    };
 
+    // plane z0 + j lives in slot (j + 1) & 3; prologue: planes z0-1, z0, z0+1
+    for (int j = 0; j < 3; ++j) load_plane(z0 - 1 + j, j);
+    load_consts(z0, cv[0]);
+    __syncthreads();
+
+    const int own = (ty + HY) * LX + tx + 1;  // own node in a slot
     double acc = 0.0;
-    auto step = [&](auto jc, int z) __attribute__((always_inline)) {
-        constexpr int J = decltype(jc)::value;
-        constexpr int QM = J & 3, QZ = (J + 1) & 3, QP = (J + 2) & 3, QN = (J + 3) & 3;
-        constexpr int CUR = J & 1, NXT = (J + 1) & 1, BUF = J & 1;
-#pragma unroll
-        for (int f = 0; f < NF; ++f) {
-            sF[BUF][f][ty + HY][tx + 1] = q[QZ][f];
-            if (has_ring) sF[BUF][f][rly][rlx] = rv[CUR][f];
+    auto step = [&](auto jc, int w) __attribute__((always_inline)) {
+        constexpr int J = decltype(jc)::value;  // w & 3
+        constexpr int SM = J & 3, SC = (J + 1) & 3, SP = (J + 2) & 3, SQ = (J + 3) & 3;
+        constexpr int CUR = J & 1, NXT = (J + 1) & 1;
+        const int z = z0 + w;
+        if (w + 1 < L) {
+            load_plane(z + 2, SQ);  // slot of plane z-2, last read before the previous barrier
+            load_consts(z + 1, cv[NXT]);
         }
-        if (z + 1 < z1) {  // prefetch plane z+2 of the own column, ring and consts of z+1
-#pragma unroll
-            for (int f = 0; f < NF; ++f) {
-                // branch-free: threads without a ring node load a valid address too
-                const float v = bld(plane_rsrc(P.f[f], z + 2, pbytes), cb);
-                const float w = bld(plane_rsrc(P.f[f], z + 1, pbytes), rb);
-                q[QN][f] = inarr ? v : 0.f;
-                rv[NXT][f] = ring_in ? w : 0.f;
-            }
-#pragma unroll
-            for (int j = 0; j < NC; ++j) cv[NXT][j] = bld(plane_rsrc(P.c[j], z + 1, pbytes), cb);
-        }
-        __syncthreads();
         Star s[NF];
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
-            s[f].c = q[QZ][f];
-            s[f].m[0] = q[QM][f];
-            s[f].p[0] = q[QP][f];
-            s[f].m[DIM - 1] = sF[BUF][f][ty + HY][tx];
-            s[f].p[DIM - 1] = sF[BUF][f][ty + HY][tx + 2];
+            const float* c = &sF[SC][f][own];
+            s[f].c = c[0];
+            s[f].m[0] = sF[SM][f][own];
+            s[f].p[0] = sF[SP][f][own];
+            s[f].m[DIM - 1] = c[-1];
+            s[f].p[DIM - 1] = c[1];
             if (DIM == 3) {
-                s[f].m[1] = sF[BUF][f][ty][tx + 1];
-                s[f].p[1] = sF[BUF][f][ty + 2][tx + 1];
+                s[f].m[1] = c[-LX];
+                s[f].p[1] = c[LX];
             }
         }
         float R[NR];
@@ -271,18 +315,19 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
 #pragma unroll
             for (int b = 0; b < NR; ++b) bst(plane_rsrc(P.out[b], z, pbytes), cb, R[b]);
         }
+        __syncthreads();  // (waits for the plane loads into LDS as well)
     };
 
-    int z = z0;
-    for (; z + 4 <= z1; z += 4) {  // four steps bring the queue and the buffers back
-        step(IC<0>{}, z);
-        step(IC<1>{}, z + 1);
-        step(IC<2>{}, z + 2);
-        step(IC<3>{}, z + 3);
+    int w = 0;
+    for (; w + 4 <= L; w += 4) {  // slot indices are constants in each copy
+        step(IC<0>{}, w);
+        step(IC<1>{}, w + 1);
+        step(IC<2>{}, w + 2);
+        step(IC<3>{}, w + 3);
     }
-    if (z < z1) step(IC<0>{}, z);
-    if (z + 1 < z1) step(IC<1>{}, z + 1);
-    if (z + 2 < z1) step(IC<2>{}, z + 2);
+    if (w < L) step(IC<0>{}, w);
+    if (w + 1 < L) step(IC<1>{}, w + 1);
+    if (w + 2 < L) step(IC<2>{}, w + 2);
     block_atomic_sum<NT>(acc * inv_M, loss);
 }
 
@@ -294,75 +339,47 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
 // tile; the gather at plane z reads the in-plane neighbours of R(z) from LDS and
 // R(z-1), R(z), R(z+1) of its own column from a register queue; one barrier.
 
-template <class OP, int TX, int TY>
-struct BwdGeo {
-    static constexpr int DIM = OP::DIM, NT = TX * TY;
-    static constexpr int HY = (DIM == 3) ? 2 : 0;   // field-slot halo (y)
-    static constexpr int FLY = TY + 2 * HY, FLX = TX + 4;
-    static constexpr int RHY = (DIM == 3) ? 1 : 0;  // R-tile halo (y)
-    static constexpr int RLY = TY + 2 * RHY, RLX = TX + 2;
-    static constexpr int FSZ = FLY * FLX;
-    static constexpr int KP = (FSZ + NT - 1) / NT;  // prefetch elements per thread
-};
-
-template <class OP, int TX, int TY>
+template <class OP, int TX, int TY, bool REV>
 __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims D, KCoef K,
-                                                     const double* dloss, double two_over_M) {
-    using G = BwdGeo<OP, TX, TY>;
-    constexpr int DIM = OP::DIM, NF = OP::NF, NC = OP::NC, NR = OP::NR, NT = G::NT;
+                                                                    const double* dloss,
+                                                                    double two_over_M) {
+    constexpr int DIM = OP::DIM, NF = OP::NF, NC = OP::NC, NR = OP::NR, NT = TX * TY;
     constexpr int NC1 = NC > 0 ? NC : 1;
-    constexpr int HY = G::HY, FLY = G::FLY, FLX = G::FLX, RHY = G::RHY, RLY = G::RLY,
-                  RLX = G::RLX, FSZ = G::FSZ, KP = G::KP;
+    constexpr int HY = (DIM == 3) ? 2 : 0;   // field-slot halo (y)
+    constexpr int FLY = TY + 2 * HY, FLX = TX + 4;
+    constexpr int RHY = (DIM == 3) ? 1 : 0;  // R-tile halo (y)
+    constexpr int RLY = TY + 2 * RHY, RLX = TX + 2;
+    using PS = PlaneStream<FLY * FLX, NT>;
     static_assert(DIM == 3 || TY == 1, "2-D grids use one-row tiles");
     static_assert(Ring<TX, TY, DIM>::COUNT <= NT, "ring larger than the workgroup");
-    // field planes in a 4-slot ring: plane pz lives in slot (pz - z0 + 1) & 3
-    __shared__ float sF[4][NF][FLY][FLX];
-    // residual tiles: R(zr) lives in buffer (zr - z0) & 1
-    __shared__ float sR[2][NR][RLY][RLX];
+    // The chunk [z0, z1) of axis 0 is marched in steps w = 0 .. L-1 over the
+    // physical planes ph(w) = z0 + w, or z1 - 1 - w when REV (top down).
+    // Field planes of march steps live in a 4-slot ring: step w in slot (w + 1) & 3;
+    // residual tiles: R of step w in buffer w & 1.
+    __shared__ float sF[4][NF][PS::FSZP];
+    __shared__ float sR[2][NR][RLY * RLX];
 
     const int t = threadIdx.x, tx = t % TX, ty = t / TX;
     const TileCoord tc = tile_coord<TX, TY>(D);
-    const int z0 = tc.z0, z1 = tc.z1;
+    const int z0 = tc.z0, z1 = tc.z1, L = z1 - z0;
+    auto ph = [&](int w) { return REV ? z1 - 1 - w : z0 + w; };
     const int gx = tc.gx0 + tx, gy = (DIM == 3) ? tc.gy0 + ty : 0;
     const uint32_t pbytes = (uint32_t)D.ny * (uint32_t)D.nx * 4u;
     const bool inarr = gx < D.nx && gy < D.ny;
     const uint32_t cb = inarr ? (uint32_t)(gy * D.nx + gx) * 4u : 0u;
     const float scale = (float)(two_over_M * (*dloss));
 
-    // This thread's share of a field plane (tile + 2-node halo): element
-    // i = t + k*NT of the slot, in slot order, so that the 64 lanes of a wave
-    // fill 64 consecutive LDS words.  Planes go straight from memory into LDS
-    // (buffer_load_dword ... lds); a position outside the array gets an offset
-    // past the descriptor's range, which the buffer unit reads as 0.
-    constexpr uint32_t kOff = 0x80000000u;
-    uint32_t poff[KP];
-#pragma unroll
-    for (int k = 0; k < KP; ++k) {
-        const int i = t + k * NT;
-        const int ly = i / FLX, lx = i % FLX;
-        const int py = (DIM == 3) ? tc.gy0 - HY + ly : 0, px = tc.gx0 - 2 + lx;
-        const bool ok = i < FSZ && px >= 0 && px < D.nx && py >= 0 && py < D.ny;
-        poff[k] = ok ? (uint32_t)(py * D.nx + px) * 4u : kOff;
-    }
-    const int wbase = t & ~63;  // first element of this wave in each round
-    // queue plane pz (uniform) into LDS slot `slot`; planes outside the grid read as 0
+    PS ps;
+    ps.init(t, [&](int i, int& lin) {
+        const int py = (DIM == 3) ? tc.gy0 - HY + i / FLX : 0, px = tc.gx0 - 2 + i % FLX;
+        lin = py * D.nx + px;
+        return px >= 0 && px < D.nx && py >= 0 && py < D.ny;
+    });
     auto load_plane = [&](int pz, int slot) __attribute__((always_inline)) {
-        const bool zok = pz >= 0 && pz < D.nz;
+        float* dst[NF];
 #pragma unroll
-        for (int f = 0; f < NF; ++f) {
-            const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
-                (void*)(reinterpret_cast<const char*>(P.f[f]) +
-                        (uint64_t)(zok ? pz : 0) * pbytes),
-                (short)0, zok ? (int)pbytes : 0, 0x00020000);
-#pragma unroll
-            for (int k = 0; k < KP; ++k) {
-                if (KP * NT == FSZ || t + k * NT < FSZ) {
-                    __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                        r, (__attribute__((address_space(3))) void*)(&sF[slot][f][0][0] + wbase + k * NT),
-                        4, (int)poff[k], 0, 0, 0);
-                }
-            }
-        }
+        for (int f = 0; f < NF; ++f) dst[f] = &sF[slot][f][0];
+        ps.template load<NF>(P.f, pz, D.nz, pbytes, dst);
     };
 
     // residual positions of this thread on the R tile: its own column and, for
@@ -378,22 +395,25 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
                          (DIM == 2 || (rgy >= 1 && rgy <= D.ny - 2));
     const uint32_t rcb = ring_om ? (uint32_t)(rgy * D.nx + rgx) * 4u : 0u;
 
-    // R(zr) at R-tile position (ly, lx) from field slots sm (zr-1), sc (zr), sp (zr+1);
-    // written to sR[dst] and returned in R (zero off the residual set)
-    auto r_at = [&](int zr, int sm, int sc, int sp, int dst, int ly, int lx, bool om_xy,
+    // R at physical plane zr, R-tile position (ly, lx), from the field slots of the
+    // previous (sb), same (sc) and next (sn) march steps; written to sR[dst] and
+    // returned in R (zero off the residual set)
+    auto r_at = [&](int zr, int sb, int sc, int sn, int dst, int ly, int lx, bool om_xy,
                     const float* cc, float* R) __attribute__((always_inline)) {
-        const int fy = ly + (HY - RHY), fx = lx + 1;
+        const int fi = (ly + HY - RHY) * FLX + lx + 1;  // node in a field slot
+        const int sm = REV ? sn : sb, sp = REV ? sb : sn;  // physical z-1, z+1
         Star s[NF];
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
-            s[f].c = sF[sc][f][fy][fx];
-            s[f].m[0] = sF[sm][f][fy][fx];
-            s[f].p[0] = sF[sp][f][fy][fx];
-            s[f].m[DIM - 1] = sF[sc][f][fy][fx - 1];
-            s[f].p[DIM - 1] = sF[sc][f][fy][fx + 1];
+            const float* c = &sF[sc][f][fi];
+            s[f].c = c[0];
+            s[f].m[0] = sF[sm][f][fi];
+            s[f].p[0] = sF[sp][f][fi];
+            s[f].m[DIM - 1] = c[-1];
+            s[f].p[DIM - 1] = c[1];
             if (DIM == 3) {
-                s[f].m[1] = sF[sc][f][fy - 1][fx];
-                s[f].p[1] = sF[sc][f][fy + 1][fx];
+                s[f].m[1] = c[-FLX];
+                s[f].p[1] = c[FLX];
             }
         }
         OP::residual(s, cc, K, R);
@@ -401,7 +421,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
 #pragma unroll
         for (int b = 0; b < NR; ++b) {
             R[b] = om ? R[b] : 0.f;
-            sR[dst][b][ly][lx] = R[b];
+            sR[dst][b][ly * RLX + lx] = R[b];
         }
     };
     // consts of the R-tile positions, for the plane whose residuals come next
@@ -415,99 +435,112 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
             cring[j] = bld(r, rcb);
         }
     };
-    // R(zr) on the whole R tile; the own column's values are returned in Rown
-    auto r_tile = [&](int zr, int sm, int sc, int sp, int dst, float* Rown)
+    // R on the whole R tile; the own column's values are returned in Rown
+    auto r_tile = [&](int zr, int sb, int sc, int sn, int dst, float* Rown)
                       __attribute__((always_inline)) {
-        r_at(zr, sm, sc, sp, dst, oly, olx, own_om, cown, Rown);
+        r_at(zr, sb, sc, sn, dst, oly, olx, own_om, cown, Rown);
         if (has_ring) {
             float Rr[NR];
-            r_at(zr, sm, sc, sp, dst, rly, rlx, ring_om, cring, Rr);
+            r_at(zr, sb, sc, sn, dst, rly, rlx, ring_om, cring, Rr);
         }
     };
 
-    // ---- prologue: planes z0-1 .. z0+2 in slots 0..3; R(z0) tile; the own
-    // column's R(z0-1), R(z0) and fields of plane z0-1 in registers
-    for (int j = 0; j < 4; ++j) load_plane(z0 - 1 + j, j);
+    const int fown = (ty + HY) * FLX + tx + 2;   // own node in a field slot
+    const int rown = (ty + RHY) * RLX + tx + 1;  // own node in an R tile
+
+    // ---- prologue: march steps -1 .. 2 in slots 0..3; R of step 0 on the tile;
+    // the own column's R of steps -1, 0 and fields of step -1 in registers
+    for (int j = 0; j < 4; ++j) load_plane(ph(j - 1), j);
     float fzm2[NF];
+    {
+        const int pz = ph(-2);
+        const bool zok = pz >= 0 && pz < D.nz;
 #pragma unroll
-    for (int f = 0; f < NF; ++f) {
-        const float v = bld(plane_rsrc(P.f[f], z0 >= 2 ? z0 - 2 : 0, pbytes), cb);
-        fzm2[f] = (inarr && z0 >= 2) ? v : 0.f;
+        for (int f = 0; f < NF; ++f) {
+            const float v = bld(plane_rsrc(P.f[f], zok ? pz : 0, pbytes), cb);
+            fzm2[f] = (inarr && zok) ? v : 0.f;
+        }
     }
-    load_consts(z0);
+    load_consts(ph(0));
     __syncthreads();
     float fzm[NF], rzm[NR], rzc[NR], rzp[NR];
-    r_tile(z0, 0, 1, 2, 0, rzc);
+    r_tile(ph(0), 0, 1, 2, 0, rzc);
     {
-        const int fy = ty + HY, fx = tx + 2;
         Star s[NF];
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
-            s[f].c = sF[0][f][fy][fx];
-            s[f].m[0] = fzm2[f];
-            s[f].p[0] = sF[1][f][fy][fx];
-            s[f].m[DIM - 1] = sF[0][f][fy][fx - 1];
-            s[f].p[DIM - 1] = sF[0][f][fy][fx + 1];
+            const float* c = &sF[0][f][fown];
+            const float nxt = sF[1][f][fown];
+            s[f].c = c[0];
+            s[f].m[0] = REV ? nxt : fzm2[f];
+            s[f].p[0] = REV ? fzm2[f] : nxt;
+            s[f].m[DIM - 1] = c[-1];
+            s[f].p[DIM - 1] = c[1];
             if (DIM == 3) {
-                s[f].m[1] = sF[0][f][fy - 1][fx];
-                s[f].p[1] = sF[0][f][fy + 1][fx];
+                s[f].m[1] = c[-FLX];
+                s[f].p[1] = c[FLX];
             }
             fzm[f] = s[f].c;
         }
+        const int pz = ph(-1);  // in [0, nz): z0 - 1 >= 0 and z1 <= nz - 1
         float cc[NC1];
 #pragma unroll
-        for (int j = 0; j < NC; ++j) cc[j] = bld(plane_rsrc(P.c[j], z0 - 1, pbytes), cb);
+        for (int j = 0; j < NC; ++j) cc[j] = bld(plane_rsrc(P.c[j], pz, pbytes), cb);
         OP::residual(s, cc, K, rzm);
-        const bool om = own_om && z0 - 1 >= 1;
+        const bool om = own_om && pz >= 1 && pz <= D.nz - 2;
 #pragma unroll
         for (int b = 0; b < NR; ++b) rzm[b] = om ? rzm[b] : 0.f;
     }
-    load_consts(z0 + 1);
+    load_consts(ph(1));  // step 0 evaluates R of step 1 (in range for L >= 1)
     __syncthreads();
 
-    // ---- march.  Step z: issue the loads of plane z+3; R(z+1) on the R tile; the
-    // gather at plane z; plane z+3 into the slot of plane z-1; one barrier.  Every
-    // LDS buffer a step writes was last read before the previous step's barrier.
-    auto step = [&](auto jc, int z) __attribute__((always_inline)) {
-        constexpr int J = decltype(jc)::value;  // (z - z0) & 3
-        // field slots of planes z-1 (reused for z+3), z, z+1, z+2; R tiles of R(z), R(z+1)
-        constexpr int SM = J & 3, SC = (J + 1) & 3, SP = (J + 2) & 3, SQ = (J + 3) & 3;
-        constexpr int RC = J & 1, RP = (J + 1) & 1;
-        const bool more = z + 1 < z1;
-        if (more) load_plane(z + 3, SM);  // the slot of plane z-1, unread in this step
-        r_tile(z + 1, SC, SP, SQ, RP, rzp);
-        if (more) load_consts(z + 2);
-        const int fy = ty + HY, fx = tx + 2, ry = ty + RHY, rx = tx + 1;
+    // ---- march.  Step w: issue the loads of step w+3; R of step w+1 on the R tile;
+    // the gather at step w; step w+3's plane goes to the slot of step w-1; one
+    // barrier.  Every LDS buffer a step writes was last read before the previous
+    // step's barrier.
+    auto step = [&](auto jc, int w) __attribute__((always_inline)) {
+        constexpr int J = decltype(jc)::value;  // w & 3
+        // field slots of steps w-1 (reused for w+3), w, w+1, w+2; R tiles of w, w+1
+        constexpr int SB = J & 3, SC = (J + 1) & 3, SN = (J + 2) & 3, SQ = (J + 3) & 3;
+        constexpr int RC = J & 1, RN = (J + 1) & 1;
+        const bool more = w + 1 < L;
+        if (more) load_plane(ph(w + 3), SB);  // the slot of step w-1, unread in this step
+        r_tile(ph(w + 1), SC, SN, SQ, RN, rzp);
+        if (more) load_consts(ph(w + 2));  // step w+1 evaluates R of step w+2 (<= L: in range)
         Star fs[NF], rs[NR];
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
-            fs[f].c = sF[SC][f][fy][fx];
-            fs[f].m[0] = fzm[f];
-            fs[f].p[0] = sF[SP][f][fy][fx];
-            fs[f].m[DIM - 1] = sF[SC][f][fy][fx - 1];
-            fs[f].p[DIM - 1] = sF[SC][f][fy][fx + 1];
+            const float* c = &sF[SC][f][fown];
+            const float fnext = sF[SN][f][fown];
+            fs[f].c = c[0];
+            fs[f].m[0] = REV ? fnext : fzm[f];
+            fs[f].p[0] = REV ? fzm[f] : fnext;
+            fs[f].m[DIM - 1] = c[-1];
+            fs[f].p[DIM - 1] = c[1];
             if (DIM == 3) {
-                fs[f].m[1] = sF[SC][f][fy - 1][fx];
-                fs[f].p[1] = sF[SC][f][fy + 1][fx];
+                fs[f].m[1] = c[-FLX];
+                fs[f].p[1] = c[FLX];
             }
         }
 #pragma unroll
         for (int b = 0; b < NR; ++b) {
+            const float* c = &sR[RC][b][rown];
             rs[b].c = rzc[b];
-            rs[b].m[0] = rzm[b];
-            rs[b].p[0] = rzp[b];
-            rs[b].m[DIM - 1] = sR[RC][b][ry][rx - 1];
-            rs[b].p[DIM - 1] = sR[RC][b][ry][rx + 1];
+            rs[b].m[0] = REV ? rzp[b] : rzm[b];
+            rs[b].p[0] = REV ? rzm[b] : rzp[b];
+            rs[b].m[DIM - 1] = c[-1];
+            rs[b].p[DIM - 1] = c[1];
             if (DIM == 3) {
-                rs[b].m[1] = sR[RC][b][ry - 1][rx];
-                rs[b].p[1] = sR[RC][b][ry + 1][rx];
+                rs[b].m[1] = c[-RLX];
+                rs[b].p[1] = c[RLX];
             }
         }
         float g[NF];
         OP::gather(fs, rs, K, g);
         if (inarr) {
+            const int pz = ph(w);
 #pragma unroll
-            for (int f = 0; f < NF; ++f) bst(plane_rsrc(P.out[f], z, pbytes), cb, scale * g[f]);
+            for (int f = 0; f < NF; ++f) bst(plane_rsrc(P.out[f], pz, pbytes), cb, scale * g[f]);
         }
 #pragma unroll
         for (int f = 0; f < NF; ++f) fzm[f] = fs[f].c;
@@ -519,16 +552,16 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
         __syncthreads();  // (waits for the plane loads into LDS as well)
     };
 
-    int z = z0;
-    for (; z + 4 <= z1; z += 4) {  // slot and buffer indices are constants in each copy
-        step(IC<0>{}, z);
-        step(IC<1>{}, z + 1);
-        step(IC<2>{}, z + 2);
-        step(IC<3>{}, z + 3);
+    int w = 0;
+    for (; w + 4 <= L; w += 4) {  // slot and buffer indices are constants in each copy
+        step(IC<0>{}, w);
+        step(IC<1>{}, w + 1);
+        step(IC<2>{}, w + 2);
+        step(IC<3>{}, w + 3);
     }
-    if (z < z1) step(IC<0>{}, z);
-    if (z + 1 < z1) step(IC<1>{}, z + 1);
-    if (z + 2 < z1) step(IC<2>{}, z + 2);
+    if (w < L) step(IC<0>{}, w);
+    if (w + 1 < L) step(IC<1>{}, w + 1);
+    if (w + 2 < L) step(IC<2>{}, w + 2);
 }
 
 // ---------------------------------------------------------------------------

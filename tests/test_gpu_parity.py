@@ -29,6 +29,10 @@ SMALL = [
     ("ns_2d", (3, 3)), ("ns_2d", (6, 257)), ("ns_2d", (71, 600)), ("ns_2d", (300, 257)),
     ("ns_3d_tgv", (3, 3, 3)), ("ns_3d_tgv", (4, 9, 66)), ("ns_3d_tgv", (19, 21, 70)),
     ("ns_3d_tgv", (40, 17, 129)),
+    # full-width planes: several chunks of several planes each along axis 0, so
+    # the unrolled march, its tail and the seams between chunks are all exercised
+    ("heat_3d", (42, 256, 256)), ("ns_3d_tgv", (42, 256, 256)), ("ns_3d_tgv", (75, 130, 200)),
+    ("ns_2d", (700, 513)),
 ]
 
 
