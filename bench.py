@@ -72,6 +72,28 @@ def copy_gbps(torch, nbytes=1 << 30, reps=20):
     return 2 * nbytes / s / 1e9
 
 
+OP_KERNEL_TAG = {1: "OpBurgers", 2: "OpHelmholtz", 3: "OpHeat", 4: "OpNS<2, false>",
+                 5: "OpNS<3, true>"}
+
+
+def measured_traffic(cfg, op, kernel):
+    """HBM bytes per launch of `kernel` ("fwd"/"bwd") from the committed rocprofv3
+    counter summary, if it was taken on this workload with the current kernel
+    sources; else None."""
+    from paper_2607_18020_amd import profiling  # noqa: PLC0415
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("source_hash") != profiling.source_hash() or not rec.get("workload", "").startswith(cfg):
+        return None
+    prefix = f"{kernel}_kernel<{OP_KERNEL_TAG[op]}"
+    for name, v in rec.get("kernels", {}).items():
+        if name.startswith(prefix):
+            return round(v["fetch_bytes"] + v["write_bytes"])
+    return None
+
+
 def cpu_baseline(W, wl_full, cfg, seed, planes):
     """The oracle (single thread, float64) on a slab of the same workload."""
     import numpy as np  # noqa: PLC0415
@@ -168,7 +190,7 @@ def main():
     achieved = bm[dom] / (per[dom] * 1e-6) / 1e9
     roofline = {"bound": "hbm", "kernel": f"{dom} ({cfg})", "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                "traffic": None,
+                "traffic": measured_traffic(cfg, wl.op, dom),
                 "algorithmic_bytes_per_launch": bm[dom], "avg_launch_us": round(per[dom], 2)}
     cpu = None
     if not args.no_cpu_baseline:
