@@ -158,6 +158,20 @@ __device__ __forceinline__ TileCoord tile_coord(const Dims& D) {
 template <int V>
 using IC = std::integral_constant<int, V>;
 
+// The LDS ring slots are four distinct __shared__ arrays, picked by a
+// compile-time index.  Distinct objects let the compiler see that a slot being
+// filled by buffer_load ... lds is not one being read, so the reads of a step
+// do not wait for the plane that the same step queues.
+#define FPDE_SLOT_RING(T, NAME, D1, D2)                                              \
+    __shared__ T NAME##0[D1][D2], NAME##1[D1][D2], NAME##2[D1][D2], NAME##3[D1][D2]; \
+    auto NAME = [&](auto sc) __attribute__((always_inline)) -> T(*)[D2] {            \
+        constexpr int S_ = decltype(sc)::value & 3;                                  \
+        if constexpr (S_ == 0) return NAME##0;                                       \
+        else if constexpr (S_ == 1) return NAME##1;                                  \
+        else if constexpr (S_ == 2) return NAME##2;                                  \
+        else return NAME##3;                                                         \
+    }
+
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t plane_rsrc(const float* p, int z,
                                                              uint32_t pbytes) {
     return __builtin_amdgcn_make_buffer_rsrc(
@@ -246,7 +260,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
     constexpr int LY = TY + 2 * HY, LX = TX + 2;
     using PS = PlaneStream<LY * LX, NT>;
     static_assert(DIM == 3 || TY == 1, "2-D grids use one-row tiles");
-    __shared__ float sF[4][NF][PS::FSZP];
+    FPDE_SLOT_RING(float, sF, NF, PS::FSZP);
 
     const int t = threadIdx.x, tx = t % TX, ty = t / TX;
     const TileCoord tc = tile_coord<TX, TY>(D);
@@ -263,10 +277,10 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
         lin = py * D.nx + px;
         return px >= 0 && px < D.nx && py >= 0 && py < D.ny;
     });
-    auto load_plane = [&](int pz, int slot) __attribute__((always_inline)) {
+    auto load_plane = [&](int pz, auto slot) __attribute__((always_inline)) {
         float* dst[NF];
 #pragma unroll
-        for (int f = 0; f < NF; ++f) dst[f] = &sF[slot][f][0];
+        for (int f = 0; f < NF; ++f) dst[f] = &sF(slot)[f][0];
         ps.template load<NF>(P.f, pz, D.nz, pbytes, dst);
     };
     float cv[2][NC1];
@@ -276,7 +290,9 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
     };
 
     // plane z0 + j lives in slot (j + 1) & 3; prologue: planes z0-1, z0, z0+1
-    for (int j = 0; j < 3; ++j) load_plane(z0 - 1 + j, j);
+    load_plane(z0 - 1, IC<0>{});
+    load_plane(z0, IC<1>{});
+    load_plane(z0 + 1, IC<2>{});
     load_consts(z0, cv[0]);
     __syncthreads();
 
@@ -288,16 +304,16 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
         constexpr int CUR = J & 1, NXT = (J + 1) & 1;
         const int z = z0 + w;
         if (w + 1 < L) {
-            load_plane(z + 2, SQ);  // slot of plane z-2, last read before the previous barrier
+            load_plane(z + 2, IC<SQ>{});  // slot of plane z-2, last read before the previous barrier
             load_consts(z + 1, cv[NXT]);
         }
         Star s[NF];
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
-            const float* c = &sF[SC][f][own];
+            const float* c = &sF(IC<SC>{})[f][own];
             s[f].c = c[0];
-            s[f].m[0] = sF[SM][f][own];
-            s[f].p[0] = sF[SP][f][own];
+            s[f].m[0] = sF(IC<SM>{})[f][own];
+            s[f].p[0] = sF(IC<SP>{})[f][own];
             s[f].m[DIM - 1] = c[-1];
             s[f].p[DIM - 1] = c[1];
             if (DIM == 3) {
@@ -356,7 +372,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     // physical planes ph(w) = z0 + w, or z1 - 1 - w when REV (top down).
     // Field planes of march steps live in a 4-slot ring: step w in slot (w + 1) & 3;
     // residual tiles: R of step w in buffer w & 1.
-    __shared__ float sF[4][NF][PS::FSZP];
+    FPDE_SLOT_RING(float, sF, NF, PS::FSZP);
     __shared__ float sR[2][NR][RLY * RLX];
 
     const int t = threadIdx.x, tx = t % TX, ty = t / TX;
@@ -375,10 +391,10 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
         lin = py * D.nx + px;
         return px >= 0 && px < D.nx && py >= 0 && py < D.ny;
     });
-    auto load_plane = [&](int pz, int slot) __attribute__((always_inline)) {
+    auto load_plane = [&](int pz, auto slot) __attribute__((always_inline)) {
         float* dst[NF];
 #pragma unroll
-        for (int f = 0; f < NF; ++f) dst[f] = &sF[slot][f][0];
+        for (int f = 0; f < NF; ++f) dst[f] = &sF(slot)[f][0];
         ps.template load<NF>(P.f, pz, D.nz, pbytes, dst);
     };
 
@@ -398,17 +414,17 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     // R at physical plane zr, R-tile position (ly, lx), from the field slots of the
     // previous (sb), same (sc) and next (sn) march steps; written to sR[dst] and
     // returned in R (zero off the residual set)
-    auto r_at = [&](int zr, int sb, int sc, int sn, int dst, int ly, int lx, bool om_xy,
+    auto r_at = [&](int zr, auto sb, auto sc, auto sn, int dst, int ly, int lx, bool om_xy,
                     const float* cc, float* R) __attribute__((always_inline)) {
         const int fi = (ly + HY - RHY) * FLX + lx + 1;  // node in a field slot
-        const int sm = REV ? sn : sb, sp = REV ? sb : sn;  // physical z-1, z+1
         Star s[NF];
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
-            const float* c = &sF[sc][f][fi];
+            const float* c = &sF(sc)[f][fi];
+            const float vb = sF(sb)[f][fi], vn = sF(sn)[f][fi];
             s[f].c = c[0];
-            s[f].m[0] = sF[sm][f][fi];
-            s[f].p[0] = sF[sp][f][fi];
+            s[f].m[0] = REV ? vn : vb;  // physical z-1, z+1
+            s[f].p[0] = REV ? vb : vn;
             s[f].m[DIM - 1] = c[-1];
             s[f].p[DIM - 1] = c[1];
             if (DIM == 3) {
@@ -436,7 +452,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
         }
     };
     // R on the whole R tile; the own column's values are returned in Rown
-    auto r_tile = [&](int zr, int sb, int sc, int sn, int dst, float* Rown)
+    auto r_tile = [&](int zr, auto sb, auto sc, auto sn, int dst, float* Rown)
                       __attribute__((always_inline)) {
         r_at(zr, sb, sc, sn, dst, oly, olx, own_om, cown, Rown);
         if (has_ring) {
@@ -450,7 +466,10 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
 
     // ---- prologue: march steps -1 .. 2 in slots 0..3; R of step 0 on the tile;
     // the own column's R of steps -1, 0 and fields of step -1 in registers
-    for (int j = 0; j < 4; ++j) load_plane(ph(j - 1), j);
+    load_plane(ph(-1), IC<0>{});
+    load_plane(ph(0), IC<1>{});
+    load_plane(ph(1), IC<2>{});
+    load_plane(ph(2), IC<3>{});
     float fzm2[NF];
     {
         const int pz = ph(-2);
@@ -464,13 +483,13 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     load_consts(ph(0));
     __syncthreads();
     float fzm[NF], rzm[NR], rzc[NR], rzp[NR];
-    r_tile(ph(0), 0, 1, 2, 0, rzc);
+    r_tile(ph(0), IC<0>{}, IC<1>{}, IC<2>{}, 0, rzc);
     {
         Star s[NF];
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
-            const float* c = &sF[0][f][fown];
-            const float nxt = sF[1][f][fown];
+            const float* c = &sF(IC<0>{})[f][fown];
+            const float nxt = sF(IC<1>{})[f][fown];
             s[f].c = c[0];
             s[f].m[0] = REV ? nxt : fzm2[f];
             s[f].p[0] = REV ? fzm2[f] : nxt;
@@ -504,14 +523,14 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
         constexpr int SB = J & 3, SC = (J + 1) & 3, SN = (J + 2) & 3, SQ = (J + 3) & 3;
         constexpr int RC = J & 1, RN = (J + 1) & 1;
         const bool more = w + 1 < L;
-        if (more) load_plane(ph(w + 3), SB);  // the slot of step w-1, unread in this step
-        r_tile(ph(w + 1), SC, SN, SQ, RN, rzp);
+        if (more) load_plane(ph(w + 3), IC<SB>{});  // the slot of step w-1, unread in this step
+        r_tile(ph(w + 1), IC<SC>{}, IC<SN>{}, IC<SQ>{}, RN, rzp);
         if (more) load_consts(ph(w + 2));  // step w+1 evaluates R of step w+2 (<= L: in range)
         Star fs[NF], rs[NR];
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
-            const float* c = &sF[SC][f][fown];
-            const float fnext = sF[SN][f][fown];
+            const float* c = &sF(IC<SC>{})[f][fown];
+            const float fnext = sF(IC<SN>{})[f][fown];
             fs[f].c = c[0];
             fs[f].m[0] = REV ? fnext : fzm[f];
             fs[f].p[0] = REV ? fzm[f] : fnext;
