@@ -172,12 +172,37 @@ using IC = std::integral_constant<int, V>;
         else return NAME##3;                                                         \
     }
 
+// Descriptor words must sit in SGPRs.  Their inputs are wave-uniform by
+// construction (kernel arguments and march counters), but after control flow
+// joins the compiler can lose track of that and wrap each load in a
+// readfirstlane loop; rebuilding the base and the size from lane 0 keeps the
+// descriptor scalar.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void* base, int nbytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    // (readfirstlane returns int: widen through uint32_t, not by sign extension)
+    const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a);
+    const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+    return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(hi << 32 | lo), (short)0,
+                                             __builtin_amdgcn_readfirstlane(nbytes), 0x00020000);
+}
+
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t plane_rsrc(const float* p, int z,
                                                              uint32_t pbytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(reinterpret_cast<const char*>(p) + (uint64_t)z * pbytes), (short)0, (int)pbytes,
-        0x00020000);
+    return uniform_rsrc(reinterpret_cast<const char*>(p) + (uint64_t)z * pbytes, (int)pbytes);
 }
+
+// Plane z if ok, else an empty range: every access through it reads 0 and
+// fetches nothing.  Keeps a step's memory operations unconditional, so that
+// the number of them in flight does not depend on the path taken.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t plane_rsrc_if(const float* p, int z,
+                                                                uint32_t pbytes, bool ok) {
+    return uniform_rsrc(reinterpret_cast<const char*>(p) + (ok ? (uint64_t)z * pbytes : 0),
+                        ok ? (int)pbytes : 0);
+}
+
+// A store offset past every plane's range (planes hold fewer than 2^29 nodes):
+// the hardware drops such a store.
+constexpr uint32_t kDropOff = 0x80000000u;
 
 __device__ __forceinline__ float bld(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
@@ -226,8 +251,7 @@ struct PlaneStream {
         __amdgpu_buffer_rsrc_t r[NF];
 #pragma unroll
         for (int f = 0; f < NF; ++f)
-            r[f] = __builtin_amdgcn_make_buffer_rsrc(
-                (void*)(reinterpret_cast<const char*>(src[f]) + zoff), (short)0, nrec, 0x00020000);
+            r[f] = uniform_rsrc(reinterpret_cast<const char*>(src[f]) + zoff, nrec);
 #pragma unroll
         for (int k = 0; k < KP; ++k) {
             // every wave takes part in the rounds that the slot fills completely
@@ -284,16 +308,16 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
         ps.template load<NF>(P.f, pz, D.nz, pbytes, dst);
     };
     float cv[2][NC1];
-    auto load_consts = [&](int pz, float* c) __attribute__((always_inline)) {
+    auto load_consts = [&](int pz, bool ok, float* c) __attribute__((always_inline)) {
 #pragma unroll
-        for (int j = 0; j < NC; ++j) c[j] = bld(plane_rsrc(P.c[j], pz, pbytes), cb);
+        for (int j = 0; j < NC; ++j) c[j] = bld(plane_rsrc_if(P.c[j], pz, pbytes, ok), cb);
     };
 
     // plane z0 + j lives in slot (j + 1) & 3; prologue: planes z0-1, z0, z0+1
     load_plane(z0 - 1, IC<0>{});
     load_plane(z0, IC<1>{});
     load_plane(z0 + 1, IC<2>{});
-    load_consts(z0, cv[0]);
+    load_consts(z0, true, cv[0]);
     __syncthreads();
 
     const int own = (ty + HY) * LX + tx + 1;  // own node in a slot
@@ -303,10 +327,10 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
         constexpr int SM = J & 3, SC = (J + 1) & 3, SP = (J + 2) & 3, SQ = (J + 3) & 3;
         constexpr int CUR = J & 1, NXT = (J + 1) & 1;
         const int z = z0 + w;
-        if (w + 1 < L) {
-            load_plane(z + 2, IC<SQ>{});  // slot of plane z-2, last read before the previous barrier
-            load_consts(z + 1, cv[NXT]);
-        }
+        const bool more = w + 1 < L;
+        // plane z+2 goes to the slot of plane z-2, last read before the previous barrier
+        load_plane(more ? z + 2 : -1, IC<SQ>{});
+        load_consts(z + 1, more, cv[NXT]);
         Star s[NF];
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
@@ -327,9 +351,10 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
 #pragma unroll
         for (int b = 0; b < NR; ++b) ss = fmaf(R[b], R[b], ss);
         acc += (double)(interior ? ss : 0.f);
-        if (STORE_R && interior) {
+        if (STORE_R) {
+            const uint32_t so = interior ? cb : kDropOff;
 #pragma unroll
-            for (int b = 0; b < NR; ++b) bst(plane_rsrc(P.out[b], z, pbytes), cb, R[b]);
+            for (int b = 0; b < NR; ++b) bst(plane_rsrc(P.out[b], z, pbytes), so, R[b]);
         }
         __syncthreads();  // (waits for the plane loads into LDS as well)
     };
@@ -443,10 +468,10 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     // consts of the R-tile positions, for the plane whose residuals come next
     // (loaded one step ahead so that their latency hides behind a step)
     float cown[NC1], cring[NC1];
-    auto load_consts = [&](int zr) __attribute__((always_inline)) {  // zr uniform, in range
+    auto load_consts = [&](int zr, bool ok) __attribute__((always_inline)) {  // zr uniform
 #pragma unroll
         for (int j = 0; j < NC; ++j) {
-            const __amdgpu_buffer_rsrc_t r = plane_rsrc(P.c[j], zr, pbytes);
+            const __amdgpu_buffer_rsrc_t r = plane_rsrc_if(P.c[j], zr, pbytes, ok);
             cown[j] = bld(r, cb);
             cring[j] = bld(r, rcb);
         }
@@ -480,7 +505,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
             fzm2[f] = (inarr && zok) ? v : 0.f;
         }
     }
-    load_consts(ph(0));
+    load_consts(ph(0), true);
     __syncthreads();
     float fzm[NF], rzm[NR], rzc[NR], rzp[NR];
     r_tile(ph(0), IC<0>{}, IC<1>{}, IC<2>{}, 0, rzc);
@@ -510,7 +535,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
 #pragma unroll
         for (int b = 0; b < NR; ++b) rzm[b] = om ? rzm[b] : 0.f;
     }
-    load_consts(ph(1));  // step 0 evaluates R of step 1 (in range for L >= 1)
+    load_consts(ph(1), true);  // step 0 evaluates R of step 1 (in range for L >= 1)
     __syncthreads();
 
     // ---- march.  Step w: issue the loads of step w+3; R of step w+1 on the R tile;
@@ -523,9 +548,11 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
         constexpr int SB = J & 3, SC = (J + 1) & 3, SN = (J + 2) & 3, SQ = (J + 3) & 3;
         constexpr int RC = J & 1, RN = (J + 1) & 1;
         const bool more = w + 1 < L;
-        if (more) load_plane(ph(w + 3), IC<SB>{});  // the slot of step w-1, unread in this step
+        // step w+3's plane goes to the slot of step w-1, unread in this step; an
+        // empty plane after the chunk's last step
+        load_plane(more ? ph(w + 3) : -1, IC<SB>{});
         r_tile(ph(w + 1), IC<SC>{}, IC<SN>{}, IC<SQ>{}, RN, rzp);
-        if (more) load_consts(ph(w + 2));  // step w+1 evaluates R of step w+2 (<= L: in range)
+        load_consts(ph(w + 2), more);  // step w+1 evaluates R of step w+2 (<= L: in range)
         Star fs[NF], rs[NR];
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
@@ -556,10 +583,11 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
         }
         float g[NF];
         OP::gather(fs, rs, K, g);
-        if (inarr) {
+        {
             const int pz = ph(w);
+            const uint32_t so = inarr ? cb : kDropOff;
 #pragma unroll
-            for (int f = 0; f < NF; ++f) bst(plane_rsrc(P.out[f], pz, pbytes), cb, scale * g[f]);
+            for (int f = 0; f < NF; ++f) bst(plane_rsrc(P.out[f], pz, pbytes), so, scale * g[f]);
         }
 #pragma unroll
         for (int f = 0; f < NF; ++f) fzm[f] = fs[f].c;
