@@ -212,6 +212,17 @@ __device__ __forceinline__ void bst(__amdgpu_buffer_rsrc_t r, uint32_t off, floa
     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)off, 0, 0);
 }
 
+// An opaque copy of v, made once per march step.  LDS addresses derived from it
+// are recomputed in the step (one add each) instead of being hoisted out of the
+// march: with buffers beyond the 64 KB reach of a ds_read offset, the hoisted
+// addresses would hold many VGPRs for the whole loop.  Only when LDS_BYTES, the
+// kernel's LDS footprint, exceeds that reach (else v itself).
+template <int LDS_BYTES>
+__device__ __forceinline__ int fresh(int v) {
+    if constexpr (LDS_BYTES > 65536) asm volatile("" : "+v"(v));
+    return v;
+}
+
 // ---------------------------------------------------------------------------
 // Streaming a plane region straight into LDS.  A workgroup's slot holds the
 // region's FSZ elements (tile plus halo, row-major) padded to a multiple of 64,
@@ -385,7 +396,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
                                                                     const double* dloss,
                                                                     double two_over_M) {
     constexpr int DIM = OP::DIM, NF = OP::NF, NC = OP::NC, NR = OP::NR, NT = TX * TY;
-    constexpr int NC1 = NC > 0 ? NC : 1;
+    constexpr int NC1 = NC > 0 ? NC : 1, NG = OP::NG, NG1 = NG > 0 ? NG : 1;
     constexpr int HY = (DIM == 3) ? 2 : 0;   // field-slot halo (y)
     constexpr int FLY = TY + 2 * HY, FLX = TX + 4;
     constexpr int RHY = (DIM == 3) ? 1 : 0;  // R-tile halo (y)
@@ -399,6 +410,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     // residual tiles: R of step w in buffer w & 1.
     FPDE_SLOT_RING(float, sF, NF, PS::FSZP);
     __shared__ float sR[2][NR][RLY * RLX];
+    constexpr int kLds = (4 * NF * PS::FSZP + 2 * NR * RLY * RLX) * 4;
 
     const int t = threadIdx.x, tx = t % TX, ty = t / TX;
     const TileCoord tc = tile_coord<TX, TY>(D);
@@ -436,12 +448,12 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
                          (DIM == 2 || (rgy >= 1 && rgy <= D.ny - 2));
     const uint32_t rcb = ring_om ? (uint32_t)(rgy * D.nx + rgx) * 4u : 0u;
 
-    // R at physical plane zr, R-tile position (ly, lx), from the field slots of the
-    // previous (sb), same (sc) and next (sn) march steps; written to sR[dst] and
-    // returned in R (zero off the residual set)
-    auto r_at = [&](int zr, auto sb, auto sc, auto sn, int dst, int ly, int lx, bool om_xy,
-                    const float* cc, float* R) __attribute__((always_inline)) {
-        const int fi = (ly + HY - RHY) * FLX + lx + 1;  // node in a field slot
+    // R at physical plane zr, at node fi of a field slot and ri of an R tile, from
+    // the field slots of the previous (sb), same (sc) and next (sn) march steps;
+    // written to sR[dst] and returned in R (zero off the residual set); with S,
+    // also the gather's self terms at that node
+    auto r_at = [&](int zr, auto sb, auto sc, auto sn, int dst, int fi, int ri, bool om_xy,
+                    const float* cc, float* R, float* S) __attribute__((always_inline)) {
         Star s[NF];
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
@@ -462,8 +474,9 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
 #pragma unroll
         for (int b = 0; b < NR; ++b) {
             R[b] = om ? R[b] : 0.f;
-            sR[dst][b][ly * RLX + lx] = R[b];
+            sR[dst][b][ri] = R[b];
         }
+        if (S) OP::gather_self(s, R, K, S);
     };
     // consts of the R-tile positions, for the plane whose residuals come next
     // (loaded one step ahead so that their latency hides behind a step)
@@ -477,17 +490,22 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
         }
     };
     // R on the whole R tile; the own column's values are returned in Rown
-    auto r_tile = [&](int zr, auto sb, auto sc, auto sn, int dst, float* Rown)
-                      __attribute__((always_inline)) {
-        r_at(zr, sb, sc, sn, dst, oly, olx, own_om, cown, Rown);
-        if (has_ring) {
-            float Rr[NR];
-            r_at(zr, sb, sc, sn, dst, rly, rlx, ring_om, cring, Rr);
-        }
-    };
-
     const int fown = (ty + HY) * FLX + tx + 2;   // own node in a field slot
     const int rown = (ty + RHY) * RLX + tx + 1;  // own node in an R tile
+    const int fring = (rly + HY - RHY) * FLX + rlx + 1, rring = rly * RLX + rlx;  // ring node
+    (void)oly;
+    (void)olx;
+
+    // R on the whole R tile; the own column's R and gather self terms are returned
+    // in Rown, Sown.  fo, ro, fr, rr: a step's copies of fown, rown, fring, rring
+    auto r_tile = [&](int zr, auto sb, auto sc, auto sn, int dst, float* Rown, float* Sown, int fo,
+                      int ro, int fr, int rr) __attribute__((always_inline)) {
+        r_at(zr, sb, sc, sn, dst, fo, ro, own_om, cown, Rown, Sown);
+        if (has_ring) {
+            float Rr[NR];
+            r_at(zr, sb, sc, sn, dst, fr, rr, ring_om, cring, Rr, nullptr);
+        }
+    };
 
     // ---- prologue: march steps -1 .. 2 in slots 0..3; R of step 0 on the tile;
     // the own column's R of steps -1, 0 and fields of step -1 in registers
@@ -507,8 +525,10 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     }
     load_consts(ph(0), true);
     __syncthreads();
-    float fzm[NF], rzm[NR], rzc[NR], rzp[NR];
-    r_tile(ph(0), IC<0>{}, IC<1>{}, IC<2>{}, 0, rzc);
+    // own column: fields of the previous step; R of the previous, current and next
+    // steps; gather self terms of the current and next steps
+    float fzm[NF], rzm[NR], rzc[NR], rzp[NR], sgc[NG1], sgp[NG1];
+    r_tile(ph(0), IC<0>{}, IC<1>{}, IC<2>{}, 0, rzc, sgc, fown, rown, fring, rring);
     {
         Star s[NF];
 #pragma unroll
@@ -551,13 +571,16 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
         // step w+3's plane goes to the slot of step w-1, unread in this step; an
         // empty plane after the chunk's last step
         load_plane(more ? ph(w + 3) : -1, IC<SB>{});
-        r_tile(ph(w + 1), IC<SC>{}, IC<SN>{}, IC<SQ>{}, RN, rzp);
+        const int fos = fown, ros = rown;
+        // (the ring's addresses, used by a few waves only, are not held across the march)
+        r_tile(ph(w + 1), IC<SC>{}, IC<SN>{}, IC<SQ>{}, RN, rzp, sgp, fos, ros, fresh<kLds>(fring),
+               fresh<kLds>(rring));
         load_consts(ph(w + 2), more);  // step w+1 evaluates R of step w+2 (<= L: in range)
         Star fs[NF], rs[NR];
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
-            const float* c = &sF(IC<SC>{})[f][fown];
-            const float fnext = sF(IC<SN>{})[f][fown];
+            const float* c = &sF(IC<SC>{})[f][fos];
+            const float fnext = sF(IC<SN>{})[f][fos];
             fs[f].c = c[0];
             fs[f].m[0] = REV ? fnext : fzm[f];
             fs[f].p[0] = REV ? fzm[f] : fnext;
@@ -570,7 +593,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
         }
 #pragma unroll
         for (int b = 0; b < NR; ++b) {
-            const float* c = &sR[RC][b][rown];
+            const float* c = &sR[RC][b][ros];
             rs[b].c = rzc[b];
             rs[b].m[0] = REV ? rzp[b] : rzm[b];
             rs[b].p[0] = REV ? rzm[b] : rzp[b];
@@ -582,7 +605,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
             }
         }
         float g[NF];
-        OP::gather(fs, rs, K, g);
+        OP::gather_rest(fs, rs, sgc, K, g);
         {
             const int pz = ph(w);
             const uint32_t so = inarr ? cb : kDropOff;
@@ -596,6 +619,8 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
             rzm[b] = rzc[b];
             rzc[b] = rzp[b];
         }
+#pragma unroll
+        for (int q = 0; q < NG; ++q) sgc[q] = sgp[q];
         __syncthreads();  // (waits for the plane loads into LDS as well)
     };
 

@@ -14,6 +14,11 @@
 //                           for a boundary-face node n = m + t e_AX whose only
 //                           residual neighbour is m: R_b(m) dR_b(m)/dq(n)
 //                           (the boundary-gradient correction, Sec. 2.3).
+// The gather splits into gather_self(f, R, K, S), its first NG partial sums,
+// which need only R(n) and the star of n, and gather_rest(f, r, S, K, g), the
+// neighbour terms added to them in the same order (gather = rest after self).
+// The backward evaluates the self part where it evaluates R(n), from the same
+// star, and carries the NG sums to the step that gathers at n.
 // Star values are indexed by array axis: m[a] / p[a] hold q(n - e_a) / q(n + e_a).
 //
 // Evaluation order: second differences are formed as ((q+ - q) + (q- - q)) / h^2,
@@ -65,7 +70,7 @@ __device__ __forceinline__ float lap(const Star& s, const KCoef& K) {
 // Burgers on a space-time grid: axis 0 = t, axis 1 = x.
 //   R = u_t + u u_x - nu u_xx
 struct OpBurgers {
-    static constexpr int DIM = 2, NF = 1, NC = 0, NR = 1;
+    static constexpr int DIM = 2, NF = 1, NC = 0, NR = 1, NG = 0;
 
     __device__ __forceinline__ static void residual(const Star* f, const float*, const KCoef& K, float* R) {
         const Star& u = f[0];
@@ -85,6 +90,11 @@ struct OpBurgers {
         g[0] = acc;
     }
 
+    __device__ __forceinline__ static void gather_self(const Star*, const float*, const KCoef&, float*) {}
+    __device__ __forceinline__ static void gather_rest(const Star* f, const Star* r, const float*, const KCoef& K, float* g) {
+        gather(f, r, K, g);
+    }
+
     template <int AX>
     __device__ __forceinline__ static void bc_term(const Star* f, const float* c, const KCoef& K, float t, float* g) {
         float R[1];
@@ -97,7 +107,7 @@ struct OpBurgers {
 // ---------------------------------------------------------------------------
 // Helmholtz: R = lap u + k^2 u - f   (self-adjoint: dL/du = k^2 R + lap R).
 struct OpHelmholtz {
-    static constexpr int DIM = 2, NF = 1, NC = 1, NR = 1;
+    static constexpr int DIM = 2, NF = 1, NC = 1, NR = 1, NG = 0;
 
     __device__ __forceinline__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
         R[0] = lap<2>(f[0], K) + K.k2 * f[0].c - c[0];
@@ -105,6 +115,10 @@ struct OpHelmholtz {
 
     __device__ __forceinline__ static void gather(const Star*, const Star* r, const KCoef& K, float* g) {
         g[0] = K.k2 * r[0].c + lap<2>(r[0], K);
+    }
+    __device__ __forceinline__ static void gather_self(const Star*, const float*, const KCoef&, float*) {}
+    __device__ __forceinline__ static void gather_rest(const Star* f, const Star* r, const float*, const KCoef& K, float* g) {
+        gather(f, r, K, g);
     }
 
     template <int AX>
@@ -118,7 +132,7 @@ struct OpHelmholtz {
 // ---------------------------------------------------------------------------
 // One implicit heat step: R = (u - u0)/dt - alpha lap u.
 struct OpHeat {
-    static constexpr int DIM = 3, NF = 1, NC = 1, NR = 1;
+    static constexpr int DIM = 3, NF = 1, NC = 1, NR = 1, NG = 0;
 
     __device__ __forceinline__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
         R[0] = (f[0].c - c[0]) * K.inv_dt - K.alpha * lap<3>(f[0], K);
@@ -126,6 +140,10 @@ struct OpHeat {
 
     __device__ __forceinline__ static void gather(const Star*, const Star* r, const KCoef& K, float* g) {
         g[0] = r[0].c * K.inv_dt - K.alpha * lap<3>(r[0], K);
+    }
+    __device__ __forceinline__ static void gather_self(const Star*, const float*, const KCoef&, float*) {}
+    __device__ __forceinline__ static void gather_rest(const Star* f, const Star* r, const float*, const KCoef& K, float* g) {
+        gather(f, r, K, g);
     }
 
     template <int AX>
@@ -143,7 +161,7 @@ struct OpHeat {
 // UNSTEADY selects the backward-Euler time term (consts = previous velocities).
 template <int D, bool UNSTEADY>
 struct OpNS {
-    static constexpr int DIM = D, NF = D + 1, NC = UNSTEADY ? D : 0, NR = D + 1;
+    static constexpr int DIM = D, NF = D + 1, NC = UNSTEADY ? D : 0, NR = D + 1, NG = D;
 
     __device__ __forceinline__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
         float cs[D];  // c_a / (2 h_a), shared by the D momentum equations
@@ -167,15 +185,24 @@ struct OpNS {
     //            + sum_a (R_q(n-e_a) c_a(n-e_a) - R_q(n+e_a) c_a(n+e_a)) / (2 h_a)
     //            + (R_div(n-e_q) - R_div(n+e_q)) / (2 h_q) - nu lap R_q(n)
     // dL/dp(n)   = sum_b (R_b(n-e_b) - R_b(n+e_b)) / (2 h_b)
-    __device__ __forceinline__ static void gather(const Star* f, const Star* r, const KCoef& K, float* g) {
+    // the node's own terms: S_q = sum_b R_b(n) D1_q c_b(n) [+ R_q(n)/dt]
+    __device__ __forceinline__ static void gather_self(const Star* f, const float* R, const KCoef& K, float* S) {
+#pragma unroll
+        for (int q = 0; q < D; ++q) {
+            float loc = R[0] * (f[0].p[q] - f[0].m[q]);
+#pragma unroll
+            for (int b = 1; b < D; ++b) loc = fmaf(R[b], f[b].p[q] - f[b].m[q], loc);
+            S[q] = loc * K.i2h[q];
+            if (UNSTEADY) S[q] = fmaf(R[q], K.inv_dt, S[q]);
+        }
+    }
+
+    // the neighbour terms, added to S in order
+    __device__ __forceinline__ static void gather_rest(const Star* f, const Star* r, const float* S, const KCoef& K, float* g) {
         float gp = 0.f;
 #pragma unroll
         for (int q = 0; q < D; ++q) {
-            float loc = r[0].c * (f[0].p[q] - f[0].m[q]);
-#pragma unroll
-            for (int b = 1; b < D; ++b) loc = fmaf(r[b].c, f[b].p[q] - f[b].m[q], loc);
-            float acc = loc * K.i2h[q];
-            if (UNSTEADY) acc = fmaf(r[q].c, K.inv_dt, acc);
+            float acc = S[q];
 #pragma unroll
             for (int a = 0; a < D; ++a)
                 acc = fmaf(fmaf(r[q].m[a], f[a].m[a], -(r[q].p[a] * f[a].p[a])), K.i2h[a], acc);
@@ -184,6 +211,14 @@ struct OpNS {
             gp = fmaf(r[q].m[q] - r[q].p[q], K.i2h[q], gp);
         }
         g[D] = gp;
+    }
+
+    __device__ __forceinline__ static void gather(const Star* f, const Star* r, const KCoef& K, float* g) {
+        float R[NR], S[D];
+#pragma unroll
+        for (int b = 0; b < NR; ++b) R[b] = r[b].c;
+        gather_self(f, R, K, S);
+        gather_rest(f, r, S, K, g);
     }
 
     // n = m + t e_AX: only the neighbour terms of R_b(m) reach n.
