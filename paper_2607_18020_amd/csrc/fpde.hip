@@ -36,6 +36,13 @@ bool op_desc(int op, OpDesc* d) {
 #ifndef FPDE_TX3
 #define FPDE_TX3 64
 #endif
+// forward tile widths (a tile's side-edge x-neighbours cost a cache line each)
+#ifndef FPDE_NS3_FWD_TX
+#define FPDE_NS3_FWD_TX 64
+#endif
+#ifndef FPDE_HEAT_FWD_TX
+#define FPDE_HEAT_FWD_TX 256
+#endif
 #ifndef FPDE_NS3_FWD_TY
 #define FPDE_NS3_FWD_TY 8
 #endif
@@ -46,7 +53,7 @@ bool op_desc(int op, OpDesc* d) {
 #define FPDE_NS3_MIN_BWD_BLOCKS 256
 #endif
 #ifndef FPDE_HEAT_FWD_TY
-#define FPDE_HEAT_FWD_TY 8
+#define FPDE_HEAT_FWD_TY 4
 #endif
 #ifndef FPDE_HEAT_BWD_TY
 #define FPDE_HEAT_BWD_TY 8
@@ -67,12 +74,14 @@ bool op_desc(int op, OpDesc* d) {
 constexpr int kTX3 = FPDE_TX3, kTX2 = FPDE_TX2, kTargetBlocks2 = FPDE_BLOCKS2;
 constexpr bool kBwdReverse = FPDE_BWD_REVERSE != 0;
 
-template <int TYF, int TYB, int MINB>
+// forward tile TXF x TYf, backward tile TXB x TYb
+template <int TXF_, int TYF, int TYB, int MINB>
 struct Geo3 {
-    static constexpr int TXF = kTX3, TYf = TYF, TXB = kTX3, TYb = TYB, MIN_BWD_BLOCKS = MINB;
+    static constexpr int TXF = TXF_, TYf = TYF, TXB = kTX3, TYb = TYB, MIN_BWD_BLOCKS = MINB;
 };
-using GeoNS3 = Geo3<FPDE_NS3_FWD_TY, FPDE_NS3_BWD_TY, FPDE_NS3_MIN_BWD_BLOCKS>;
-using GeoHeat = Geo3<FPDE_HEAT_FWD_TY, FPDE_HEAT_BWD_TY, FPDE_HEAT_MIN_BWD_BLOCKS>;
+using GeoNS3 = Geo3<FPDE_NS3_FWD_TX, FPDE_NS3_FWD_TY, FPDE_NS3_BWD_TY, FPDE_NS3_MIN_BWD_BLOCKS>;
+using GeoHeat =
+    Geo3<FPDE_HEAT_FWD_TX, FPDE_HEAT_FWD_TY, FPDE_HEAT_BWD_TY, FPDE_HEAT_MIN_BWD_BLOCKS>;
 
 struct Req {
     int op;

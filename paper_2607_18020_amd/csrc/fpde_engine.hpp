@@ -42,8 +42,10 @@
 
 // Minimum waves per SIMD requested from the compiler for the marching kernels
 // (bounds their VGPR budget; 1 leaves the compiler free).
+// minimum waves per SIMD (the second launch bound): 4 lets two 8-wave forward
+// workgroups share a CU, with at most 128 VGPRs each
 #ifndef FPDE_FWD_MINW
-#define FPDE_FWD_MINW 1
+#define FPDE_FWD_MINW 4
 #endif
 #ifndef FPDE_BWD_MINW
 #define FPDE_BWD_MINW 1
@@ -228,13 +230,18 @@ __device__ __forceinline__ int fresh(int v) {
 // region's FSZ elements (tile plus halo, row-major) padded to a multiple of 64,
 // and element i is loaded by thread i mod NT in round i / NT: the 64 lanes of a
 // wave fill 64 consecutive LDS words (buffer_load_dword ... lds, M0 = the
-// wave's base).  Whether a wave takes part in a round is uniform across the
-// wave.  Elements outside the array, and the padding, carry an offset past the
-// descriptor's range and read as 0; so does a whole plane outside the grid.
+// wave's base).  Every wave issues the same KP loads per array and plane, so
+// that the number of loads in flight does not depend on the wave (the
+// compiler's wait counts are exact only then): a wave whose part of a round
+// lies past the slot sends it to the 64-word spill line after the slot (slot
+// arrays hold FSZS words).  Elements outside the array, and the padding, carry
+// an offset past the descriptor's range and read as 0 without a memory access;
+// so does a whole plane outside the grid.
 
 template <int FSZ, int NT>
 struct PlaneStream {
     static constexpr int FSZP = (FSZ + 63) / 64 * 64;  // padded slot size (elements)
+    static constexpr int FSZS = FSZP + 64;              // with the spill line
     static constexpr int KP = (FSZP + NT - 1) / NT;     // load rounds
     static constexpr uint32_t kOff = 0x80000000u;
     uint32_t off[KP];  // byte offset of this thread's element in each round
@@ -265,14 +272,14 @@ struct PlaneStream {
             r[f] = uniform_rsrc(reinterpret_cast<const char*>(src[f]) + zoff, nrec);
 #pragma unroll
         for (int k = 0; k < KP; ++k) {
-            // every wave takes part in the rounds that the slot fills completely
-            if ((k + 1) * NT <= FSZP || wl + k * NT < (uint32_t)FSZP) {
+            // rounds that the slot fills completely hold a part of every wave
+            const bool in = (k + 1) * NT <= FSZP || wl + k * NT < (uint32_t)FSZP;
+            const uint32_t at = in ? wl + k * NT : (uint32_t)FSZP;  // uniform
 #pragma unroll
-                for (int f = 0; f < NF; ++f)
-                    __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                        r[f], (__attribute__((address_space(3))) void*)(dst[f] + wl + k * NT), 4,
-                        (int)off[k], 0, 0, 0);
-            }
+            for (int f = 0; f < NF; ++f)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    r[f], (__attribute__((address_space(3))) void*)(dst[f] + at), 4, (int)off[k], 0,
+                    0, 0);
         }
     }
 };
@@ -292,10 +299,18 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
     constexpr int DIM = OP::DIM, NF = OP::NF, NC = OP::NC, NR = OP::NR, NT = TX * TY;
     constexpr int NC1 = NC > 0 ? NC : 1;
     constexpr int HY = (DIM == 3) ? 1 : 0;
-    constexpr int LY = TY + 2 * HY, LX = TX + 2;
-    using PS = PlaneStream<LY * LX, NT>;
+    // A slot holds the tile's own TX columns for TY + 2 HY rows, so that every
+    // wavefront's plane load is one aligned 64-node row segment (a halo column in
+    // each row would misalign them all), followed by one 64-element group with
+    // the x-neighbours across the tile's side edges: element LY*TX + r is the
+    // left neighbour of own row r, element LY*TX + TY + r the right one.  Each of
+    // those is a cache line of its own, so tiles are made wide.
+    constexpr int LY = TY + 2 * HY, LX = TX, XG = LY * LX;
+    static_assert(TX % 64 == 0, "a wavefront loads whole aligned row segments");
+    static_assert(2 * TY <= 64, "the side-edge neighbours fill one 64-element group");
+    using PS = PlaneStream<XG + 64, NT>;
     static_assert(DIM == 3 || TY == 1, "2-D grids use one-row tiles");
-    FPDE_SLOT_RING(float, sF, NF, PS::FSZP);
+    FPDE_SLOT_RING(float, sF, NF, PS::FSZS);
 
     const int t = threadIdx.x, tx = t % TX, ty = t / TX;
     const TileCoord tc = tile_coord<TX, TY>(D);
@@ -308,7 +323,16 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
 
     PS ps;
     ps.init(t, [&](int i, int& lin) {
-        const int py = (DIM == 3) ? tc.gy0 - HY + i / LX : 0, px = tc.gx0 - 1 + i % LX;
+        int py, px;
+        if (i < XG) {
+            py = (DIM == 3) ? tc.gy0 - HY + i / LX : 0;
+            px = tc.gx0 + i % LX;
+        } else {
+            const int j = i - XG, side = j / TY;
+            py = (DIM == 3) ? tc.gy0 + j % TY : 0;
+            px = side == 0 ? tc.gx0 - 1 : tc.gx0 + TX;
+            if (side > 1) return false;
+        }
         lin = py * D.nx + px;
         return px >= 0 && px < D.nx && py >= 0 && py < D.ny;
     });
@@ -331,7 +355,9 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
     load_consts(z0, true, cv[0]);
     __syncthreads();
 
-    const int own = (ty + HY) * LX + tx + 1;  // own node in a slot
+    const int own = (ty + HY) * LX + tx;  // own node in a slot
+    // its x-neighbours: in the row, or in the side-edge group
+    const int xm = tx == 0 ? XG + ty : own - 1, xp = tx == TX - 1 ? XG + TY + ty : own + 1;
     double acc = 0.0;
     auto step = [&](auto jc, int w) __attribute__((always_inline)) {
         constexpr int J = decltype(jc)::value;  // w & 3
@@ -341,6 +367,9 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
         const bool more = w + 1 < L;
         // plane z+2 goes to the slot of plane z-2, last read before the previous barrier
         load_plane(more ? z + 2 : -1, IC<SQ>{});
+        // the plane loads go first: the barrier then waits for them alone, not
+        // for the const loads queued after them for the next step
+        __builtin_amdgcn_sched_barrier(0);
         load_consts(z + 1, more, cv[NXT]);
         Star s[NF];
 #pragma unroll
@@ -349,8 +378,8 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
             s[f].c = c[0];
             s[f].m[0] = sF(IC<SM>{})[f][own];
             s[f].p[0] = sF(IC<SP>{})[f][own];
-            s[f].m[DIM - 1] = c[-1];
-            s[f].p[DIM - 1] = c[1];
+            s[f].m[DIM - 1] = sF(IC<SC>{})[f][xm];
+            s[f].p[DIM - 1] = sF(IC<SC>{})[f][xp];
             if (DIM == 3) {
                 s[f].m[1] = c[-LX];
                 s[f].p[1] = c[LX];
@@ -362,6 +391,9 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
 #pragma unroll
         for (int b = 0; b < NR; ++b) ss = fmaf(R[b], R[b], ss);
         acc += (double)(interior ? ss : 0.f);
+        // the step's arithmetic feeds nothing but acc: pin acc here, or the compiler
+        // may sink that arithmetic past the barriers and keep several steps' loads live
+        asm volatile("" : "+v"(acc));
         if (STORE_R) {
             const uint32_t so = interior ? cb : kDropOff;
 #pragma unroll
@@ -408,9 +440,9 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     // physical planes ph(w) = z0 + w, or z1 - 1 - w when REV (top down).
     // Field planes of march steps live in a 4-slot ring: step w in slot (w + 1) & 3;
     // residual tiles: R of step w in buffer w & 1.
-    FPDE_SLOT_RING(float, sF, NF, PS::FSZP);
+    FPDE_SLOT_RING(float, sF, NF, PS::FSZS);
     __shared__ float sR[2][NR][RLY * RLX];
-    constexpr int kLds = (4 * NF * PS::FSZP + 2 * NR * RLY * RLX) * 4;
+    constexpr int kLds = (4 * NF * PS::FSZS + 2 * NR * RLY * RLX) * 4;
 
     const int t = threadIdx.x, tx = t % TX, ty = t / TX;
     const TileCoord tc = tile_coord<TX, TY>(D);
@@ -571,6 +603,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
         // step w+3's plane goes to the slot of step w-1, unread in this step; an
         // empty plane after the chunk's last step
         load_plane(more ? ph(w + 3) : -1, IC<SB>{});
+        __builtin_amdgcn_sched_barrier(0);  // (the plane loads first, as in the forward)
         const int fos = fown, ros = rown;
         // (the ring's addresses, used by a few waves only, are not held across the march)
         r_tile(ph(w + 1), IC<SC>{}, IC<SN>{}, IC<SQ>{}, RN, rzp, sgp, fos, ros, fresh<kLds>(fring),

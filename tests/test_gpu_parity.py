@@ -18,7 +18,8 @@ from tests import gpu_helpers as H
 pytestmark = pytest.mark.gpu
 
 # (config, shape): several tiles along every axis plus ragged tails (2-D rows are
-# 256-node segments; 3-D tiles are 64 x 8 columns; chunks of planes along axis 0)
+# 256-node segments; 3-D tiles are 64 or 256 nodes wide in x; chunks of planes
+# along axis 0)
 SMALL = [
     ("burgers_1dt", (3, 3)), ("burgers_1dt", (5, 7)), ("burgers_1dt", (41, 300)),
     ("burgers_1dt", (128, 256)),
@@ -29,6 +30,8 @@ SMALL = [
     ("ns_2d", (3, 3)), ("ns_2d", (6, 257)), ("ns_2d", (71, 600)), ("ns_2d", (300, 257)),
     ("ns_3d_tgv", (3, 3, 3)), ("ns_3d_tgv", (4, 9, 66)), ("ns_3d_tgv", (19, 21, 70)),
     ("ns_3d_tgv", (40, 17, 129)),
+    # wider than one 256-node tile: side edges between tiles, ragged last tile
+    ("heat_3d", (9, 10, 300)), ("heat_3d", (6, 7, 520)), ("ns_3d_tgv", (7, 9, 300)),
     # full-width planes: several chunks of several planes each along axis 0, so
     # the unrolled march, its tail and the seams between chunks are all exercised
     ("heat_3d", (42, 256, 256)), ("ns_3d_tgv", (42, 256, 256)), ("ns_3d_tgv", (75, 130, 200)),
