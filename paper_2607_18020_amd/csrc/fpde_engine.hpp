@@ -206,13 +206,24 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t plane_rsrc_if(const float* p, 
 // the hardware drops such a store.
 constexpr uint32_t kDropOff = 0x80000000u;
 
+// AUX: the cache-policy bits of the access (0: default; 2: non-temporal).
+// Outputs (gradients, residuals) are written once and not read again by the
+// operator: they are stored non-temporally, so that they neither evict the
+// halo rows that neighbouring tiles share in L2 nor leave dirty lines in the
+// caches for the next kernel to write back.
+constexpr int kStream = 2;
+
+template <int AUX = 0>
 __device__ __forceinline__ float bld(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
+    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, AUX));
 }
 
+template <int AUX = 0>
 __device__ __forceinline__ void bst(__amdgpu_buffer_rsrc_t r, uint32_t off, float v) {
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)off, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)off, 0, AUX);
 }
+
+
 
 // An opaque copy of v, made once per march step.  LDS addresses derived from it
 // are recomputed in the step (one add each) instead of being hoisted out of the
@@ -345,7 +356,8 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
     float cv[2][NC1];
     auto load_consts = [&](int pz, bool ok, float* c) __attribute__((always_inline)) {
 #pragma unroll
-        for (int j = 0; j < NC; ++j) c[j] = bld(plane_rsrc_if(P.c[j], pz, pbytes, ok), cb);
+        for (int j = 0; j < NC; ++j)
+            c[j] = bld(plane_rsrc_if(P.c[j], pz, pbytes, ok), cb);
     };
 
     // plane z0 + j lives in slot (j + 1) & 3; prologue: planes z0-1, z0, z0+1
@@ -397,7 +409,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
         if (STORE_R) {
             const uint32_t so = interior ? cb : kDropOff;
 #pragma unroll
-            for (int b = 0; b < NR; ++b) bst(plane_rsrc(P.out[b], z, pbytes), so, R[b]);
+            for (int b = 0; b < NR; ++b) bst<kStream>(plane_rsrc(P.out[b], z, pbytes), so, R[b]);
         }
         __syncthreads();  // (waits for the plane loads into LDS as well)
     };
@@ -643,7 +655,8 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
             const int pz = ph(w);
             const uint32_t so = inarr ? cb : kDropOff;
 #pragma unroll
-            for (int f = 0; f < NF; ++f) bst(plane_rsrc(P.out[f], pz, pbytes), so, scale * g[f]);
+            for (int f = 0; f < NF; ++f)
+                bst<kStream>(plane_rsrc(P.out[f], pz, pbytes), so, scale * g[f]);
         }
 #pragma unroll
         for (int f = 0; f < NF; ++f) fzm[f] = fs[f].c;
@@ -730,7 +743,7 @@ __global__ __launch_bounds__(256) void bc_kernel(Ptrs P, Dims D, KCoef K, const 
             for (int f = 0; f < NF; ++f) g[f] = 0.f;
         }
 #pragma unroll
-        for (int f = 0; f < NF; ++f) P.out[f][node] = g[f];
+        for (int f = 0; f < NF; ++f) __builtin_nontemporal_store(g[f], &P.out[f][node]);
     }
 }
 
