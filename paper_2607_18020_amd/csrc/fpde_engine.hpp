@@ -3,11 +3,10 @@
 // Grid geometry: array axis 0 is the march axis ("z"); the last axis is x
 // (fastest, coalesced); for 3-D grids axis 1 is y.  A workgroup owns a TX x TY
 // column tile of the (y, x) plane (TY = 1 for 2-D grids, where the "plane" is a
-// row segment) and marches a chunk of ZC planes along axis 0:
-//   * the in-plane neighbours come from a halo tile of the current plane in LDS;
-//   * the axis-0 neighbours come from a per-thread register queue (planes
-//     z-1, z, z+1 of the thread's own column);
-// so every input element is read from HBM once per chunk plus the halo.
+// row segment) and marches a chunk of planes along axis 0.  Each plane region
+// streams from memory straight into a ring of LDS slots, so every input element
+// is read from HBM once per chunk plus the halo; the 7-point star of a node is
+// read from the slots of planes z-1, z, z+1.
 //
 // Forward: one residual per interior node, sum of squares accumulated in a
 // per-thread float64 register, reduced with DPP across the wavefront and through
@@ -17,12 +16,10 @@
 // Backward: gather form of the transposed stencil (Sec. 2.2).  The residuals
 // that the gather needs are recomputed, never read: at step z the workgroup
 // evaluates R(z+1) on the tile plus a one-node ring into an LDS tile, so the
-// gather for plane z reads R(z) (in-plane star, LDS), R(z+1) (LDS) and R(z-1)
-// (register queue).  Field planes live in a 4-slot LDS ring (tile plus a
-// two-node halo); the next plane is prefetched into registers one step ahead.
-// Every node of the visited planes 1..nz-2 is written exactly once (boundary
-// columns included: there the residuals off the residual set are zero, which
-// the LDS tiles already hold); no atomics.
+// gather for plane z reads R(z) (in-plane star, LDS), R(z+1) and R(z-1) of its
+// own column (registers).  Every node of the visited planes 1..nz-2 is written
+// exactly once (boundary columns included: there the residuals off the residual
+// set are zero, which the LDS tiles already hold); no atomics.
 //
 // Boundary correction: a 1-D launch over the two end planes of axis 0, the
 // boundary nodes the march does not visit (Sec. 2.3).
@@ -297,10 +294,10 @@ struct PlaneStream {
 
 // ---------------------------------------------------------------------------
 // Forward: residuals of one chunk of planes + fused sum of squares.  Each plane
-// (tile + one-node halo) streams from memory straight into a 4-slot LDS ring;
-// the 7-point star of every field is read from the slots of planes z-1, z, z+1.
-// One barrier per step: plane z+2 streams into the slot of plane z-2 while
-// plane z is evaluated.  The sum of squares is accumulated per thread in
+// (tile rows plus one row above and below, and the side-edge x-neighbours)
+// streams from memory straight into a 4-slot LDS ring; the 7-point star of
+// every field is read from the slots of planes z-1, z, z+1.  One barrier per
+// step: plane z+2 streams into the slot of plane z-2 while plane z is evaluated.  The sum of squares is accumulated per thread in
 // float64, reduced with DPP across the wavefront and through LDS across waves,
 // then added with ONE float64 atomic per workgroup.
 

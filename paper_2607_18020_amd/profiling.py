@@ -9,7 +9,8 @@ Traffic calibration: FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are scaled by
 what the same counters read for the benchmark's stream kernel (y = 1 * x over
 1 GiB: 1 GiB read, 1 GiB written), so the figures are bytes, whatever the
 counters' own unit and coverage.  ``traffic.json`` records a hash of the kernel
-sources; ``bench.py`` reports the traffic only while that hash still matches.
+sources (comments and whitespace ignored); ``bench.py`` reports the traffic
+only while that hash still matches.
 """
 from __future__ import annotations
 
@@ -19,6 +20,7 @@ import glob
 import hashlib
 import json
 import os
+import re
 from collections import defaultdict
 from typing import Dict, List
 
@@ -28,11 +30,19 @@ STREAM_KERNEL = "MulFunctor"  # the benchmark's 1 GiB y = 1 * x kernel
 STREAM_BYTES = 1 << 30
 
 
-def source_hash() -> str:
+def _code_only(text: str) -> str:
+    """The source without comments and with whitespace collapsed: edits to
+    comments do not change what was measured."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
+def source_hash(root: str = PKG) -> str:
     h = hashlib.sha256()
     for rel in KERNEL_SOURCES:
-        with open(os.path.join(PKG, rel), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(root, rel), encoding="utf-8") as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()[:16]
 
 
@@ -102,7 +112,7 @@ def main():
     kern = sorted(k for k in stats if k.startswith(("fwd_kernel", "bwd_kernel", "bc_kernel", "fill")))
     lines = [f"# Kernel timings and HBM traffic, {a.workload}", "",
              "Commands (run from the repository root on one MI355X):", "", "```", cmds, "```", "",
-             f"Kernel sources hash: `{sha}`.", "",
+             f"Kernel sources hash (comments and whitespace ignored): `{sha}`.", "",
              "## rocprofv3 --kernel-trace --stats (same process as the bench line below)", "",
              "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
     for k in kern:
