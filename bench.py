@@ -38,14 +38,17 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-planes", type=int, default=0,
                    help="planes of the oracle sample along axis 0 (0: sized automatically)")
+    p.add_argument("--bc-mode", type=int, default=0, choices=(0, 1),
+                   help="0: interior residual set (the benchmark); 1: periodic wrap on every axis")
     p.add_argument("--sample-every", type=int, default=10,
                    help="per-kernel HIP events on every n-th timed step (the others carry none)")
     return p.parse_args()
 
 
-def byte_model(wl):
+def byte_model(wl, bc_mode=0):
     nf, nc = len(wl.spec.fields), len(wl.spec.consts)
-    N, M = wl.n_points, wl.n_residual_points
+    N = wl.n_points
+    M = N if bc_mode == 1 else wl.n_residual_points  # nodes the backward writes
     return {
         "step": (2 * (nf + nc) + nf) * 4 * N + 8,
         "fwd": (nf + nc) * 4 * N + 8,
@@ -96,7 +99,7 @@ def measured_traffic(cfg, op, kernel):
     return None
 
 
-def cpu_baseline(W, wl_full, cfg, seed, planes):
+def cpu_baseline(W, wl_full, cfg, seed, planes, bc_mode=0):
     """The oracle (single thread, float64) on a slab of the same workload."""
     import numpy as np  # noqa: PLC0415
     import oracle  # noqa: PLC0415  (CPU baseline leg only)
@@ -111,8 +114,9 @@ def cpu_baseline(W, wl_full, cfg, seed, planes):
     consts = [np.ascontiguousarray(c[sl], dtype=np.float64) for c in wl_full.consts]
     sshape = fields[0].shape
     t0 = time.perf_counter()
-    oracle.loss(wl_full.op, sshape, wl_full.h, wl_full.coeffs, fields, consts)
-    oracle.grad(wl_full.op, sshape, wl_full.h, wl_full.coeffs, fields, consts, dloss=1.0)
+    oracle.loss(wl_full.op, sshape, wl_full.h, wl_full.coeffs, fields, consts, bc_mode=bc_mode)
+    oracle.grad(wl_full.op, sshape, wl_full.h, wl_full.coeffs, fields, consts, dloss=1.0,
+                bc_mode=bc_mode)
     dt = time.perf_counter() - t0
     npts = int(np.prod(sshape))
     return {"value": npts / dt, "unit": "grid-points/s", "cores": 1, "kind": "oracle",
@@ -148,14 +152,16 @@ def main():
     stream = torch.cuda.current_stream()
     op, h, co = wl.op, wl.h, wl.coeffs
 
+    bcm = args.bc_mode
+
     def fwd():
-        B.fpde_residual_fwd(op, fields, consts, h, co, loss=loss, stream=stream)
+        B.fpde_residual_fwd(op, fields, consts, h, co, loss=loss, bc_mode=bcm, stream=stream)
 
     def bwd():
-        B.fpde_residual_bwd(op, fields, consts, h, co, dl, grads=grads, stream=stream)
+        B.fpde_residual_bwd(op, fields, consts, h, co, dl, grads=grads, bc_mode=bcm, stream=stream)
 
     def bc():
-        B.fpde_bc_correct(op, fields, consts, h, co, dl, grads=grads, stream=stream)
+        B.fpde_bc_correct(op, fields, consts, h, co, dl, grads=grads, bc_mode=bcm, stream=stream)
 
     for _ in range(args.warmup):
         fwd(), bwd(), bc()
@@ -192,7 +198,7 @@ def main():
     if not (L == L) or L <= 0:
         raise RuntimeError(f"bad loss {L}")
 
-    bm = byte_model(wl)
+    bm = byte_model(wl, bcm)
     N = wl.n_points
     ms = total_s / K * 1e3
     gbps = bm["step"] * K / total_s / 1e9
@@ -204,7 +210,7 @@ def main():
                 "algorithmic_bytes_per_launch": bm[dom], "avg_launch_us": round(per[dom], 2)}
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(W, wl, cfg, args.seed, args.cpu_planes)
+        cpu = cpu_baseline(W, wl, cfg, args.seed, args.cpu_planes, bcm)
     out = {
         "metric": METRIC,
         "value": N * K / total_s,
@@ -221,7 +227,8 @@ def main():
         "config": {"workload": f"{cfg}: {W.CONFIGS[cfg].description}",
                    "grid": list(wl.shape), "nodes": N,
                    "fields": list(wl.spec.fields), "consts": list(wl.spec.consts),
-                   "seed": args.seed, "step": "fwd+loss, bwd, bc on one stream"},
+                   "seed": args.seed, "step": "fwd+loss, bwd, bc on one stream",
+                   "bc_mode": bcm},
         "hbm_gbps": round(gbps, 1),
         "hbm_frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4),
         "bytes_per_step": bm["step"],

@@ -14,7 +14,9 @@
  *   - arrays are dense C-contiguous float32, shape n[0..ndim-1], last axis
  *     fastest; h[a] is the node spacing along array axis a;
  *   - the residual set is Omega = { nodes with 1 <= i_a <= n_a - 2 on every
- *     axis }, M = prod_a (n_a - 2);
+ *     axis }, M = prod_a (n_a - 2) (bc_mode 0); with bc_mode 1 (periodic) the
+ *     grid wraps on every axis, q(m +- e_a) reading node i_a +- 1 mod n_a, and
+ *     Omega is every node, M = prod_a n_a;
  *   - D1_a q(m) = (q(m+e_a) - q(m-e_a)) / (2 h_a),
  *     D2_a q(m) = (q(m+e_a) - 2 q(m) + q(m-e_a)) / h_a^2     (App. A.3);
  *   - loss L = sum over equations b of (1/M) sum_{m in Omega} R_b(m)^2;
@@ -69,7 +71,7 @@ typedef enum fpde_status {
     FPDE_ERR_COEFF = -4,       /* non-finite coefficient, or dt <= 0 for a time-stepping op */
     FPDE_ERR_ALIGN = -5,       /* a device pointer not 4-byte aligned */
     FPDE_ERR_HIP = -6,         /* the HIP runtime reported an error while queueing */
-    FPDE_ERR_UNSUPPORTED = -7  /* valid request this build does not implement (bc_mode != 0) */
+    FPDE_ERR_UNSUPPORTED = -7  /* valid request this build does not implement (none at present) */
 } fpde_status;
 
 typedef enum fpde_op {
@@ -81,8 +83,9 @@ typedef enum fpde_op {
 } fpde_op;
 
 /* Grid: rank, residual-set mode, sizes per array axis, spacings per axis.
- * bc_mode 0 is the residual set Omega above; other values are rejected with
- * FPDE_ERR_UNSUPPORTED.  Entries past ndim are ignored.
+ * bc_mode 0: the interior residual set Omega above; 1: periodic wrap on every
+ * axis (the survey's reading B of the Taylor-Green grid); other values are
+ * rejected with FPDE_ERR_ARG.  Entries past ndim are ignored.
  * Limits: every n_a >= 3 and n_a < 2^31; a plane of the non-marching axes
  * (n[1]*n[2] for ndim 3, n[1] for ndim 2) holds fewer than 2^29 nodes. */
 typedef struct fpde_grid {
@@ -109,7 +112,8 @@ int fpde_op_info(int op, int* ndim, int* n_fields, int* n_consts, int* n_residua
 /* Fused forward stencil + mean-squared residual loss (Sec. 2.1).
  *   loss          device pointer to one double; OVERWRITTEN with L (not accumulated).
  *   residual_out  NULL, or a host array of n_residuals device pointers: R_b is
- *                 written on Omega only; nodes off Omega are left untouched.
+ *                 written on Omega only; nodes off Omega are left untouched
+ *                 (periodic grids: every node).
  * Queues 2 kernels: a one-element fill that zeroes *loss, then the stencil
  * kernel (one float64 atomic add per workgroup onto *loss). */
 int fpde_residual_fwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
@@ -125,7 +129,8 @@ int fpde_residual_fwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
  *          of those planes included: there the transposed stencil is evaluated
  *          with the residuals off Omega taken as zero, which is their exact
  *          boundary term.  The end planes i_0 = 0 and i_0 = n_0 - 1 are not
- *          touched (fpde_bc_correct writes them).
+ *          touched (fpde_bc_correct writes them).  Periodic grids have no
+ *          boundary: every node of every plane is written.
  * The residuals are recomputed from the fields; no sensitivity tensor is read.
  * Queues 1 kernel; no atomics. */
 int fpde_residual_bwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
@@ -139,7 +144,9 @@ int fpde_residual_bwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
  * boundary coordinate (an edge or corner) touches no residual node and
  * receives 0.  Arguments as fpde_residual_bwd; OVERWRITES grads on those two
  * planes only, so bwd and bc together write every node exactly once, in
- * either order.  Queues 1 kernel. */
+ * either order.  Queues 1 kernel.  On a periodic grid (bc_mode 1) there is no
+ * boundary: the call validates its arguments and returns FPDE_OK without
+ * queueing anything or writing grads. */
 int fpde_bc_correct(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
                     const float* const* fields, const float* const* consts,
                     const double* dloss, float* const* grads, void* stream);

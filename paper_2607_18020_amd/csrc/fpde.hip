@@ -114,12 +114,13 @@ int validate_common(int op, const fpde_grid* g, const fpde_coeffs* c, const floa
     if (g->bc_mode != 0 && g->bc_mode != 1) return FPDE_ERR_ARG;
     if (g->ndim != r->d.ndim) return FPDE_ERR_SHAPE;
     const int D = r->d.ndim;
+    const bool per = g->bc_mode == 1;
     long long N = 1, M = 1;
     for (int a = 0; a < D; ++a) {
         if (g->n[a] < 3 || g->n[a] >= (1LL << 31)) return FPDE_ERR_SHAPE;
         if (N > (1LL << 62) / g->n[a]) return FPDE_ERR_SHAPE;
         N *= g->n[a];
-        M *= g->n[a] - 2;
+        M *= per ? g->n[a] : g->n[a] - 2;  // periodic: a residual at every node
     }
     // plane of the last two axes (one row for 2-D grids) addressed with 32-bit byte offsets
     if ((D == 3 ? g->n[1] * g->n[2] : g->n[1]) >= (1LL << 29)) return FPDE_ERR_SHAPE;
@@ -150,7 +151,6 @@ int validate_common(int op, const fpde_grid* g, const fpde_coeffs* c, const floa
         if ((uintptr_t)fields[f] & 3u) return FPDE_ERR_ALIGN;
     for (int j = 0; j < r->d.nc; ++j)
         if ((uintptr_t)consts[j] & 3u) return FPDE_ERR_ALIGN;
-    if (g->bc_mode == 1) return FPDE_ERR_UNSUPPORTED;
 
     r->op = op;
     r->K = K;
@@ -167,6 +167,8 @@ int validate_common(int op, const fpde_grid* g, const fpde_coeffs* c, const floa
     dm.ny = (D == 3) ? (int)g->n[1] : 1;
     dm.nx = (int)g->n[D - 1];
     dm.tiles_x = dm.tiles_y = dm.zc = dm.nblocks = 0;
+    dm.per = per ? 1 : 0;
+    dm.zlo = per ? 0 : 1;  // the marched planes: 1 .. n0-2, or all of them
     // every launch shape used below must have fewer than 2^31 workgroups
     if ((long long)(dm.nx / 32 + 1) * (dm.ny + 1) * (dm.nz + 1) >= (1LL << 31)) return FPDE_ERR_SHAPE;
     return FPDE_OK;
@@ -177,7 +179,7 @@ Dims tile_dims(const Dims& n, int TX, int TY, int zc) {
     Dims dm = n;
     dm.tiles_x = (dm.nx + TX - 1) / TX;
     dm.tiles_y = (dm.ny + TY - 1) / TY;
-    const int nplanes = dm.nz - 2;
+    const int nplanes = dm.nz - 2 * dm.zlo;
     dm.zc = zc;
     const long long nch = (nplanes + zc - 1) / zc;
     dm.nblocks = (int)((long long)dm.tiles_x * dm.tiles_y * nch);
@@ -188,7 +190,7 @@ Dims tile_dims(const Dims& n, int TX, int TY, int zc) {
 // (each chunk at least one plane).
 int chunk_planes(const Dims& n, int TX, int TY, int target) {
     const long long tiles = (long long)((n.nx + TX - 1) / TX) * ((n.ny + TY - 1) / TY);
-    const int nplanes = n.nz - 2;
+    const int nplanes = n.nz - 2 * n.zlo;
     long long nch = (target + tiles - 1) / tiles;
     if (nch < 1) nch = 1;
     if (nch > nplanes) nch = nplanes;
@@ -285,6 +287,7 @@ int run_bwd(const Req& r, const double* dloss) {
 }
 
 int run_bc(const Req& r, const double* dloss) {
+    if (r.dims.per) return FPDE_OK;  // a periodic grid has no boundary: the march wrote every node
     switch (r.op) {
     case FPDE_BURGERS_1DT: return launch_bc<OpBurgers>(r, dloss);
     case FPDE_HELMHOLTZ_2D: return launch_bc<OpHelmholtz>(r, dloss);
@@ -373,7 +376,7 @@ extern "C" const char* fpde_status_string(int status) {
     case FPDE_ERR_COEFF: return "FPDE_ERR_COEFF: non-finite coefficient or dt <= 0";
     case FPDE_ERR_ALIGN: return "FPDE_ERR_ALIGN: misaligned device pointer";
     case FPDE_ERR_HIP: return "FPDE_ERR_HIP: HIP runtime error while queueing work";
-    case FPDE_ERR_UNSUPPORTED: return "FPDE_ERR_UNSUPPORTED: bc_mode not implemented";
+    case FPDE_ERR_UNSUPPORTED: return "FPDE_ERR_UNSUPPORTED: request not implemented by this build";
     default: return "unknown fpde status";
     }
 }

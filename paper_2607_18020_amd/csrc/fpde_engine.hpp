@@ -60,7 +60,14 @@ struct Dims {
     int nz, ny, nx;         // ny = 1 for 2-D grids
     int tiles_x, tiles_y;   // tiles_y = 1 for 2-D grids
     int zc, nblocks;        // planes per chunk, workgroups launched
+    int per;                // periodic wrap on every axis (residual at every node)
+    int zlo;                // first marched plane: 1, or 0 when periodic
 };
+
+// i in [-n, 2n) wrapped into [0, n) (periodic grids; a ragged tile reaches past n)
+__device__ __forceinline__ int wrap_idx(int i, int n) {
+    return i < 0 ? i + n : (i >= n ? (i >= 2 * n ? i % n : i - n) : i);
+}
 
 __device__ __forceinline__ int remap_xcd(int b, int nb) {
     const int nb8 = nb & ~7;
@@ -142,8 +149,8 @@ __device__ __forceinline__ TileCoord tile_coord(const Dims& D) {
     TileCoord tc;
     tc.gx0 = bx * TX;
     tc.gy0 = by * TY;
-    tc.z0 = 1 + ch * D.zc;
-    tc.z1 = min(tc.z0 + D.zc, D.nz - 1);
+    tc.z0 = D.zlo + ch * D.zc;
+    tc.z1 = min(tc.z0 + D.zc, D.nz - D.zlo);
     return tc;
 }
 
@@ -326,8 +333,10 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
     const int gx = tc.gx0 + tx, gy = (DIM == 3) ? tc.gy0 + ty : 0;
     const uint32_t pbytes = (uint32_t)D.ny * (uint32_t)D.nx * 4u;
     const bool inarr = gx < D.nx && gy < D.ny;
-    const bool interior = gx >= 1 && gx <= D.nx - 2 && (DIM == 2 || (gy >= 1 && gy <= D.ny - 2));
+    const bool interior =
+        D.per ? inarr : gx >= 1 && gx <= D.nx - 2 && (DIM == 2 || (gy >= 1 && gy <= D.ny - 2));
     const uint32_t cb = inarr ? (uint32_t)(gy * D.nx + gx) * 4u : 0u;
+    auto zw = [&](int z) { return D.per ? wrap_idx(z, D.nz) : z; };  // plane index
 
     PS ps;
     ps.init(t, [&](int i, int& lin) {
@@ -340,6 +349,10 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
             py = (DIM == 3) ? tc.gy0 + j % TY : 0;
             px = side == 0 ? tc.gx0 - 1 : tc.gx0 + TX;
             if (side > 1) return false;
+        }
+        if (D.per) {  // every position is a node of the wrapped grid
+            px = wrap_idx(px, D.nx);
+            py = wrap_idx(py, D.ny);
         }
         lin = py * D.nx + px;
         return px >= 0 && px < D.nx && py >= 0 && py < D.ny;
@@ -358,9 +371,9 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
     };
 
     // plane z0 + j lives in slot (j + 1) & 3; prologue: planes z0-1, z0, z0+1
-    load_plane(z0 - 1, IC<0>{});
+    load_plane(zw(z0 - 1), IC<0>{});
     load_plane(z0, IC<1>{});
-    load_plane(z0 + 1, IC<2>{});
+    load_plane(zw(z0 + 1), IC<2>{});
     load_consts(z0, true, cv[0]);
     __syncthreads();
 
@@ -375,7 +388,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
         const int z = z0 + w;
         const bool more = w + 1 < L;
         // plane z+2 goes to the slot of plane z-2, last read before the previous barrier
-        load_plane(more ? z + 2 : -1, IC<SQ>{});
+        load_plane(more ? zw(z + 2) : -1, IC<SQ>{});
         // the plane loads go first: the barrier then waits for them alone, not
         // for the const loads queued after them for the next step
         __builtin_amdgcn_sched_barrier(0);
@@ -456,16 +469,28 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     const int t = threadIdx.x, tx = t % TX, ty = t / TX;
     const TileCoord tc = tile_coord<TX, TY>(D);
     const int z0 = tc.z0, z1 = tc.z1, L = z1 - z0;
-    auto ph = [&](int w) { return REV ? z1 - 1 - w : z0 + w; };
+    auto ph = [&](int w) {  // (wrapped into the grid when periodic)
+        const int p = REV ? z1 - 1 - w : z0 + w;
+        return D.per ? wrap_idx(p, D.nz) : p;
+    };
     const int gx = tc.gx0 + tx, gy = (DIM == 3) ? tc.gy0 + ty : 0;
     const uint32_t pbytes = (uint32_t)D.ny * (uint32_t)D.nx * 4u;
     const bool inarr = gx < D.nx && gy < D.ny;
     const uint32_t cb = inarr ? (uint32_t)(gy * D.nx + gx) * 4u : 0u;
+    // offset of the node whose residual this lane evaluates: its own, or on a
+    // periodic grid the wrapped one (a ragged tile's first lane past the last
+    // column holds the residual that column's gather needs as its x+1 term)
+    const uint32_t cbr =
+        D.per ? (uint32_t)(wrap_idx(gy, D.ny) * D.nx + wrap_idx(gx, D.nx)) * 4u : cb;
     const float scale = (float)(two_over_M * (*dloss));
 
     PS ps;
     ps.init(t, [&](int i, int& lin) {
-        const int py = (DIM == 3) ? tc.gy0 - HY + i / FLX : 0, px = tc.gx0 - 2 + i % FLX;
+        int py = (DIM == 3) ? tc.gy0 - HY + i / FLX : 0, px = tc.gx0 - 2 + i % FLX;
+        if (D.per) {  // every position is a node of the wrapped grid
+            px = wrap_idx(px, D.nx);
+            py = wrap_idx(py, D.ny);
+        }
         lin = py * D.nx + px;
         return px >= 0 && px < D.nx && py >= 0 && py < D.ny;
     });
@@ -480,14 +505,18 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     // the first threads, one node of the ring; their in-plane part of the
     // residual-set test and their const offsets are fixed for the whole march
     const int oly = ty + RHY, olx = tx + 1;
-    const bool own_om = gx >= 1 && gx <= D.nx - 2 && (DIM == 2 || (gy >= 1 && gy <= D.ny - 2));
+    const bool own_om =
+        D.per || (gx >= 1 && gx <= D.nx - 2 && (DIM == 2 || (gy >= 1 && gy <= D.ny - 2)));
     const bool has_ring = t < Ring<TX, TY, DIM>::COUNT;
     int rly = 0, rlx = 0;
     if (has_ring) Ring<TX, TY, DIM>::pos(t, rly, rlx);
     const int rgy = (DIM == 3) ? tc.gy0 - RHY + rly : 0, rgx = tc.gx0 - 1 + rlx;
-    const bool ring_om = has_ring && rgx >= 1 && rgx <= D.nx - 2 &&
-                         (DIM == 2 || (rgy >= 1 && rgy <= D.ny - 2));
-    const uint32_t rcb = ring_om ? (uint32_t)(rgy * D.nx + rgx) * 4u : 0u;
+    const bool ring_om = has_ring && (D.per || (rgx >= 1 && rgx <= D.nx - 2 &&
+                                                (DIM == 2 || (rgy >= 1 && rgy <= D.ny - 2))));
+    const uint32_t rcb =
+        !ring_om ? 0u
+        : D.per  ? (uint32_t)(wrap_idx(rgy, D.ny) * D.nx + wrap_idx(rgx, D.nx)) * 4u
+                 : (uint32_t)(rgy * D.nx + rgx) * 4u;
 
     // R at physical plane zr, at node fi of a field slot and ri of an R tile, from
     // the field slots of the previous (sb), same (sc) and next (sn) march steps;
@@ -511,7 +540,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
             }
         }
         OP::residual(s, cc, K, R);
-        const bool om = om_xy && zr >= 1 && zr <= D.nz - 2;
+        const bool om = om_xy && (D.per || (zr >= 1 && zr <= D.nz - 2));
 #pragma unroll
         for (int b = 0; b < NR; ++b) {
             R[b] = om ? R[b] : 0.f;
@@ -526,7 +555,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
 #pragma unroll
         for (int j = 0; j < NC; ++j) {
             const __amdgpu_buffer_rsrc_t r = plane_rsrc_if(P.c[j], zr, pbytes, ok);
-            cown[j] = bld(r, cb);
+            cown[j] = bld(r, cbr);
             cring[j] = bld(r, rcb);
         }
     };
@@ -560,8 +589,8 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
         const bool zok = pz >= 0 && pz < D.nz;
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
-            const float v = bld(plane_rsrc(P.f[f], zok ? pz : 0, pbytes), cb);
-            fzm2[f] = (inarr && zok) ? v : 0.f;
+            const float v = bld(plane_rsrc(P.f[f], zok ? pz : 0, pbytes), cbr);
+            fzm2[f] = ((inarr || D.per) && zok) ? v : 0.f;
         }
     }
     load_consts(ph(0), true);
@@ -587,12 +616,12 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
             }
             fzm[f] = s[f].c;
         }
-        const int pz = ph(-1);  // in [0, nz): z0 - 1 >= 0 and z1 <= nz - 1
+        const int pz = ph(-1);  // in [0, nz): z0 - 1 >= 0 and z1 <= nz - 1, or wrapped
         float cc[NC1];
 #pragma unroll
-        for (int j = 0; j < NC; ++j) cc[j] = bld(plane_rsrc(P.c[j], pz, pbytes), cb);
+        for (int j = 0; j < NC; ++j) cc[j] = bld(plane_rsrc(P.c[j], pz, pbytes), cbr);
         OP::residual(s, cc, K, rzm);
-        const bool om = own_om && pz >= 1 && pz <= D.nz - 2;
+        const bool om = own_om && (D.per || (pz >= 1 && pz <= D.nz - 2));
 #pragma unroll
         for (int b = 0; b < NR; ++b) rzm[b] = om ? rzm[b] : 0.f;
     }

@@ -18,7 +18,7 @@ def shell_mask(shape):
     return m
 
 
-def run_gpu(wl, dloss=1.0, store_residual=True, order=("bwd", "bc")):
+def run_gpu(wl, dloss=1.0, store_residual=True, order=("bwd", "bc"), bc_mode=0):
     """fwd (+ residuals) then bwd and bc on cuda:0; outputs pre-filled with NaN so
     that untouched nodes are visible.  Returns numpy (R list, loss, grads list)."""
     import torch  # noqa: PLC0415
@@ -29,12 +29,13 @@ def run_gpu(wl, dloss=1.0, store_residual=True, order=("bwd", "bc")):
     R = None
     if store_residual:
         R = [torch.full_like(fields[0], float("nan")) for _ in wl.spec.residuals]
-    loss = B.fpde_residual_fwd(wl.op, fields, consts, wl.h, wl.coeffs, residual_out=R)
+    loss = B.fpde_residual_fwd(wl.op, fields, consts, wl.h, wl.coeffs, residual_out=R,
+                               bc_mode=bc_mode)
     dl = torch.tensor(float(dloss), dtype=torch.float64, device=dev)
     grads = [torch.full_like(f, float("nan")) for f in fields]
     for step in order:
         fn = B.fpde_residual_bwd if step == "bwd" else B.fpde_bc_correct
-        fn(wl.op, fields, consts, wl.h, wl.coeffs, dl, grads=grads)
+        fn(wl.op, fields, consts, wl.h, wl.coeffs, dl, grads=grads, bc_mode=bc_mode)
     torch.cuda.synchronize()
     Rn = [r.cpu().numpy() for r in R] if R is not None else None
     return Rn, float(loss.item()), [g.cpu().numpy() for g in grads]

@@ -129,7 +129,6 @@ def test_validation_status_codes(B, fn):
     # misaligned field
     assert _call(B, fn, op3, s3, fields=[_addr(0), _addr(1, 2), _addr(2), _addr(3)]) == ALIGN
     # periodic mode is reserved
-    assert _call(B, fn, op3, s3, bc_mode=1) == UNSUP
     assert _call(B, fn, op3, s3, bc_mode=7) == ARG
 
 
