@@ -11,6 +11,10 @@ Byte model (each input read once per pass, each output written once):
   fwd reads every field and const (the loss write is 8 bytes); bwd + bc read
   them again and write one gradient per field, so one step moves
   (2 (NF + NC) + NF) * 4 bytes per grid node (72 B/node for the 3D NS case).
+
+--path residual times the autograd form instead: fwd writing the residual
+arrays (on the residual set), then fpde_residual_vjp on resident upstream
+sensitivities (read on the residual set) writing every gradient node.
 """
 from __future__ import annotations
 
@@ -40,15 +44,22 @@ def parse():
                    help="planes of the oracle sample along axis 0 (0: sized automatically)")
     p.add_argument("--bc-mode", type=int, default=0, choices=(0, 1),
                    help="0: interior residual set (the benchmark); 1: periodic wrap on every axis")
+    p.add_argument("--path", default="loss", choices=("loss", "residual"),
+                   help="loss: fwd+loss, bwd, bc (the benchmark); residual: fwd writing R, "
+                        "then the explicit-sensitivity backward")
     p.add_argument("--sample-every", type=int, default=10,
                    help="per-kernel HIP events on every n-th timed step (the others carry none)")
     return p.parse_args()
 
 
-def byte_model(wl, bc_mode=0):
-    nf, nc = len(wl.spec.fields), len(wl.spec.consts)
+def byte_model(wl, bc_mode=0, path="loss"):
+    nf, nc, nr = len(wl.spec.fields), len(wl.spec.consts), len(wl.spec.residuals)
     N = wl.n_points
     M = N if bc_mode == 1 else wl.n_residual_points  # nodes the backward writes
+    if path == "residual":
+        fwd = (nf + nc) * 4 * N + nr * 4 * M + 8  # + the residual arrays on the residual set
+        vjp = nf * 4 * N + nr * 4 * M + nf * 4 * N  # fields, G on the residual set, grads
+        return {"step": fwd + vjp, "fwd": fwd, "vjp": vjp, "per_node": (2 * nf + nc + 2 * nr) * 4}
     return {
         "step": (2 * (nf + nc) + nf) * 4 * N + 8,
         "fwd": (nf + nc) * 4 * N + 8,
@@ -81,7 +92,7 @@ OP_KERNEL_TAG = {1: "OpBurgers", 2: "OpHelmholtz", 3: "OpHeat", 4: "OpNS<2, fals
                  5: "OpNS<3, true>"}
 
 
-def measured_traffic(cfg, op, kernel):
+def measured_traffic(cfg, op, kernel, path="loss"):
     """HBM bytes per launch of `kernel` ("fwd"/"bwd") from the committed rocprofv3
     counter summary, if it was taken on this workload with the current kernel
     sources; else None."""
@@ -92,6 +103,8 @@ def measured_traffic(cfg, op, kernel):
     rec = json.load(open(path))
     if rec.get("source_hash") != profiling.source_hash() or not rec.get("workload", "").startswith(cfg):
         return None
+    if rec.get("path", "loss") != path:  # (the residual path runs other kernel variants)
+        return None
     prefix = f"{kernel}_kernel<{OP_KERNEL_TAG[op]}"
     for name, v in rec.get("kernels", {}).items():
         if name.startswith(prefix):
@@ -99,7 +112,7 @@ def measured_traffic(cfg, op, kernel):
     return None
 
 
-def cpu_baseline(W, wl_full, cfg, seed, planes, bc_mode=0):
+def cpu_baseline(W, wl_full, cfg, seed, planes, bc_mode=0, path="loss"):
     """The oracle (single thread, float64) on a slab of the same workload."""
     import numpy as np  # noqa: PLC0415
     import oracle  # noqa: PLC0415  (CPU baseline leg only)
@@ -113,15 +126,24 @@ def cpu_baseline(W, wl_full, cfg, seed, planes, bc_mode=0):
     fields = [np.ascontiguousarray(f[sl], dtype=np.float64) for f in wl_full.fields]
     consts = [np.ascontiguousarray(c[sl], dtype=np.float64) for c in wl_full.consts]
     sshape = fields[0].shape
-    t0 = time.perf_counter()
-    oracle.loss(wl_full.op, sshape, wl_full.h, wl_full.coeffs, fields, consts, bc_mode=bc_mode)
-    oracle.grad(wl_full.op, sshape, wl_full.h, wl_full.coeffs, fields, consts, dloss=1.0,
-                bc_mode=bc_mode)
+    args = (wl_full.op, sshape, wl_full.h, wl_full.coeffs, fields, consts)
+    if path == "residual":
+        G = [np.ascontiguousarray(g[sl], dtype=np.float64)
+             for g in W.sensitivities(wl_full.op, shape, seed + 1)]
+        t0 = time.perf_counter()
+        oracle.residual(*args, bc_mode=bc_mode)
+        oracle.vjp(*args, G, bc_mode=bc_mode)
+        what = "residuals + transposed-Jacobian action"
+    else:
+        t0 = time.perf_counter()
+        oracle.loss(*args, bc_mode=bc_mode)
+        oracle.grad(*args, dloss=1.0, bc_mode=bc_mode)
+        what = "loss + full gradient"
     dt = time.perf_counter() - t0
     npts = int(np.prod(sshape))
     return {"value": npts / dt, "unit": "grid-points/s", "cores": 1, "kind": "oracle",
             "sample": f"{cfg} seed {seed}: first {planes} planes along axis 0 "
-                      f"({'x'.join(map(str, sshape))} = {npts} nodes), loss + full gradient, "
+                      f"({'x'.join(map(str, sshape))} = {npts} nodes), {what}, "
                       f"float64, single thread, {dt:.2f} s"}
 
 
@@ -163,8 +185,27 @@ def main():
     def bc():
         B.fpde_bc_correct(op, fields, consts, h, co, dl, grads=grads, bc_mode=bcm, stream=stream)
 
+    kernels = (("fwd", fwd), ("bwd", bwd), ("bc", bc))
+    if args.path == "residual":
+        R = [torch.empty_like(fields[0]) for _ in wl.spec.residuals]
+        sens = [torch.from_numpy(g).to(dev) for g in W.sensitivities(op, wl.shape, args.seed + 1)]
+
+        def fwd_r():
+            B.fpde_residual_fwd(op, fields, consts, h, co, residual_out=R, loss=loss, bc_mode=bcm,
+                                stream=stream)
+
+        def vjp():
+            B.fpde_residual_vjp(op, fields, h, co, sens, grads=grads, bc_mode=bcm, stream=stream)
+
+        kernels = (("fwd", fwd_r), ("vjp", vjp))
+    names = [n for n, _ in kernels]
+
+    def step():
+        for _, fn in kernels:
+            fn()
+
     for _ in range(args.warmup):
-        fwd(), bwd(), bc()
+        step()
     torch.cuda.synchronize()
 
     # Timed region: K steps between two events.  A timestamp between two kernels
@@ -173,44 +214,42 @@ def main():
     K = args.steps
     every = max(1, args.sample_every)
     sampled = [k for k in range(K) if k % every == every - 1] or [K - 1]
-    ev = {k: [torch.cuda.Event(enable_timing=True) for _ in range(4)] for k in sampled}
+    ev = {k: [torch.cuda.Event(enable_timing=True) for _ in range(len(kernels) + 1)]
+          for k in sampled}
     t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_start.record(stream)
     for k in range(K):
         e = ev.get(k)
         if e is None:
-            fwd(), bwd(), bc()
+            step()
             continue
         e[0].record(stream)
-        fwd()
-        e[1].record(stream)
-        bwd()
-        e[2].record(stream)
-        bc()
-        e[3].record(stream)
+        for i, (_, fn) in enumerate(kernels):
+            fn()
+            e[i + 1].record(stream)
     t_end.record(stream)
     torch.cuda.synchronize()
     total_s = t_start.elapsed_time(t_end) / 1e3
     per = {n: sum(ev[k][i].elapsed_time(ev[k][i + 1]) for k in sampled) / len(sampled) * 1e3
-           for i, n in enumerate(("fwd", "bwd", "bc"))}  # microseconds
+           for i, n in enumerate(names)}  # microseconds
     L = float(loss.item())
     if not (L == L) or L <= 0:
         raise RuntimeError(f"bad loss {L}")
 
-    bm = byte_model(wl, bcm)
+    bm = byte_model(wl, bcm, args.path)
     N = wl.n_points
     ms = total_s / K * 1e3
     gbps = bm["step"] * K / total_s / 1e9
-    dom = max(("fwd", "bwd"), key=lambda n: per[n])
+    dom = max((n for n in names if n in bm), key=lambda n: per[n])
     achieved = bm[dom] / (per[dom] * 1e-6) / 1e9
     roofline = {"bound": "hbm", "kernel": f"{dom} ({cfg})", "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                "traffic": measured_traffic(cfg, wl.op, dom),
+                "traffic": measured_traffic(cfg, wl.op, dom, args.path),
                 "algorithmic_bytes_per_launch": bm[dom], "avg_launch_us": round(per[dom], 2)}
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(W, wl, cfg, args.seed, args.cpu_planes, bcm)
+        cpu = cpu_baseline(W, wl, cfg, args.seed, args.cpu_planes, bcm, args.path)
     out = {
         "metric": METRIC,
         "value": N * K / total_s,
@@ -227,8 +266,10 @@ def main():
         "config": {"workload": f"{cfg}: {W.CONFIGS[cfg].description}",
                    "grid": list(wl.shape), "nodes": N,
                    "fields": list(wl.spec.fields), "consts": list(wl.spec.consts),
-                   "seed": args.seed, "step": "fwd+loss, bwd, bc on one stream",
-                   "bc_mode": bcm},
+                   "seed": args.seed,
+                   "step": ("fwd+loss, bwd, bc on one stream" if args.path == "loss" else
+                            "fwd writing residuals, explicit-sensitivity vjp on one stream"),
+                   "path": args.path, "bc_mode": bcm},
         "hbm_gbps": round(gbps, 1),
         "hbm_frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4),
         "bytes_per_step": bm["step"],

@@ -9,6 +9,9 @@
  * backward recomputes the residuals it needs instead of reading an upstream
  * sensitivity tensor, so one call sequence is
  *     fpde_residual_fwd -> fpde_residual_bwd + fpde_bc_correct.
+ * fpde_residual_vjp is the general backward of Sec. 2.2: it applies the
+ * transposed residual Jacobian to upstream sensitivities the caller supplies,
+ * for objectives other than the mean-squared loss.
  *
  * Notation (used by every entry point):
  *   - arrays are dense C-contiguous float32, shape n[0..ndim-1], last axis
@@ -40,7 +43,7 @@
  *       R_div = sum_a D1_a c_a
  *
  * Common argument rules:
- *   - `fields`, `consts`, `residual_out`, `grads` are HOST arrays holding
+ *   - `fields`, `consts`, `residual_out`, `sens`, `grads` are HOST arrays holding
  *     DEVICE pointers, one per array in the order listed above (`consts` may be
  *     NULL for ops without consts).  Every device array is n[0]*...*n[ndim-1]
  *     floats, 4-byte aligned, allocated on the current HIP device.
@@ -150,6 +153,26 @@ int fpde_residual_bwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
 int fpde_bc_correct(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
                     const float* const* fields, const float* const* consts,
                     const double* dloss, float* const* grads, void* stream);
+
+/* Explicit-sensitivity backward: the transpose-Jacobian action of the
+ * residual operator on upstream residual sensitivities G_b = dObj/dR_b, the
+ * form in which the backward of Sec. 2.2 receives them from autograd:
+ *     grads[q](n) (+)= sum_b sum_{m in Omega} G_b(m) dR_b(m)/dq(n)
+ * for every node n of every field q, boundary nodes included.
+ *   sens        host array of n_residuals device pointers, full-size arrays in
+ *               the residual order of the op; only the values on Omega are
+ *               read (entries off Omega are ignored, whatever they hold).
+ *   accumulate  0: grads are OVERWRITTEN with the action; 1: the action is
+ *               ADDED to what grads hold (every node read, then written once).
+ *               Any other value: FPDE_ERR_ARG.
+ *   grads       host array of n_fields device pointers; every node of every
+ *               array is written, so no bc call follows this one.
+ * The consts enter every residual additively, so the Jacobian, and this call,
+ * do not depend on them: none are passed.  grads must not overlap the fields,
+ * the sensitivities or each other (FPDE_ERR_ARG).  Queues 1 kernel; no atomics. */
+int fpde_residual_vjp(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+                      const float* const* fields, const float* const* sens, int accumulate,
+                      float* const* grads, void* stream);
 
 /* Static string naming a status code (never NULL). */
 const char* fpde_status_string(int status);

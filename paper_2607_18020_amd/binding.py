@@ -21,7 +21,7 @@ STATUS_NAMES = {0: "FPDE_OK", -1: "FPDE_ERR_ARG", -2: "FPDE_ERR_SHAPE", -3: "FPD
                 -4: "FPDE_ERR_COEFF", -5: "FPDE_ERR_ALIGN", -6: "FPDE_ERR_HIP",
                 -7: "FPDE_ERR_UNSUPPORTED"}
 EXPORTED = ("fpde_op_info", "fpde_residual_fwd", "fpde_residual_bwd", "fpde_bc_correct",
-            "fpde_status_string", "fpde_version")
+            "fpde_residual_vjp", "fpde_status_string", "fpde_version")
 
 
 class FpdeGrid(ctypes.Structure):
@@ -56,7 +56,9 @@ def _load():
         lib.fpde_residual_fwd.argtypes = [ctypes.c_int, gp, cp, pp, pp, pp, vp, vp]
         lib.fpde_residual_bwd.argtypes = [ctypes.c_int, gp, cp, pp, pp, vp, pp, vp]
         lib.fpde_bc_correct.argtypes = [ctypes.c_int, gp, cp, pp, pp, vp, pp, vp]
-        for name in ("fpde_op_info", "fpde_residual_fwd", "fpde_residual_bwd", "fpde_bc_correct"):
+        lib.fpde_residual_vjp.argtypes = [ctypes.c_int, gp, cp, pp, pp, ctypes.c_int, pp, vp]
+        for name in ("fpde_op_info", "fpde_residual_fwd", "fpde_residual_bwd", "fpde_bc_correct",
+                     "fpde_residual_vjp"):
             getattr(lib, name).restype = ctypes.c_int
         lib.fpde_status_string.argtypes = [ctypes.c_int]
         lib.fpde_status_string.restype = ctypes.c_char_p
@@ -167,24 +169,80 @@ def fpde_bc_correct(op: int, fields, consts, h, coeffs, dloss, *, grads=None, bc
                       coeffs, dloss, grads, bc_mode, stream)
 
 
+def fpde_residual_vjp(op: int, fields, h, coeffs, sens, *, grads=None, accumulate: bool = False,
+                      bc_mode: int = 0, stream=None):
+    """Queue the transposed-Jacobian action on upstream residual sensitivities
+    ``sens`` (one full-size array per residual; read on the residual set only).
+    Overwrites ``grads`` (allocated if None), or adds to them if ``accumulate``."""
+    shape = tuple(fields[0].shape)
+    _check_tensors(list(fields) + list(sens), shape, "fpde_residual_vjp")
+    if grads is None:
+        if accumulate:
+            raise ValueError("fpde_residual_vjp: accumulate needs grads")
+        grads = [torch.empty_like(f) for f in fields]
+    _check_tensors(grads, shape, "fpde_residual_vjp grads")
+    g, c = make_grid(shape, h, bc_mode), make_coeffs(coeffs)
+    st = _load().fpde_residual_vjp(int(op), ctypes.byref(g), ctypes.byref(c), _ptr_array(fields),
+                                   _ptr_array(sens), int(bool(accumulate)), _ptr_array(grads),
+                                   _stream(stream))
+    if st != FPDE_OK:
+        raise FpdeError(st, "fpde_residual_vjp")
+    return grads
+
+
+class Residual(torch.autograd.Function):
+    """Drop-in differentiable residual op: forward = the fused stencil writing
+    the residual arrays (zero off the residual set), backward = the
+    explicit-sensitivity transposed-Jacobian action on their gradients.
+
+    Usage: ``R = Residual.apply(op, h, coeffs, consts, bc_mode, *fields)`` (a
+    tuple with one tensor per residual); any objective of R can follow.
+    """
+
+    @staticmethod
+    def forward(ctx, op, h, coeffs, consts, bc_mode, *fields):
+        fields = [f.contiguous() for f in fields]
+        ctx.op, ctx.h, ctx.coeffs, ctx.bc_mode = op, h, coeffs, bc_mode
+        ctx.save_for_backward(*fields)
+        nr = op_info(op)[3]
+        R = [torch.zeros_like(fields[0]) for _ in range(nr)]
+        fpde_residual_fwd(op, fields, consts, h, coeffs, residual_out=R, bc_mode=bc_mode)
+        return tuple(R)
+
+    @staticmethod
+    def backward(ctx, *gR):
+        fields = list(ctx.saved_tensors)
+        sens = [torch.zeros_like(fields[0]) if g is None else g.detach().float().contiguous()
+                for g in gR]
+        grads = fpde_residual_vjp(ctx.op, fields, ctx.h, ctx.coeffs, sens, bc_mode=ctx.bc_mode)
+        return (None, None, None, None, None, *grads)
+
+
 class ResidualLoss(torch.autograd.Function):
     """Drop-in differentiable loss op: forward = fused stencil + MSE loss,
     backward = interior adjoint + boundary correction with dloss = grad_output.
 
-    Usage: ``loss = ResidualLoss.apply(op, h, coeffs, consts, *fields)``.
+    Usage: ``loss = ResidualLoss.apply(op, h, coeffs, consts, *fields)``;
+    ``ResidualLoss.apply(op, h, coeffs, consts, bc_mode, *fields)`` with an int
+    ``bc_mode`` before the fields selects the boundary mode (0 by default).
     """
 
     @staticmethod
-    def forward(ctx, op, h, coeffs, consts, *fields):
-        fields = [f.contiguous() for f in fields]
-        ctx.op, ctx.h, ctx.coeffs, ctx.consts = op, h, coeffs, consts
+    def forward(ctx, op, h, coeffs, consts, *rest):
+        bc_mode = 0
+        ctx.n_lead = 4 + (len(rest) > 0 and not isinstance(rest[0], torch.Tensor))
+        if ctx.n_lead == 5:
+            bc_mode, rest = int(rest[0]), rest[1:]
+        fields = [f.contiguous() for f in rest]
+        ctx.op, ctx.h, ctx.coeffs, ctx.consts, ctx.bc_mode = op, h, coeffs, consts, bc_mode
         ctx.save_for_backward(*fields)
-        return fpde_residual_fwd(op, fields, consts, h, coeffs)
+        return fpde_residual_fwd(op, fields, consts, h, coeffs, bc_mode=bc_mode)
 
     @staticmethod
     def backward(ctx, gout):
         fields = list(ctx.saved_tensors)
         dl = gout.detach().to(torch.float64).reshape(()).contiguous()
-        grads = fpde_residual_bwd(ctx.op, fields, ctx.consts, ctx.h, ctx.coeffs, dl)
-        fpde_bc_correct(ctx.op, fields, ctx.consts, ctx.h, ctx.coeffs, dl, grads=grads)
-        return (None, None, None, None, *grads)
+        kw = dict(bc_mode=ctx.bc_mode)
+        grads = fpde_residual_bwd(ctx.op, fields, ctx.consts, ctx.h, ctx.coeffs, dl, **kw)
+        fpde_bc_correct(ctx.op, fields, ctx.consts, ctx.h, ctx.coeffs, dl, grads=grads, **kw)
+        return (None,) * ctx.n_lead + tuple(grads)

@@ -64,6 +64,13 @@ bool op_desc(int op, OpDesc* d) {
 #ifndef FPDE_TX2
 #define FPDE_TX2 256
 #endif
+// explicit-sensitivity backward tiles (3-D)
+#ifndef FPDE_VJP_TX3
+#define FPDE_VJP_TX3 64
+#endif
+#ifndef FPDE_VJP_TY3
+#define FPDE_VJP_TY3 8
+#endif
 #ifndef FPDE_BLOCKS2
 #define FPDE_BLOCKS2 1024
 #endif
@@ -101,15 +108,18 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 
 bool finite_pos(double v) { return isfinite(v) && v > 0.0; }
 
-// Validates everything except the outputs; fills req.
+// Validates everything except the outputs; fills req.  need_consts: the call
+// reads the const arrays (the explicit-sensitivity backward does not).
 int validate_common(int op, const fpde_grid* g, const fpde_coeffs* c, const float* const* fields,
-                    const float* const* consts, Req* r) {
+                    const float* const* consts, Req* r, bool need_consts = true) {
     if (!op_desc(op, &r->d)) return FPDE_ERR_ARG;
     if (!g || !c || !fields) return FPDE_ERR_ARG;
-    if (r->d.nc > 0 && !consts) return FPDE_ERR_ARG;
+    if (!need_consts) consts = nullptr;
+    const int nc = need_consts ? r->d.nc : 0;
+    if (nc > 0 && !consts) return FPDE_ERR_ARG;
     for (int f = 0; f < r->d.nf; ++f)
         if (!fields[f]) return FPDE_ERR_ARG;
-    for (int j = 0; j < r->d.nc; ++j)
+    for (int j = 0; j < nc; ++j)
         if (!consts[j]) return FPDE_ERR_ARG;
     if (g->bc_mode != 0 && g->bc_mode != 1) return FPDE_ERR_ARG;
     if (g->ndim != r->d.ndim) return FPDE_ERR_SHAPE;
@@ -149,7 +159,7 @@ int validate_common(int op, const fpde_grid* g, const fpde_coeffs* c, const floa
 
     for (int f = 0; f < r->d.nf; ++f)
         if ((uintptr_t)fields[f] & 3u) return FPDE_ERR_ALIGN;
-    for (int j = 0; j < r->d.nc; ++j)
+    for (int j = 0; j < nc; ++j)
         if ((uintptr_t)consts[j] & 3u) return FPDE_ERR_ALIGN;
 
     r->op = op;
@@ -160,7 +170,7 @@ int validate_common(int op, const fpde_grid* g, const fpde_coeffs* c, const floa
     r->two_over_M = 2.0 / (double)M;
     memset(&r->P, 0, sizeof r->P);
     for (int f = 0; f < r->d.nf; ++f) r->P.f[f] = fields[f];
-    for (int j = 0; j < r->d.nc; ++j) r->P.c[j] = consts[j];
+    for (int j = 0; j < nc; ++j) r->P.c[j] = consts[j];
 
     Dims& dm = r->dims;  // sizes only; tiles and chunks are set per launch
     dm.nz = (int)g->n[0];
@@ -258,6 +268,33 @@ int launch_bc(const Req& r, const double* dloss) {
     hipLaunchKernelGGL((bc_kernel<OP>), dim3((unsigned)nb), dim3(256), 0, r.stream, r.P, r.dims,
                        r.K, dloss, r.two_over_M);
     return hip_status();
+}
+
+// Explicit-sensitivity backward: every plane of axis 0 is marched (zlo = 0).
+template <class OP, int TX, int TY>
+int launch_vjp(const Req& r, bool acc, int target) {
+    Dims base = r.dims;
+    base.zlo = 0;
+    const Dims dm = tile_dims(base, TX, TY, chunk_planes(base, TX, TY, target));
+    if (acc)
+        hipLaunchKernelGGL((vjp_kernel<OP, TX, TY, true>), dim3(dm.nblocks), dim3(TX * TY), 0,
+                           r.stream, r.P, dm, r.K);
+    else
+        hipLaunchKernelGGL((vjp_kernel<OP, TX, TY, false>), dim3(dm.nblocks), dim3(TX * TY), 0,
+                           r.stream, r.P, dm, r.K);
+    return hip_status();
+}
+
+int run_vjp(const Req& r, bool acc) {
+    constexpr int kTarget3 = 512;  // workgroups per launch (3-D)
+    switch (r.op) {
+    case FPDE_BURGERS_1DT: return launch_vjp<OpBurgers, kTX2, 1>(r, acc, kTargetBlocks2);
+    case FPDE_HELMHOLTZ_2D: return launch_vjp<OpHelmholtz, kTX2, 1>(r, acc, kTargetBlocks2);
+    case FPDE_HEAT_3D_BE: return launch_vjp<OpHeat, FPDE_VJP_TX3, FPDE_VJP_TY3>(r, acc, kTarget3);
+    case FPDE_NS_2D_STEADY: return launch_vjp<OpNS2, kTX2, 1>(r, acc, kTargetBlocks2);
+    case FPDE_NS_3D_BE: return launch_vjp<OpNS3, FPDE_VJP_TX3, FPDE_VJP_TY3>(r, acc, kTarget3);
+    }
+    return FPDE_ERR_ARG;
 }
 
 int run_fwd(const Req& r, bool store, double* loss) {
@@ -365,6 +402,35 @@ extern "C" int fpde_bc_correct(int op, const fpde_grid* grid, const fpde_coeffs*
     const int st = prepare_grad_call(op, grid, coeffs, fields, consts, dloss, grads, stream, &r);
     if (st != FPDE_OK) return st;
     return run_bc(r, dloss);
+}
+
+extern "C" int fpde_residual_vjp(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+                                 const float* const* fields, const float* const* sens,
+                                 int accumulate, float* const* grads, void* stream) {
+    Req r;
+    int st = validate_common(op, grid, coeffs, fields, nullptr, &r, false);
+    if (st != FPDE_OK) return st;
+    if (!sens || !grads) return FPDE_ERR_ARG;
+    if (accumulate != 0 && accumulate != 1) return FPDE_ERR_ARG;
+    const size_t bytes = (size_t)r.N * sizeof(float);
+    for (int b = 0; b < r.d.nr; ++b) {
+        if (!sens[b]) return FPDE_ERR_ARG;
+        if ((uintptr_t)sens[b] & 3u) return FPDE_ERR_ALIGN;
+    }
+    for (int f = 0; f < r.d.nf; ++f) {
+        if (!grads[f]) return FPDE_ERR_ARG;
+        if ((uintptr_t)grads[f] & 3u) return FPDE_ERR_ALIGN;
+        for (int q = 0; q < r.d.nf; ++q)
+            if (overlaps(grads[f], bytes, fields[q], bytes)) return FPDE_ERR_ARG;
+        for (int b = 0; b < r.d.nr; ++b)
+            if (overlaps(grads[f], bytes, sens[b], bytes)) return FPDE_ERR_ARG;
+        for (int q = 0; q < f; ++q)
+            if (overlaps(grads[f], bytes, grads[q], bytes)) return FPDE_ERR_ARG;
+    }
+    for (int b = 0; b < r.d.nr; ++b) r.P.s[b] = sens[b];
+    for (int f = 0; f < r.d.nf; ++f) r.P.out[f] = grads[f];
+    r.stream = (hipStream_t)stream;
+    return run_vjp(r, accumulate == 1);
 }
 
 extern "C" const char* fpde_status_string(int status) {

@@ -47,6 +47,9 @@
 #ifndef FPDE_BWD_MINW
 #define FPDE_BWD_MINW 1
 #endif
+#ifndef FPDE_VJP_MINW
+#define FPDE_VJP_MINW 1
+#endif
 
 namespace fpde {
 
@@ -54,6 +57,7 @@ struct Ptrs {
     const float* f[4];
     const float* c[3];
     float* out[4];
+    const float* s[4];  // caller-given residual sensitivities (explicit-sensitivity backward)
 };
 
 struct Dims {
@@ -698,6 +702,145 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
 
     int w = 0;
     for (; w + 4 <= L; w += 4) {  // slot and buffer indices are constants in each copy
+        step(IC<0>{}, w);
+        step(IC<1>{}, w + 1);
+        step(IC<2>{}, w + 2);
+        step(IC<3>{}, w + 3);
+    }
+    if (w < L) step(IC<0>{}, w);
+    if (w + 1 < L) step(IC<1>{}, w + 1);
+    if (w + 2 < L) step(IC<2>{}, w + 2);
+}
+
+// ---------------------------------------------------------------------------
+// Explicit-sensitivity backward: grads (=, or += when ACC) J^T G for caller-given
+// residual sensitivities G_b = dL/dR_b (Sec. 2.2).  The gather is the one above
+// with G in place of the recomputed residuals, so no residual, const or ring is
+// needed: fields and sensitivities (radius 1) stream through one LDS ring with
+// the forward's slot layout, and the march covers every plane 0..nz-1, writing
+// every node once (boundary shell included: G is zero off the residual set,
+// which the loads enforce with out-of-range offsets, whatever the arrays hold
+// there).
+
+template <class OP, int TX, int TY, bool ACC>
+__global__ __launch_bounds__(TX* TY, FPDE_VJP_MINW) void vjp_kernel(Ptrs P, Dims D, KCoef K) {
+    constexpr int DIM = OP::DIM, NF = OP::NF, NR = OP::NR, NT = TX * TY;
+    constexpr int NA = NF + NR;  // arrays per slot: fields, then sensitivities
+    constexpr int HY = (DIM == 3) ? 1 : 0;
+    constexpr int LY = TY + 2 * HY, LX = TX, XG = LY * LX;
+    static_assert(TX % 64 == 0, "a wavefront loads whole aligned row segments");
+    static_assert(2 * TY <= 64, "the side-edge neighbours fill one 64-element group");
+    using PS = PlaneStream<XG + 64, NT>;
+    static_assert(DIM == 3 || TY == 1, "2-D grids use one-row tiles");
+    FPDE_SLOT_RING(float, sF, NA, PS::FSZS);
+
+    const int t = threadIdx.x, tx = t % TX, ty = t / TX;
+    const TileCoord tc = tile_coord<TX, TY>(D);  // (D.zlo = 0: every plane)
+    const int z0 = tc.z0, z1 = tc.z1, L = z1 - z0;
+    const int gx = tc.gx0 + tx, gy = (DIM == 3) ? tc.gy0 + ty : 0;
+    const uint32_t pbytes = (uint32_t)D.ny * (uint32_t)D.nx * 4u;
+    const bool inarr = gx < D.nx && gy < D.ny;
+    const uint32_t cb = inarr ? (uint32_t)(gy * D.nx + gx) * 4u : 0u;
+    auto zw = [&](int z) { return D.per ? wrap_idx(z, D.nz) : z; };  // plane index
+
+    // slot element -> grid position (the forward's layout); for the
+    // sensitivities, positions off the residual set read as 0
+    auto node_at = [&](int i, int& lin, bool omega) {
+        int py, px;
+        if (i < XG) {
+            py = (DIM == 3) ? tc.gy0 - HY + i / LX : 0;
+            px = tc.gx0 + i % LX;
+        } else {
+            const int j = i - XG, side = j / TY;
+            py = (DIM == 3) ? tc.gy0 + j % TY : 0;
+            px = side == 0 ? tc.gx0 - 1 : tc.gx0 + TX;
+            if (side > 1) return false;
+        }
+        if (D.per) {
+            px = wrap_idx(px, D.nx);
+            py = wrap_idx(py, D.ny);
+        }
+        lin = py * D.nx + px;
+        if (omega && !D.per)
+            return px >= 1 && px <= D.nx - 2 && (DIM == 2 || (py >= 1 && py <= D.ny - 2));
+        return px >= 0 && px < D.nx && py >= 0 && py < D.ny;
+    };
+    PS psf, psg;
+    psf.init(t, [&](int i, int& lin) { return node_at(i, lin, false); });
+    psg.init(t, [&](int i, int& lin) { return node_at(i, lin, true); });
+    // plane pz (wrapped or -1) of the fields and the sensitivities into a slot;
+    // the sensitivities of a plane off the residual set read as 0
+    auto load_plane = [&](int pz, auto slot) __attribute__((always_inline)) {
+        float* dst[NA];
+#pragma unroll
+        for (int a = 0; a < NA; ++a) dst[a] = &sF(slot)[a][0];
+        psf.template load<NF>(P.f, pz, D.nz, pbytes, dst);
+        const bool gok = D.per || (pz >= 1 && pz <= D.nz - 2);
+        psg.template load<NR>(P.s, gok ? pz : -1, D.nz, pbytes, dst + NF);
+    };
+    float gq[2][NF];  // accumulate mode: the stored gradients of the next plane
+    auto load_old = [&](int pz, bool ok, float* o) __attribute__((always_inline)) {
+        if (ACC) {
+#pragma unroll
+            for (int f = 0; f < NF; ++f) o[f] = bld(plane_rsrc_if(P.out[f], pz, pbytes, ok), cb);
+        }
+    };
+
+    // plane z0 + j lives in slot (j + 1) & 3; prologue: planes z0-1, z0, z0+1
+    load_plane(zw(z0 - 1), IC<0>{});
+    load_plane(z0, IC<1>{});
+    load_plane(zw(z0 + 1), IC<2>{});
+    load_old(z0, true, gq[0]);
+    __syncthreads();
+
+    const int own = (ty + HY) * LX + tx;  // own node in a slot
+    const int xm = tx == 0 ? XG + ty : own - 1, xp = tx == TX - 1 ? XG + TY + ty : own + 1;
+    auto star = [&](auto sm, auto sc, auto sp, int a, Star& st) __attribute__((always_inline)) {
+        const float* c = &sF(sc)[a][0];
+        st.c = c[own];
+        st.m[0] = sF(sm)[a][own];
+        st.p[0] = sF(sp)[a][own];
+        st.m[DIM - 1] = c[xm];
+        st.p[DIM - 1] = c[xp];
+        if (DIM == 3) {
+            st.m[1] = c[own - LX];
+            st.p[1] = c[own + LX];
+        }
+    };
+    auto step = [&](auto jc, int w) __attribute__((always_inline)) {
+        constexpr int J = decltype(jc)::value;  // w & 3
+        constexpr int SM = J & 3, SC = (J + 1) & 3, SP = (J + 2) & 3, SQ = (J + 3) & 3;
+        constexpr int CUR = J & 1, NXT = (J + 1) & 1;
+        const int z = z0 + w;
+        const bool more = w + 1 < L;
+        // plane z+2 goes to the slot of plane z-2, last read before the previous barrier
+        load_plane(more ? zw(z + 2) : -1, IC<SQ>{});
+        __builtin_amdgcn_sched_barrier(0);  // (the plane loads first, as in the forward)
+        load_old(z + 1, more, gq[NXT]);
+        Star fs[NF], gs[NR];
+#pragma unroll
+        for (int f = 0; f < NF; ++f) star(IC<SM>{}, IC<SC>{}, IC<SP>{}, f, fs[f]);
+#pragma unroll
+        for (int b = 0; b < NR; ++b) star(IC<SM>{}, IC<SC>{}, IC<SP>{}, NF + b, gs[b]);
+        float g[NF];
+        OP::gather(fs, gs, K, g);
+        const uint32_t so = inarr ? cb : kDropOff;
+#pragma unroll
+        for (int f = 0; f < NF; ++f) {
+            float v = g[f];
+            if (ACC) {
+                // the stored value plus the action, each rounded on its own: the
+                // add is kept apart from the product that formed the action
+                asm volatile("" : "+v"(v));
+                v = gq[CUR][f] + v;
+            }
+            bst<kStream>(plane_rsrc(P.out[f], z, pbytes), so, v);
+        }
+        __syncthreads();  // (waits for the plane loads into LDS as well)
+    };
+
+    int w = 0;
+    for (; w + 4 <= L; w += 4) {  // slot indices are constants in each copy
         step(IC<0>{}, w);
         step(IC<1>{}, w + 1);
         step(IC<2>{}, w + 2);

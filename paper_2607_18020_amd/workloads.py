@@ -260,3 +260,11 @@ def normal_fields(op: int, shape: Sequence[int], seed: int,
                   NS_3D_BE: Coeffs(nu=0.01, dt=1e-2)}[op]
     return Workload(f"normal_{OP_NAMES[op]}", op, shape, tuple(float(x) for x in h), coeffs,
                     fields, consts)
+
+
+def sensitivities(op: int, shape: Sequence[int], seed: int) -> List[np.ndarray]:
+    """Upstream residual sensitivities G_b (one standard-normal float32 array
+    per residual, full size) for the explicit-sensitivity backward."""
+    rng = np.random.default_rng(seed)
+    return [_f32(rng.standard_normal(tuple(int(s) for s in shape)))
+            for _ in OPS[op].residuals]

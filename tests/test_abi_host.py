@@ -76,7 +76,8 @@ def _arr(vals):
 
 
 def _call(B, fn, op, shape, h=None, coef=W.Coeffs(nu=0.01, k=1.0, dt=0.1, alpha=0.1),
-          fields=None, consts=None, outs=None, scalar=None, bc_mode=0, ndim=None):
+          fields=None, consts=None, outs=None, scalar=None, bc_mode=0, ndim=None, sens=None,
+          accumulate=0):
     lib = B.lib()
     spec = W.OPS[op]
     h = h if h is not None else (0.1,) * len(shape)
@@ -94,6 +95,10 @@ def _call(B, fn, op, shape, h=None, coef=W.Coeffs(nu=0.01, k=1.0, dt=0.1, alpha=
                                      _arr(consts) if nc else None,
                                      _arr(outs) if outs is not None else None, scalar, None)
     outs = outs if outs is not None else [_addr(20 + i) for i in range(nf)]
+    if fn == "vjp":
+        sens = sens if sens is not None else [_addr(40 + b) for b in range(nr)]
+        return lib.fpde_residual_vjp(op, ctypes.byref(g), ctypes.byref(c), _arr(fields),
+                                     _arr(sens), accumulate, _arr(outs), None)
     f = lib.fpde_residual_bwd if fn == "bwd" else lib.fpde_bc_correct
     return f(op, ctypes.byref(g), ctypes.byref(c), _arr(fields), _arr(consts) if nc else None,
              scalar, _arr(outs), None)
@@ -102,7 +107,7 @@ def _call(B, fn, op, shape, h=None, coef=W.Coeffs(nu=0.01, k=1.0, dt=0.1, alpha=
 ARG, SHAPE, SPACING, COEFF, ALIGN, UNSUP = -1, -2, -3, -4, -5, -7
 
 
-@pytest.mark.parametrize("fn", ["fwd", "bwd", "bc"])
+@pytest.mark.parametrize("fn", ["fwd", "bwd", "bc", "vjp"])
 def test_validation_status_codes(B, fn):
     op3, op2 = W.NS_3D_BE, W.NS_2D_STEADY
     s3 = (8, 9, 10)
@@ -125,7 +130,8 @@ def test_validation_status_codes(B, fn):
     assert _call(B, fn, W.HEAT_3D_BE, s3, coef=W.Coeffs(dt=-1.0, alpha=0.1)) == COEFF
     # null field / const pointers
     assert _call(B, fn, op3, s3, fields=[_addr(0), 0, _addr(2), _addr(3)]) == ARG
-    assert _call(B, fn, op3, s3, consts=[_addr(10), _addr(11), 0]) == ARG
+    if fn != "vjp":
+        assert _call(B, fn, op3, s3, consts=[_addr(10), _addr(11), 0]) == ARG
     # misaligned field
     assert _call(B, fn, op3, s3, fields=[_addr(0), _addr(1, 2), _addr(2), _addr(3)]) == ALIGN
     # periodic mode is reserved
@@ -153,6 +159,17 @@ def test_output_checks(B):
         assert _call(B, fn, op, s3, outs=[_addr(20), _addr(21), _addr(22), _addr(30, 0)],
                      scalar=_addr(30, 16)) == ARG
         assert _call(B, fn, op, s3, outs=[_addr(20), _addr(21), _addr(22), _addr(23, 2)]) == ALIGN
+    # vjp: accumulate flag, null / misaligned sensitivities, grads aliasing fields,
+    # sensitivities or each other
+    assert _call(B, "vjp", op, s3, accumulate=2) == ARG
+    assert _call(B, "vjp", op, s3, accumulate=-1) == ARG
+    assert _call(B, "vjp", op, s3, sens=[_addr(40), 0, _addr(42), _addr(43)]) == ARG
+    assert _call(B, "vjp", op, s3, sens=[_addr(40), _addr(41, 2), _addr(42), _addr(43)]) == ALIGN
+    assert _call(B, "vjp", op, s3, outs=[_addr(20), _addr(1, 8), _addr(22), _addr(23)]) == ARG
+    assert _call(B, "vjp", op, s3, outs=[_addr(20), _addr(21), _addr(42, nbytes - 4), _addr(23)]) == ARG
+    assert _call(B, "vjp", op, s3, outs=[_addr(20), _addr(20), _addr(22), _addr(23)]) == ARG
+    assert _call(B, "vjp", op, s3, outs=[_addr(20), _addr(21), 0, _addr(23)]) == ARG
+    assert _call(B, "vjp", op, s3, outs=[_addr(20), _addr(21), _addr(22), _addr(23, 2)]) == ALIGN
 
 
 def test_product_path_shares_nothing_with_the_oracle():
