@@ -13,8 +13,9 @@ Byte model (each input read once per pass, each output written once):
   (2 (NF + NC) + NF) * 4 bytes per grid node (72 B/node for the 3D NS case).
 
 --path residual times the autograd form instead: fwd writing the residual
-arrays (on the residual set), then fpde_residual_vjp on resident upstream
-sensitivities (read on the residual set) writing every gradient node.
+arrays (every node; zero off the residual set), then fpde_residual_vjp on
+resident upstream sensitivities (read on the residual set), reading the fields
+the Jacobian depends on and writing every gradient node.
 """
 from __future__ import annotations
 
@@ -52,14 +53,22 @@ def parse():
     return p.parse_args()
 
 
+# fields the residual Jacobian depends on (what the explicit-sensitivity backward
+# reads besides G): none for the linear operators, the velocity but not the
+# pressure for NS
+JAC_FIELDS = {1: 1, 2: 0, 3: 0, 4: 2, 5: 3}
+
+
 def byte_model(wl, bc_mode=0, path="loss"):
     nf, nc, nr = len(wl.spec.fields), len(wl.spec.consts), len(wl.spec.residuals)
     N = wl.n_points
     M = N if bc_mode == 1 else wl.n_residual_points  # nodes the backward writes
     if path == "residual":
-        fwd = (nf + nc) * 4 * N + nr * 4 * M + 8  # + the residual arrays on the residual set
-        vjp = nf * 4 * N + nr * 4 * M + nf * 4 * N  # fields, G on the residual set, grads
-        return {"step": fwd + vjp, "fwd": fwd, "vjp": vjp, "per_node": (2 * nf + nc + 2 * nr) * 4}
+        nfg = JAC_FIELDS[wl.op]
+        fwd = (nf + nc + nr) * 4 * N + 8  # + the residual arrays (every node is written)
+        vjp = nfg * 4 * N + nr * 4 * M + nf * 4 * N  # fields, G on the residual set, grads
+        return {"step": fwd + vjp, "fwd": fwd, "vjp": vjp,
+                "per_node": (2 * nf + nc + 2 * nr + nfg) * 4}
     return {
         "step": (2 * (nf + nc) + nf) * 4 * N + 8,
         "fwd": (nf + nc) * 4 * N + 8,

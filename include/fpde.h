@@ -114,9 +114,9 @@ int fpde_op_info(int op, int* ndim, int* n_fields, int* n_consts, int* n_residua
 
 /* Fused forward stencil + mean-squared residual loss (Sec. 2.1).
  *   loss          device pointer to one double; OVERWRITTEN with L (not accumulated).
- *   residual_out  NULL, or a host array of n_residuals device pointers: R_b is
- *                 written on Omega only; nodes off Omega are left untouched
- *                 (periodic grids: every node).
+ *   residual_out  NULL, or a host array of n_residuals device pointers: every
+ *                 node of R_b is written, R_b(m) on Omega and 0 off Omega
+ *                 (periodic grids: Omega is every node).
  * Queues 2 kernels: a one-element fill that zeroes *loss, then the stencil
  * kernel (one float64 atomic add per workgroup onto *loss). */
 int fpde_residual_fwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,

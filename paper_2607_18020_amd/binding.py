@@ -205,7 +205,7 @@ class Residual(torch.autograd.Function):
         ctx.op, ctx.h, ctx.coeffs, ctx.bc_mode = op, h, coeffs, bc_mode
         ctx.save_for_backward(*fields)
         nr = op_info(op)[3]
-        R = [torch.zeros_like(fields[0]) for _ in range(nr)]
+        R = [torch.empty_like(fields[0]) for _ in range(nr)]  # (every node is written)
         fpde_residual_fwd(op, fields, consts, h, coeffs, residual_out=R, bc_mode=bc_mode)
         return tuple(R)
 

@@ -69,7 +69,16 @@ bool op_desc(int op, OpDesc* d) {
 #define FPDE_VJP_TX3 64
 #endif
 #ifndef FPDE_VJP_TY3
-#define FPDE_VJP_TY3 8
+#define FPDE_VJP_TY3 4
+#endif
+#ifndef FPDE_VJP_HEAT_TX
+#define FPDE_VJP_HEAT_TX 128
+#endif
+#ifndef FPDE_VJP_HEAT_TY
+#define FPDE_VJP_HEAT_TY 8
+#endif
+#ifndef FPDE_VJP_TARGET3
+#define FPDE_VJP_TARGET3 512
 #endif
 #ifndef FPDE_BLOCKS2
 #define FPDE_BLOCKS2 1024
@@ -286,11 +295,12 @@ int launch_vjp(const Req& r, bool acc, int target) {
 }
 
 int run_vjp(const Req& r, bool acc) {
-    constexpr int kTarget3 = 512;  // workgroups per launch (3-D)
+    constexpr int kTarget3 = FPDE_VJP_TARGET3;  // workgroups per launch (3-D)
     switch (r.op) {
     case FPDE_BURGERS_1DT: return launch_vjp<OpBurgers, kTX2, 1>(r, acc, kTargetBlocks2);
     case FPDE_HELMHOLTZ_2D: return launch_vjp<OpHelmholtz, kTX2, 1>(r, acc, kTargetBlocks2);
-    case FPDE_HEAT_3D_BE: return launch_vjp<OpHeat, FPDE_VJP_TX3, FPDE_VJP_TY3>(r, acc, kTarget3);
+    case FPDE_HEAT_3D_BE:
+        return launch_vjp<OpHeat, FPDE_VJP_HEAT_TX, FPDE_VJP_HEAT_TY>(r, acc, kTarget3);
     case FPDE_NS_2D_STEADY: return launch_vjp<OpNS2, kTX2, 1>(r, acc, kTargetBlocks2);
     case FPDE_NS_3D_BE: return launch_vjp<OpNS3, FPDE_VJP_TX3, FPDE_VJP_TY3>(r, acc, kTarget3);
     }

@@ -374,6 +374,19 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
             c[j] = bld(plane_rsrc_if(P.c[j], pz, pbytes, ok), cb);
     };
 
+    // The end planes of axis 0, which the march does not visit, hold no residual
+    // node: the first and the last chunk write their zeros.  (Whole rows are
+    // written, boundary columns included, so that no cache line of R is stored
+    // in part.)
+    if (STORE_R && !D.per) {
+        const uint32_t so = inarr ? cb : kDropOff;
+#pragma unroll
+        for (int b = 0; b < NR; ++b) {
+            if (z0 == 1) bst<kStream>(plane_rsrc(P.out[b], 0, pbytes), so, 0.f);
+            if (z1 == D.nz - 1) bst<kStream>(plane_rsrc(P.out[b], D.nz - 1, pbytes), so, 0.f);
+        }
+    }
+
     // plane z0 + j lives in slot (j + 1) & 3; prologue: planes z0-1, z0, z0+1
     load_plane(zw(z0 - 1), IC<0>{});
     load_plane(z0, IC<1>{});
@@ -420,10 +433,11 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
         // the step's arithmetic feeds nothing but acc: pin acc here, or the compiler
         // may sink that arithmetic past the barriers and keep several steps' loads live
         asm volatile("" : "+v"(acc));
-        if (STORE_R) {
-            const uint32_t so = interior ? cb : kDropOff;
+        if (STORE_R) {  // every node of the plane: R on the residual set, 0 off it
+            const uint32_t so = inarr ? cb : kDropOff;
 #pragma unroll
-            for (int b = 0; b < NR; ++b) bst<kStream>(plane_rsrc(P.out[b], z, pbytes), so, R[b]);
+            for (int b = 0; b < NR; ++b)
+                bst<kStream>(plane_rsrc(P.out[b], z, pbytes), so, interior ? R[b] : 0.f);
         }
         __syncthreads();  // (waits for the plane loads into LDS as well)
     };
@@ -716,8 +730,10 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
 // Explicit-sensitivity backward: grads (=, or += when ACC) J^T G for caller-given
 // residual sensitivities G_b = dL/dR_b (Sec. 2.2).  The gather is the one above
 // with G in place of the recomputed residuals, so no residual, const or ring is
-// needed: fields and sensitivities (radius 1) stream through one LDS ring with
-// the forward's slot layout, and the march covers every plane 0..nz-1, writing
+// needed: the fields the Jacobian depends on (OP::NFG of them: none for a linear
+// operator, no pressure for NS) and the sensitivities, each with a radius-1
+// halo, stream through one LDS ring with the forward's slot layout, and the
+// march covers every plane 0..nz-1, writing
 // every node once (boundary shell included: G is zero off the residual set,
 // which the loads enforce with out-of-range offsets, whatever the arrays hold
 // there).
@@ -725,7 +741,9 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
 template <class OP, int TX, int TY, bool ACC>
 __global__ __launch_bounds__(TX* TY, FPDE_VJP_MINW) void vjp_kernel(Ptrs P, Dims D, KCoef K) {
     constexpr int DIM = OP::DIM, NF = OP::NF, NR = OP::NR, NT = TX * TY;
-    constexpr int NA = NF + NR;  // arrays per slot: fields, then sensitivities
+    constexpr int NFG = OP::NFG;  // fields the Jacobian depends on (the others are not read)
+    static_assert(NT <= 1024, "a workgroup holds at most 1024 threads");
+    constexpr int NA = NFG + NR;  // arrays per slot: those fields, then the sensitivities
     constexpr int HY = (DIM == 3) ? 1 : 0;
     constexpr int LY = TY + 2 * HY, LX = TX, XG = LY * LX;
     static_assert(TX % 64 == 0, "a wavefront loads whole aligned row segments");
@@ -766,7 +784,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_VJP_MINW) void vjp_kernel(Ptrs P, Dims
         return px >= 0 && px < D.nx && py >= 0 && py < D.ny;
     };
     PS psf, psg;
-    psf.init(t, [&](int i, int& lin) { return node_at(i, lin, false); });
+    if constexpr (NFG > 0) psf.init(t, [&](int i, int& lin) { return node_at(i, lin, false); });
     psg.init(t, [&](int i, int& lin) { return node_at(i, lin, true); });
     // plane pz (wrapped or -1) of the fields and the sensitivities into a slot;
     // the sensitivities of a plane off the residual set read as 0
@@ -774,9 +792,9 @@ __global__ __launch_bounds__(TX* TY, FPDE_VJP_MINW) void vjp_kernel(Ptrs P, Dims
         float* dst[NA];
 #pragma unroll
         for (int a = 0; a < NA; ++a) dst[a] = &sF(slot)[a][0];
-        psf.template load<NF>(P.f, pz, D.nz, pbytes, dst);
+        if constexpr (NFG > 0) psf.template load<NFG>(P.f, pz, D.nz, pbytes, dst);
         const bool gok = D.per || (pz >= 1 && pz <= D.nz - 2);
-        psg.template load<NR>(P.s, gok ? pz : -1, D.nz, pbytes, dst + NF);
+        psg.template load<NR>(P.s, gok ? pz : -1, D.nz, pbytes, dst + NFG);
     };
     float gq[2][NF];  // accumulate mode: the stored gradients of the next plane
     auto load_old = [&](int pz, bool ok, float* o) __attribute__((always_inline)) {
@@ -817,11 +835,11 @@ __global__ __launch_bounds__(TX* TY, FPDE_VJP_MINW) void vjp_kernel(Ptrs P, Dims
         load_plane(more ? zw(z + 2) : -1, IC<SQ>{});
         __builtin_amdgcn_sched_barrier(0);  // (the plane loads first, as in the forward)
         load_old(z + 1, more, gq[NXT]);
-        Star fs[NF], gs[NR];
+        Star fs[NF] = {}, gs[NR];
 #pragma unroll
-        for (int f = 0; f < NF; ++f) star(IC<SM>{}, IC<SC>{}, IC<SP>{}, f, fs[f]);
+        for (int f = 0; f < NFG; ++f) star(IC<SM>{}, IC<SC>{}, IC<SP>{}, f, fs[f]);
 #pragma unroll
-        for (int b = 0; b < NR; ++b) star(IC<SM>{}, IC<SC>{}, IC<SP>{}, NF + b, gs[b]);
+        for (int b = 0; b < NR; ++b) star(IC<SM>{}, IC<SC>{}, IC<SP>{}, NFG + b, gs[b]);
         float g[NF];
         OP::gather(fs, gs, K, g);
         const uint32_t so = inarr ? cb : kDropOff;

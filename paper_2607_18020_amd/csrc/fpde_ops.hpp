@@ -19,6 +19,9 @@
 // neighbour terms added to them in the same order (gather = rest after self).
 // The backward evaluates the self part where it evaluates R(n), from the same
 // star, and carries the NG sums to the step that gathers at n.
+// NFG: the gather reads the stars of the first NFG fields only (the fields the
+// residual Jacobian depends on: none for a linear operator, the velocity and not
+// the pressure for NS, whose pressure enters linearly).
 // Star values are indexed by array axis: m[a] / p[a] hold q(n - e_a) / q(n + e_a).
 //
 // Evaluation order: second differences are formed as ((q+ - q) + (q- - q)) / h^2,
@@ -70,7 +73,7 @@ __device__ __forceinline__ float lap(const Star& s, const KCoef& K) {
 // Burgers on a space-time grid: axis 0 = t, axis 1 = x.
 //   R = u_t + u u_x - nu u_xx
 struct OpBurgers {
-    static constexpr int DIM = 2, NF = 1, NC = 0, NR = 1, NG = 0;
+    static constexpr int DIM = 2, NF = 1, NC = 0, NR = 1, NG = 0, NFG = 1;
 
     __device__ __forceinline__ static void residual(const Star* f, const float*, const KCoef& K, float* R) {
         const Star& u = f[0];
@@ -107,7 +110,7 @@ struct OpBurgers {
 // ---------------------------------------------------------------------------
 // Helmholtz: R = lap u + k^2 u - f   (self-adjoint: dL/du = k^2 R + lap R).
 struct OpHelmholtz {
-    static constexpr int DIM = 2, NF = 1, NC = 1, NR = 1, NG = 0;
+    static constexpr int DIM = 2, NF = 1, NC = 1, NR = 1, NG = 0, NFG = 0;
 
     __device__ __forceinline__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
         R[0] = lap<2>(f[0], K) + K.k2 * f[0].c - c[0];
@@ -132,7 +135,7 @@ struct OpHelmholtz {
 // ---------------------------------------------------------------------------
 // One implicit heat step: R = (u - u0)/dt - alpha lap u.
 struct OpHeat {
-    static constexpr int DIM = 3, NF = 1, NC = 1, NR = 1, NG = 0;
+    static constexpr int DIM = 3, NF = 1, NC = 1, NR = 1, NG = 0, NFG = 0;
 
     __device__ __forceinline__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
         R[0] = (f[0].c - c[0]) * K.inv_dt - K.alpha * lap<3>(f[0], K);
@@ -161,7 +164,7 @@ struct OpHeat {
 // UNSTEADY selects the backward-Euler time term (consts = previous velocities).
 template <int D, bool UNSTEADY>
 struct OpNS {
-    static constexpr int DIM = D, NF = D + 1, NC = UNSTEADY ? D : 0, NR = D + 1, NG = D;
+    static constexpr int DIM = D, NF = D + 1, NC = UNSTEADY ? D : 0, NR = D + 1, NG = D, NFG = D;
 
     __device__ __forceinline__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
         float cs[D];  // c_a / (2 h_a), shared by the D momentum equations
