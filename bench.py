@@ -12,6 +12,9 @@ Byte model (each input read once per pass, each output written once):
   them again and write one gradient per field, so one step moves
   (2 (NF + NC) + NF) * 4 bytes per grid node (72 B/node for the 3D NS case).
 
+--path fused times fpde_residual_value_and_grad, the same loss and gradient
+from one read of the inputs ((2 NF + NC) * 4 B/node: 44 for the 3D NS case).
+
 --path residual times the autograd form instead: fwd writing the residual
 arrays (every node; zero off the residual set), then fpde_residual_vjp on
 resident upstream sensitivities (read on the residual set), reading the fields
@@ -45,9 +48,10 @@ def parse():
                    help="planes of the oracle sample along axis 0 (0: sized automatically)")
     p.add_argument("--bc-mode", type=int, default=0, choices=(0, 1),
                    help="0: interior residual set (the benchmark); 1: periodic wrap on every axis")
-    p.add_argument("--path", default="loss", choices=("loss", "residual"),
+    p.add_argument("--path", default="loss", choices=("loss", "residual", "fused"),
                    help="loss: fwd+loss, bwd, bc (the benchmark); residual: fwd writing R, "
-                        "then the explicit-sensitivity backward")
+                        "then the explicit-sensitivity backward; fused: the one-pass value "
+                        "and gradient")
     p.add_argument("--sample-every", type=int, default=10,
                    help="per-kernel HIP events on every n-th timed step (the others carry none)")
     return p.parse_args()
@@ -63,6 +67,9 @@ def byte_model(wl, bc_mode=0, path="loss"):
     nf, nc, nr = len(wl.spec.fields), len(wl.spec.consts), len(wl.spec.residuals)
     N = wl.n_points
     M = N if bc_mode == 1 else wl.n_residual_points  # nodes the backward writes
+    if path == "fused":
+        vg = (nf + nc) * 4 * N + nf * 4 * N + 8
+        return {"step": vg, "value_and_grad": vg, "per_node": (2 * nf + nc) * 4}
     if path == "residual":
         nfg = JAC_FIELDS[wl.op]
         fwd = (nf + nc + nr) * 4 * N + 8  # + the residual arrays (every node is written)
@@ -207,6 +214,12 @@ def main():
             B.fpde_residual_vjp(op, fields, h, co, sens, grads=grads, bc_mode=bcm, stream=stream)
 
         kernels = (("fwd", fwd_r), ("vjp", vjp))
+    if args.path == "fused":
+        def value_and_grad():
+            B.fpde_residual_value_and_grad(op, fields, consts, h, co, dl, loss=loss, grads=grads,
+                                           bc_mode=bcm, stream=stream)
+
+        kernels = (("value_and_grad", value_and_grad),)  # (fill, march, bc: one call)
     names = [n for n, _ in kernels]
 
     def step():
@@ -276,8 +289,10 @@ def main():
                    "grid": list(wl.shape), "nodes": N,
                    "fields": list(wl.spec.fields), "consts": list(wl.spec.consts),
                    "seed": args.seed,
-                   "step": ("fwd+loss, bwd, bc on one stream" if args.path == "loss" else
-                            "fwd writing residuals, explicit-sensitivity vjp on one stream"),
+                   "step": {"loss": "fwd+loss, bwd, bc on one stream",
+                            "residual": "fwd writing residuals, explicit-sensitivity vjp",
+                            "fused": "one-pass loss + gradient (fill, bwd march with loss, bc)"
+                            }[args.path],
                    "path": args.path, "bc_mode": bcm},
         "hbm_gbps": round(gbps, 1),
         "hbm_frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4),

@@ -154,6 +154,25 @@ int fpde_bc_correct(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
                     const float* const* fields, const float* const* consts,
                     const double* dloss, float* const* grads, void* stream);
 
+/* Value and gradient in one pass: the loss L of fpde_residual_fwd and the
+ * gradient dloss * dL/dq of fpde_residual_bwd + fpde_bc_correct, from one read
+ * of the fields and consts.  The gradient of the mean-squared loss needs only
+ * the residuals (dL/dq = (2/M) J^T R), which the backward recomputes anyway, so
+ * the forward pass of Sec. 2.1 folds into it when the upstream derivative
+ * dloss is known before the call (1.0 for L itself): the backward kernel also
+ * sums the squares of the residuals it evaluates.
+ *   dloss  device pointer to one double, as in fpde_residual_bwd.
+ *   loss   device pointer to one double; OVERWRITTEN with L (not dloss * L);
+ *          must not overlap any other argument array (FPDE_ERR_ARG).
+ *   grads  host array of n_fields device pointers; OVERWRITTEN at every node.
+ * Other arguments and errors as fpde_residual_bwd.  Queues 3 kernels (2 on a
+ * periodic grid): a one-element fill zeroing *loss, the backward march (one
+ * float64 atomic add per workgroup onto *loss) and the boundary correction. */
+int fpde_residual_value_and_grad(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+                                 const float* const* fields, const float* const* consts,
+                                 const double* dloss, double* loss, float* const* grads,
+                                 void* stream);
+
 /* Explicit-sensitivity backward: the transpose-Jacobian action of the
  * residual operator on upstream residual sensitivities G_b = dObj/dR_b, the
  * form in which the backward of Sec. 2.2 receives them from autograd:

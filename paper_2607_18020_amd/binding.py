@@ -21,7 +21,8 @@ STATUS_NAMES = {0: "FPDE_OK", -1: "FPDE_ERR_ARG", -2: "FPDE_ERR_SHAPE", -3: "FPD
                 -4: "FPDE_ERR_COEFF", -5: "FPDE_ERR_ALIGN", -6: "FPDE_ERR_HIP",
                 -7: "FPDE_ERR_UNSUPPORTED"}
 EXPORTED = ("fpde_op_info", "fpde_residual_fwd", "fpde_residual_bwd", "fpde_bc_correct",
-            "fpde_residual_vjp", "fpde_status_string", "fpde_version")
+            "fpde_residual_vjp", "fpde_residual_value_and_grad", "fpde_status_string",
+            "fpde_version")
 
 
 class FpdeGrid(ctypes.Structure):
@@ -57,8 +58,9 @@ def _load():
         lib.fpde_residual_bwd.argtypes = [ctypes.c_int, gp, cp, pp, pp, vp, pp, vp]
         lib.fpde_bc_correct.argtypes = [ctypes.c_int, gp, cp, pp, pp, vp, pp, vp]
         lib.fpde_residual_vjp.argtypes = [ctypes.c_int, gp, cp, pp, pp, ctypes.c_int, pp, vp]
+        lib.fpde_residual_value_and_grad.argtypes = [ctypes.c_int, gp, cp, pp, pp, vp, vp, pp, vp]
         for name in ("fpde_op_info", "fpde_residual_fwd", "fpde_residual_bwd", "fpde_bc_correct",
-                     "fpde_residual_vjp"):
+                     "fpde_residual_vjp", "fpde_residual_value_and_grad"):
             getattr(lib, name).restype = ctypes.c_int
         lib.fpde_status_string.argtypes = [ctypes.c_int]
         lib.fpde_status_string.restype = ctypes.c_char_p
@@ -167,6 +169,24 @@ def fpde_bc_correct(op: int, fields, consts, h, coeffs, dloss, *, grads=None, bc
     """Queue the boundary-shell correction; returns the grads list."""
     return _grad_call(_load().fpde_bc_correct, "fpde_bc_correct", op, fields, consts, h,
                       coeffs, dloss, grads, bc_mode, stream)
+
+
+def fpde_residual_value_and_grad(op: int, fields, consts, h, coeffs, dloss=1.0, *,
+                                 loss: Optional[torch.Tensor] = None, grads=None,
+                                 bc_mode: int = 0, stream=None):
+    """Queue the one-pass loss + gradient (dloss known up front).  Returns
+    (loss, grads): the float64 loss L and dloss * dL/dq for every field."""
+    if loss is None:
+        loss = torch.empty((), dtype=torch.float64, device=fields[0].device)
+    if loss.dtype != torch.float64 or not loss.is_cuda or loss.numel() != 1:
+        raise ValueError("fpde_residual_value_and_grad: loss must be a one-element float64 CUDA tensor")
+
+    def fn(op_, g, c, fp, cp_, dl, gp, st):
+        return _load().fpde_residual_value_and_grad(op_, g, c, fp, cp_, dl, loss.data_ptr(), gp, st)
+
+    grads = _grad_call(fn, "fpde_residual_value_and_grad", op, fields, consts, h, coeffs, dloss,
+                       grads, bc_mode, stream)
+    return loss, grads
 
 
 def fpde_residual_vjp(op: int, fields, h, coeffs, sens, *, grads=None, accumulate: bool = False,

@@ -255,10 +255,18 @@ int launch_fwd(const Req& r, bool store, double* loss, int zc) {
 }
 
 template <class OP, int TX, int TY>
-int launch_bwd(const Req& r, const double* dloss, int zc) {
+int launch_bwd(const Req& r, const double* dloss, int zc, double* loss) {
     const Dims dm = tile_dims(r.dims, TX, TY, zc);
-    hipLaunchKernelGGL((bwd_kernel<OP, TX, TY, kBwdReverse>), dim3(dm.nblocks), dim3(TX * TY), 0,
-                       r.stream, r.P, dm, r.K, dloss, r.two_over_M);
+    if (loss) {  // value and gradient in one pass
+        hipLaunchKernelGGL(fill_f64_kernel, dim3(1), dim3(1), 0, r.stream, loss, 0.0);
+        hipLaunchKernelGGL((bwd_kernel<OP, TX, TY, kBwdReverse, true>), dim3(dm.nblocks),
+                           dim3(TX * TY), 0, r.stream, r.P, dm, r.K, dloss, r.two_over_M, r.inv_M,
+                           loss);
+    } else {
+        hipLaunchKernelGGL((bwd_kernel<OP, TX, TY, kBwdReverse, false>), dim3(dm.nblocks),
+                           dim3(TX * TY), 0, r.stream, r.P, dm, r.K, dloss, r.two_over_M, r.inv_M,
+                           nullptr);
+    }
     return hip_status();
 }
 
@@ -320,15 +328,16 @@ int run_fwd(const Req& r, bool store, double* loss) {
     return FPDE_ERR_ARG;
 }
 
-int run_bwd(const Req& r, const double* dloss) {
+// loss: nullptr for the gradient alone, else also the loss (fused value and grad)
+int run_bwd(const Req& r, const double* dloss, double* loss = nullptr) {
     switch (r.op) {
-    case FPDE_BURGERS_1DT: return launch_bwd<OpBurgers, kTX2, 1>(r, dloss, zc2(r));
-    case FPDE_HELMHOLTZ_2D: return launch_bwd<OpHelmholtz, kTX2, 1>(r, dloss, zc2(r));
+    case FPDE_BURGERS_1DT: return launch_bwd<OpBurgers, kTX2, 1>(r, dloss, zc2(r), loss);
+    case FPDE_HELMHOLTZ_2D: return launch_bwd<OpHelmholtz, kTX2, 1>(r, dloss, zc2(r), loss);
     case FPDE_HEAT_3D_BE:
-        return launch_bwd<OpHeat, GeoHeat::TXB, GeoHeat::TYb>(r, dloss, zc3<GeoHeat>(r));
-    case FPDE_NS_2D_STEADY: return launch_bwd<OpNS2, kTX2, 1>(r, dloss, zc2(r));
+        return launch_bwd<OpHeat, GeoHeat::TXB, GeoHeat::TYb>(r, dloss, zc3<GeoHeat>(r), loss);
+    case FPDE_NS_2D_STEADY: return launch_bwd<OpNS2, kTX2, 1>(r, dloss, zc2(r), loss);
     case FPDE_NS_3D_BE:
-        return launch_bwd<OpNS3, GeoNS3::TXB, GeoNS3::TYb>(r, dloss, zc3<GeoNS3>(r));
+        return launch_bwd<OpNS3, GeoNS3::TXB, GeoNS3::TYb>(r, dloss, zc3<GeoNS3>(r), loss);
     }
     return FPDE_ERR_ARG;
 }
@@ -410,6 +419,28 @@ extern "C" int fpde_bc_correct(int op, const fpde_grid* grid, const fpde_coeffs*
                                const double* dloss, float* const* grads, void* stream) {
     Req r;
     const int st = prepare_grad_call(op, grid, coeffs, fields, consts, dloss, grads, stream, &r);
+    if (st != FPDE_OK) return st;
+    return run_bc(r, dloss);
+}
+
+extern "C" int fpde_residual_value_and_grad(int op, const fpde_grid* grid,
+                                            const fpde_coeffs* coeffs, const float* const* fields,
+                                            const float* const* consts, const double* dloss,
+                                            double* loss, float* const* grads, void* stream) {
+    Req r;
+    int st = prepare_grad_call(op, grid, coeffs, fields, consts, dloss, grads, stream, &r);
+    if (st != FPDE_OK) return st;
+    if (!loss) return FPDE_ERR_ARG;
+    if ((uintptr_t)loss & 7u) return FPDE_ERR_ALIGN;
+    const size_t bytes = (size_t)r.N * sizeof(float);
+    if (overlaps(loss, sizeof(double), dloss, sizeof(double))) return FPDE_ERR_ARG;
+    for (int f = 0; f < r.d.nf; ++f)
+        if (overlaps(loss, sizeof(double), fields[f], bytes) ||
+            overlaps(loss, sizeof(double), grads[f], bytes))
+            return FPDE_ERR_ARG;
+    for (int j = 0; j < r.d.nc; ++j)
+        if (overlaps(loss, sizeof(double), consts[j], bytes)) return FPDE_ERR_ARG;
+    st = run_bwd(r, dloss, loss);
     if (st != FPDE_OK) return st;
     return run_bc(r, dloss);
 }

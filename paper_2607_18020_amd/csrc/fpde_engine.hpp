@@ -462,11 +462,18 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
 // plane z-1; R(z+1) is evaluated on the tile and its one-node ring into an LDS
 // tile; the gather at plane z reads the in-plane neighbours of R(z) from LDS and
 // R(z-1), R(z), R(z+1) of its own column from a register queue; one barrier.
+//
+// LOSS: the value and the gradient in one pass.  Every residual of the chunk's
+// planes is evaluated here anyway (own column, once per step), so the kernel
+// also adds their squares to the loss as the forward does (float32 sum over
+// the equations, float64 accumulation, one float64 atomic per workgroup onto
+// *loss, which the host zeroes first): the fields are read once for both.
 
-template <class OP, int TX, int TY, bool REV>
+template <class OP, int TX, int TY, bool REV, bool LOSS>
 __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims D, KCoef K,
                                                                     const double* dloss,
-                                                                    double two_over_M) {
+                                                                    double two_over_M,
+                                                                    double inv_M, double* loss) {
     constexpr int DIM = OP::DIM, NF = OP::NF, NC = OP::NC, NR = OP::NR, NT = TX * TY;
     constexpr int NC1 = NC > 0 ? NC : 1, NG = OP::NG, NG1 = NG > 0 ? NG : 1;
     constexpr int HY = (DIM == 3) ? 2 : 0;   // field-slot halo (y)
@@ -650,6 +657,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     // the gather at step w; step w+3's plane goes to the slot of step w-1; one
     // barrier.  Every LDS buffer a step writes was last read before the previous
     // step's barrier.
+    double acc = 0.0;  // LOSS: sum of squares of the own column's residuals
     auto step = [&](auto jc, int w) __attribute__((always_inline)) {
         constexpr int J = decltype(jc)::value;  // w & 3
         // field slots of steps w-1 (reused for w+3), w, w+1, w+2; R tiles of w, w+1
@@ -693,6 +701,14 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
                 rs[b].p[1] = c[RLX];
             }
         }
+        if (LOSS) {  // R of step w (zero off the residual set); a lane past the
+                     // grid's edge holds a wrapped duplicate on a periodic grid
+            float ss = 0.f;
+#pragma unroll
+            for (int b = 0; b < NR; ++b) ss = fmaf(rzc[b], rzc[b], ss);
+            acc += (double)(inarr ? ss : 0.f);
+            asm volatile("" : "+v"(acc));
+        }
         float g[NF];
         OP::gather_rest(fs, rs, sgc, K, g);
         {
@@ -724,6 +740,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     if (w < L) step(IC<0>{}, w);
     if (w + 1 < L) step(IC<1>{}, w + 1);
     if (w + 2 < L) step(IC<2>{}, w + 2);
+    if (LOSS) block_atomic_sum<NT>(acc * inv_M, loss);
 }
 
 // ---------------------------------------------------------------------------

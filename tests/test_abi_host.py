@@ -77,7 +77,7 @@ def _arr(vals):
 
 def _call(B, fn, op, shape, h=None, coef=W.Coeffs(nu=0.01, k=1.0, dt=0.1, alpha=0.1),
           fields=None, consts=None, outs=None, scalar=None, bc_mode=0, ndim=None, sens=None,
-          accumulate=0):
+          accumulate=0, loss=None):
     lib = B.lib()
     spec = W.OPS[op]
     h = h if h is not None else (0.1,) * len(shape)
@@ -99,6 +99,11 @@ def _call(B, fn, op, shape, h=None, coef=W.Coeffs(nu=0.01, k=1.0, dt=0.1, alpha=
         sens = sens if sens is not None else [_addr(40 + b) for b in range(nr)]
         return lib.fpde_residual_vjp(op, ctypes.byref(g), ctypes.byref(c), _arr(fields),
                                      _arr(sens), accumulate, _arr(outs), None)
+    if fn == "vg":
+        loss = _addr(31) if loss is None else loss
+        return lib.fpde_residual_value_and_grad(op, ctypes.byref(g), ctypes.byref(c), _arr(fields),
+                                                _arr(consts) if nc else None, scalar, loss,
+                                                _arr(outs), None)
     f = lib.fpde_residual_bwd if fn == "bwd" else lib.fpde_bc_correct
     return f(op, ctypes.byref(g), ctypes.byref(c), _arr(fields), _arr(consts) if nc else None,
              scalar, _arr(outs), None)
@@ -107,7 +112,7 @@ def _call(B, fn, op, shape, h=None, coef=W.Coeffs(nu=0.01, k=1.0, dt=0.1, alpha=
 ARG, SHAPE, SPACING, COEFF, ALIGN, UNSUP = -1, -2, -3, -4, -5, -7
 
 
-@pytest.mark.parametrize("fn", ["fwd", "bwd", "bc", "vjp"])
+@pytest.mark.parametrize("fn", ["fwd", "bwd", "bc", "vjp", "vg"])
 def test_validation_status_codes(B, fn):
     op3, op2 = W.NS_3D_BE, W.NS_2D_STEADY
     s3 = (8, 9, 10)
@@ -149,7 +154,14 @@ def test_output_checks(B):
     assert _call(B, "fwd", op, s3, outs=[_addr(20), _addr(21), _addr(1, 4 * 10), _addr(23)]) == ARG
     assert _call(B, "fwd", op, s3, outs=[_addr(20), 0, _addr(22), _addr(23)]) == ARG
     assert _call(B, "fwd", op, s3, outs=[_addr(20), _addr(20, nbytes - 4), _addr(22), _addr(23)]) == ARG
-    for fn in ("bwd", "bc"):
+    # value_and_grad: null / misaligned loss, loss on dloss, inside a field, const or grad
+    assert _call(B, "vg", op, s3, loss=0) == ARG
+    assert _call(B, "vg", op, s3, loss=_addr(31, 4)) == ALIGN
+    assert _call(B, "vg", op, s3, loss=_addr(30)) == ARG
+    assert _call(B, "vg", op, s3, loss=_addr(2, 64)) == ARG
+    assert _call(B, "vg", op, s3, loss=_addr(11, 8)) == ARG
+    assert _call(B, "vg", op, s3, loss=_addr(22, nbytes - 8)) == ARG
+    for fn in ("bwd", "bc", "vg"):
         # null / misaligned dloss, grads aliasing fields, consts, each other or dloss
         assert _call(B, fn, op, s3, scalar=0) == ARG
         assert _call(B, fn, op, s3, scalar=_addr(30, 4)) == ALIGN
