@@ -104,28 +104,33 @@ def copy_gbps(torch, nbytes=1 << 30, reps=20):
     return 2 * nbytes / s / 1e9
 
 
+# the kernels one timed call queues, where it queues several
+TRAFFIC_KERNELS = {"value_and_grad": ("fill_f64", "bwd", "bc")}
 OP_KERNEL_TAG = {1: "OpBurgers", 2: "OpHelmholtz", 3: "OpHeat", 4: "OpNS<2, false>",
                  5: "OpNS<3, true>"}
 
 
-def measured_traffic(cfg, op, kernel, path="loss"):
-    """HBM bytes per launch of `kernel` ("fwd"/"bwd") from the committed rocprofv3
-    counter summary, if it was taken on this workload with the current kernel
-    sources; else None."""
+def measured_traffic(cfg, op, kernels, path="loss"):
+    """HBM bytes per launch from the committed rocprofv3 counter summary of this
+    bench path, summed over `kernels` (name stems such as "bwd", "fill_f64"), if
+    it was taken on this workload with the current kernel sources; else None."""
     from paper_2607_18020_amd import profiling  # noqa: PLC0415
-    path = os.path.join(ROOT, "profiles", "traffic.json")
-    if not os.path.exists(path):
+    fn = os.path.join(ROOT, "profiles", f"traffic_{path}.json")
+    if not os.path.exists(fn):
         return None
-    rec = json.load(open(path))
+    rec = json.load(open(fn))
     if rec.get("source_hash") != profiling.source_hash() or not rec.get("workload", "").startswith(cfg):
         return None
-    if rec.get("path", "loss") != path:  # (the residual path runs other kernel variants)
+    if rec.get("path") != path:
         return None
-    prefix = f"{kernel}_kernel<{OP_KERNEL_TAG[op]}"
-    for name, v in rec.get("kernels", {}).items():
-        if name.startswith(prefix):
-            return round(v["fetch_bytes"] + v["write_bytes"])
-    return None
+    total = 0.0
+    for stem in kernels:
+        prefix = stem if stem.startswith("fill") else f"{stem}_kernel<{OP_KERNEL_TAG[op]}"
+        hits = [v for name, v in rec.get("kernels", {}).items() if name.startswith(prefix)]
+        if len(hits) != 1:
+            return None
+        total += hits[0]["fetch_bytes"] + hits[0]["write_bytes"]
+    return round(total)
 
 
 def cpu_baseline(W, wl_full, cfg, seed, planes, bc_mode=0, path="loss"):
@@ -267,7 +272,7 @@ def main():
     achieved = bm[dom] / (per[dom] * 1e-6) / 1e9
     roofline = {"bound": "hbm", "kernel": f"{dom} ({cfg})", "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                "traffic": measured_traffic(cfg, wl.op, dom, args.path),
+                "traffic": measured_traffic(cfg, wl.op, TRAFFIC_KERNELS.get(dom, (dom,)), args.path),
                 "algorithmic_bytes_per_launch": bm[dom], "avg_launch_us": round(per[dom], 2)}
     cpu = None
     if not args.no_cpu_baseline:

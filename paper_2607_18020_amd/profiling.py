@@ -3,12 +3,15 @@
 Usage (after the rocprofv3 runs listed in ``--help`` have produced their CSVs):
 
     python -m paper_2607_18020_amd.profiling --stats DIR --fetch DIR --write DIR \
-        --bench-json FILE --out profiles/
+        --bench-json FILE --commands FILE --path PATH --name STEM --out profiles/
+
+(PATH: the ``bench.py --path`` the runs were taken with; STEM: the summary's
+file name.)
 
 Traffic calibration: FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are scaled by
 what the same counters read for the benchmark's stream kernel (y = 1 * x over
 1 GiB: 1 GiB read, 1 GiB written), so the figures are bytes, whatever the
-counters' own unit and coverage.  ``traffic.json`` records a hash of the kernel
+counters' own unit and coverage.  ``traffic_<PATH>.json`` records a hash of the kernel
 sources (comments and whitespace ignored); ``bench.py`` reports the traffic
 only while that hash still matches.
 """
@@ -84,7 +87,7 @@ def calibrated(pmc_dir: str, counter: str) -> Dict[str, dict]:
     factor = STREAM_BYTES / ref_kib  # bytes per counted KiB
     out = {"_calibration": {"stream_kib": ref_kib, "bytes_per_kib": factor}}
     for k, vs in vals.items():
-        if k.startswith(("fwd_kernel", "bwd_kernel", "bc_kernel")):
+        if k.startswith(("fwd_kernel", "bwd_kernel", "bc_kernel", "vjp_kernel", "fill_f64")):
             avg = sum(vs) / len(vs)
             out[k] = {"dispatches": len(vs), "avg_kib": avg, "bytes": avg * factor}
     return out
@@ -99,6 +102,9 @@ def main():
     ap.add_argument("--commands", required=True, help="text file with the three rocprofv3 commands")
     ap.add_argument("--out", required=True)
     ap.add_argument("--workload", default="ns_3d_tgv 256^3")
+    ap.add_argument("--path", default="loss", choices=("loss", "residual", "fused"),
+                    help="the bench.py --path the runs were taken with")
+    ap.add_argument("--name", default="ns3d_256_fwd_bwd_bc", help="summary file stem")
     a = ap.parse_args()
 
     stats = kernel_stats(a.stats)
@@ -109,8 +115,9 @@ def main():
     sha = source_hash()
     os.makedirs(a.out, exist_ok=True)
 
-    kern = sorted(k for k in stats if k.startswith(("fwd_kernel", "bwd_kernel", "bc_kernel", "fill")))
-    lines = [f"# Kernel timings and HBM traffic, {a.workload}", "",
+    kern = sorted(k for k in stats
+                  if k.startswith(("fwd_kernel", "bwd_kernel", "bc_kernel", "vjp_kernel", "fill")))
+    lines = [f"# Kernel timings and HBM traffic, {a.workload}, bench.py --path {a.path}", "",
              "Commands (run from the repository root on one MI355X):", "", "```", cmds, "```", "",
              f"Kernel sources hash (comments and whitespace ignored): `{sha}`.", "",
              "## rocprofv3 --kernel-trace --stats (same process as the bench line below)", "",
@@ -136,10 +143,10 @@ def main():
         lines.append(f"| `{k}` | {fetch.get(k, {}).get('avg_kib', 0):.0f} | {fb / 1e6:.1f} | "
                      f"{write.get(k, {}).get('avg_kib', 0):.0f} | {wb / 1e6:.1f} |")
         traffic[k] = {"fetch_bytes": fb, "write_bytes": wb}
-    with open(os.path.join(a.out, "ns3d_256_fwd_bwd_bc.md"), "w") as f:
+    with open(os.path.join(a.out, a.name + ".md"), "w") as f:
         f.write("\n".join(lines) + "\n")
-    with open(os.path.join(a.out, "traffic.json"), "w") as f:
-        json.dump({"source_hash": sha, "workload": a.workload, "kernels": traffic,
+    with open(os.path.join(a.out, f"traffic_{a.path}.json"), "w") as f:
+        json.dump({"source_hash": sha, "workload": a.workload, "path": a.path, "kernels": traffic,
                    "calibration": {"fetch": fetch["_calibration"], "write": write["_calibration"]}},
                   f, indent=1)
     print("\n".join(lines))
