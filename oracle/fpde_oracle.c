@@ -45,6 +45,10 @@ static int op_shape(int op, int* ndim, int* nf, int* nc, int* nr) {
     case 3: *ndim = 3; *nf = 1; *nc = 1; *nr = 1; return 0; /* heat 3D: u ; u0          */
     case 4: *ndim = 2; *nf = 3; *nc = 0; *nr = 3; return 0; /* NS 2D: u,v,p             */
     case 5: *ndim = 3; *nf = 4; *nc = 3; *nr = 4; return 0; /* NS 3D: u,v,w,p ; prev    */
+    case 6: *ndim = 3; *nf = 4; *nc = 0; *nr = 4; return 0; /* steady NS 3D: u,v,w,p    */
+    case 7: *ndim = 2; *nf = 1; *nc = 1; *nr = 1; return 0; /* Poisson 2D: u ; f        */
+    case 8: *ndim = 3; *nf = 1; *nc = 1; *nr = 1; return 0; /* Poisson 3D: u ; f        */
+    case 9: *ndim = 3; *nf = 3; *nc = 0; *nr = 3; return 0; /* NS 2D+t: u,v,p (t,x,y)   */
     default: return -1;
     }
 }
@@ -172,7 +176,8 @@ static void res_heat(const grid_t* g, const coef_t* c, const double* const* F,
  * pressure after the velocities (Sec. 2.1 for the steady 2D case):
  *   R_b = [(c_b - c_b^prev)/dt] + sum_a c_a D1_a c_b + D1_b p - nu sum_a D2_a c_b
  *   R_div = sum_a D1_a c_a
- * The bracketed time term is present for the backward-Euler step only (op 5). */
+ * The bracketed time term is present for the backward-Euler step only (op 5);
+ * ops 4 (2D) and 6 (3D) are steady. */
 static void res_ns(const grid_t* g, const coef_t* c, const double* const* F,
                    const double* const* C, long m, const long* iv, double* R, int unsteady) {
     int d = g->ndim, a, b;
@@ -190,6 +195,40 @@ static void res_ns(const grid_t* g, const coef_t* c, const double* const* F,
     for (a = 0; a < d; a++) R[d] += D1(g, F[a], iv, m, a);
 }
 
+/* Poisson: R = lap u - f. */
+static void res_poisson(const grid_t* g, const coef_t* c, const double* const* F,
+                        const double* const* C, long m, const long* iv, double* R) {
+    const double* u = F[0];
+    double lap = 0.0;
+    int a;
+    (void)c;
+    for (a = 0; a < g->ndim; a++) lap += D2(g, u, iv, m, a);
+    R[0] = lap - C[0][m];
+}
+
+/* Unsteady incompressible NS on a space-time grid: array axis 0 is t, velocity
+ * component b lives on array axis b+1 (u<->1, v<->2), pressure after the
+ * velocities; every derivative, the time derivative included, is a centred
+ * difference (the time step is the grid spacing h_0):
+ *   R_b = D1_0 c_b + sum_a c_a D1_{a+1} c_b + D1_{b+1} p - nu sum_a D2_{a+1} c_b
+ *   R_div = sum_a D1_{a+1} c_a              (a, b over the spatial components) */
+static void res_ns_t(const grid_t* g, const coef_t* c, const double* const* F,
+                     const double* const* C, long m, const long* iv, double* R) {
+    int d = g->ndim - 1, a, b;
+    const double* p = F[d];
+    (void)C;
+    for (b = 0; b < d; b++) {
+        const double* cb = F[b];
+        double r = D1(g, cb, iv, m, 0);
+        for (a = 0; a < d; a++) r += F[a][m] * D1(g, cb, iv, m, a + 1);
+        r += D1(g, p, iv, m, b + 1);
+        for (a = 0; a < d; a++) r -= c->nu * D2(g, cb, iv, m, a + 1);
+        R[b] = r;
+    }
+    R[d] = 0.0;
+    for (a = 0; a < d; a++) R[d] += D1(g, F[a], iv, m, a + 1);
+}
+
 static void residual_at(int op, const grid_t* g, const coef_t* c, const double* const* F,
                         const double* const* C, long m, const long* iv, double* R) {
     switch (op) {
@@ -198,6 +237,9 @@ static void residual_at(int op, const grid_t* g, const coef_t* c, const double* 
     case 3: res_heat(g, c, F, C, m, iv, R); break;
     case 4: res_ns(g, c, F, C, m, iv, R, 0); break;
     case 5: res_ns(g, c, F, C, m, iv, R, 1); break;
+    case 6: res_ns(g, c, F, C, m, iv, R, 0); break;
+    case 7: case 8: res_poisson(g, c, F, C, m, iv, R); break;
+    case 9: res_ns_t(g, c, F, C, m, iv, R); break;
     }
 }
 
@@ -299,6 +341,60 @@ static void jt_ns(const grid_t* g, const coef_t* c, const double* const* F,
     }
 }
 
+static void jt_poisson(const grid_t* g, const coef_t* c, const double* const* F,
+                       const double* const* C, long m, const long* iv, const double* G,
+                       double* const* gr) {
+    double* du = gr[0];
+    double gm = G[0];
+    int a;
+    (void)c; (void)F; (void)C;
+    /* D2_a u: d/du(m) = -2/h_a^2; d/du(m +- e_a) = 1/h_a^2  (f is a constant input) */
+    for (a = 0; a < g->ndim; a++) {
+        double ih2 = 1.0 / (g->h[a] * g->h[a]);
+        du[m] -= gm * 2.0 * ih2;
+        du[nb(g, iv, m, a, +1)] += gm * ih2;
+        du[nb(g, iv, m, a, -1)] += gm * ih2;
+    }
+}
+
+static void jt_ns_t(const grid_t* g, const coef_t* c, const double* const* F,
+                    const double* const* C, long m, const long* iv, const double* G,
+                    double* const* gr) {
+    int d = g->ndim - 1, a, b;
+    double* dp = gr[d];
+    (void)C;
+    for (b = 0; b < d; b++) {
+        const double* cb = F[b];
+        double gm = G[b];
+        /* D1_0 c_b: d/dc_b(m +- e_0) = +- 1/(2 h_0) */
+        gr[b][nb(g, iv, m, 0, +1)] += gm / (2.0 * g->h[0]);
+        gr[b][nb(g, iv, m, 0, -1)] -= gm / (2.0 * g->h[0]);
+        for (a = 0; a < d; a++) {
+            double i2h = 1.0 / (2.0 * g->h[a + 1]);
+            /* c_a(m) * D1_{a+1} c_b: d/dc_a(m) = D1_{a+1} c_b(m);
+             *                        d/dc_b(m +- e_{a+1}) = +- c_a(m) / (2 h_{a+1}) */
+            gr[a][m] += gm * D1(g, cb, iv, m, a + 1);
+            gr[b][nb(g, iv, m, a + 1, +1)] += gm * F[a][m] * i2h;
+            gr[b][nb(g, iv, m, a + 1, -1)] -= gm * F[a][m] * i2h;
+        }
+        /* D1_{b+1} p: d/dp(m +- e_{b+1}) = +- 1/(2 h_{b+1}) */
+        dp[nb(g, iv, m, b + 1, +1)] += gm / (2.0 * g->h[b + 1]);
+        dp[nb(g, iv, m, b + 1, -1)] -= gm / (2.0 * g->h[b + 1]);
+        /* -nu D2_{a+1} c_b: d/dc_b(m) = 2 nu/h^2; d/dc_b(m +- e_{a+1}) = -nu/h^2 */
+        for (a = 0; a < d; a++) {
+            double ih2 = 1.0 / (g->h[a + 1] * g->h[a + 1]);
+            gr[b][m] += gm * 2.0 * c->nu * ih2;
+            gr[b][nb(g, iv, m, a + 1, +1)] -= gm * c->nu * ih2;
+            gr[b][nb(g, iv, m, a + 1, -1)] -= gm * c->nu * ih2;
+        }
+    }
+    /* R_div = sum_a D1_{a+1} c_a: d/dc_a(m +- e_{a+1}) = +- 1/(2 h_{a+1}) */
+    for (a = 0; a < d; a++) {
+        gr[a][nb(g, iv, m, a + 1, +1)] += G[d] / (2.0 * g->h[a + 1]);
+        gr[a][nb(g, iv, m, a + 1, -1)] -= G[d] / (2.0 * g->h[a + 1]);
+    }
+}
+
 static void jt_at(int op, const grid_t* g, const coef_t* c, const double* const* F,
                   const double* const* C, long m, const long* iv, const double* G,
                   double* const* gr) {
@@ -308,6 +404,9 @@ static void jt_at(int op, const grid_t* g, const coef_t* c, const double* const*
     case 3: jt_heat(g, c, F, C, m, iv, G, gr); break;
     case 4: jt_ns(g, c, F, C, m, iv, G, gr, 0); break;
     case 5: jt_ns(g, c, F, C, m, iv, G, gr, 1); break;
+    case 6: jt_ns(g, c, F, C, m, iv, G, gr, 0); break;
+    case 7: case 8: jt_poisson(g, c, F, C, m, iv, G, gr); break;
+    case 9: jt_ns_t(g, c, F, C, m, iv, G, gr); break;
     }
 }
 

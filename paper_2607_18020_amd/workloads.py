@@ -1,4 +1,4 @@
-"""Seeded synthetic workloads for the five FD residual operators.
+"""Seeded synthetic workloads for the FD residual operators.
 
 This module holds the operator registry (op ids, field/const names, grid
 spacings, PDE coefficients) and the seeded input generators.  It contains none
@@ -27,6 +27,10 @@ HELMHOLTZ_2D = 2
 HEAT_3D_BE = 3
 NS_2D_STEADY = 4
 NS_3D_BE = 5
+NS_3D_STEADY = 6
+POISSON_2D = 7
+POISSON_3D = 8
+NS_2DT = 9
 
 OP_NAMES = {
     BURGERS_1DT: "burgers_1dt",
@@ -34,6 +38,10 @@ OP_NAMES = {
     HEAT_3D_BE: "heat_3d_be",
     NS_2D_STEADY: "ns_2d_steady",
     NS_3D_BE: "ns_3d_be",
+    NS_3D_STEADY: "ns_3d_steady",
+    POISSON_2D: "poisson_2d",
+    POISSON_3D: "poisson_3d",
+    NS_2DT: "ns_2dt",
 }
 
 
@@ -55,7 +63,16 @@ OPS: Dict[int, OpSpec] = {
     NS_2D_STEADY: OpSpec(NS_2D_STEADY, 2, ("u", "v", "p"), (), ("R_u", "R_v", "R_c")),
     NS_3D_BE: OpSpec(NS_3D_BE, 3, ("u", "v", "w", "p"), ("u_prev", "v_prev", "w_prev"),
                      ("R_u", "R_v", "R_w", "R_c")),
+    NS_3D_STEADY: OpSpec(NS_3D_STEADY, 3, ("u", "v", "w", "p"), (), ("R_u", "R_v", "R_w", "R_c")),
+    POISSON_2D: OpSpec(POISSON_2D, 2, ("u",), ("f",), ("R",)),
+    POISSON_3D: OpSpec(POISSON_3D, 3, ("u",), ("f",), ("R",)),
+    # space-time grid (t, x, y): velocity component b on array axis b + 1
+    NS_2DT: OpSpec(NS_2DT, 3, ("u", "v", "p"), (), ("R_u", "R_v", "R_c")),
 }
+
+# the operators of the five benchmark workloads; the others are the adjacent
+# operators that share their kernels
+CORE_OPS = (BURGERS_1DT, HELMHOLTZ_2D, HEAT_3D_BE, NS_2D_STEADY, NS_3D_BE)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -123,24 +140,40 @@ CONFIGS: Dict[str, Config] = {
     "ns_3d_tgv": Config("ns_3d_tgv", NS_3D_BE, (256, 256, 256),
                         Coeffs(nu=0.01, dt=1e-2),
                         "3D Taylor-Green NS (u,v,w,p), one backward-Euler step, 256^3 on [0,2pi)^3, nu=0.01, dt=1e-2"),
+    # adjacent operators (same kernels, other point functions)
+    "ns_3d_steady": Config("ns_3d_steady", NS_3D_STEADY, (256, 256, 256), Coeffs(nu=0.01),
+                           "3D steady incompressible NS (u,v,w,p), 256^3 on [0,1]^3, nu=0.01"),
+    "poisson_2d": Config("poisson_2d", POISSON_2D, (1024, 1024), Coeffs(),
+                         "2D Poisson 1024^2 on [0,1]^2, 5-point Laplacian"),
+    "poisson_3d": Config("poisson_3d", POISSON_3D, (256, 256, 256), Coeffs(),
+                         "3D Poisson 256^3 on [0,1]^3, 7-point Laplacian"),
+    "ns_2dt": Config("ns_2dt", NS_2DT, (64, 512, 512), Coeffs(nu=0.01),
+                     "2D+t unsteady incompressible NS (u,v,p) on a space-time grid 64 x 512^2, "
+                     "t in [0,1], (x,y) on [0,2pi)^2, nu=0.01, central time differences"),
 }
 
 CONFIG_ORDER = ("burgers_1dt", "helmholtz_2d", "heat_3d", "ns_2d", "ns_3d_tgv")
+ADJACENT_CONFIGS = ("ns_3d_steady", "poisson_2d", "poisson_3d", "ns_2dt")
 
 
 def spacing(cfg_name: str, shape: Sequence[int]) -> Tuple[float, ...]:
     """Grid spacing per array axis for a config at a given shape.
 
     Burgers: axis 0 is t on [0,1], axis 1 is x on [-1,1], endpoint-inclusive.
-    Helmholtz, heat, 2D NS: endpoint-inclusive nodes on [0,1] per axis.
+    Helmholtz, heat, 2D NS, 3D steady NS, Poisson: endpoint-inclusive nodes on
+    [0,1] per axis.
     3D TGV: periodic sampling x_i = 2*pi*i/n on [0,2pi).
+    2D+t NS: axis 0 is t on [0,1] endpoint-inclusive; x, y periodic on [0,2pi).
     """
     if cfg_name == "burgers_1dt":
         return (1.0 / (shape[0] - 1), 2.0 / (shape[1] - 1))
-    if cfg_name in ("helmholtz_2d", "heat_3d", "ns_2d"):
+    if cfg_name in ("helmholtz_2d", "heat_3d", "ns_2d", "ns_3d_steady", "poisson_2d",
+                    "poisson_3d"):
         return tuple(1.0 / (s - 1) for s in shape)
     if cfg_name == "ns_3d_tgv":
         return tuple(2.0 * math.pi / s for s in shape)
+    if cfg_name == "ns_2dt":
+        return (1.0 / (shape[0] - 1),) + tuple(2.0 * math.pi / s for s in shape[1:])
     raise KeyError(cfg_name)
 
 
@@ -236,6 +269,46 @@ def make(cfg_name: str, seed: int = 42, shape: Optional[Sequence[int]] = None) -
         fields = [_f32(u_ic + noise()), _f32(v_ic + noise()), _f32(w_ic + noise()),
                   _f32(p_ic + noise())]
         consts = [_f32(u_ic), _f32(v_ic), _f32(w_ic)]
+    elif cfg_name == "ns_3d_steady":
+        # velocity = curl of a vector potential A (three sums of 6 modes of
+        # amplitude a / (2 pi |kappa|)), so it is divergence-free analytically;
+        # p = 8 modes; + N(0, 0.01^2) on every field
+        def modes(n):
+            out = []
+            for _ in range(n):
+                kap = rng.integers(1, 5, size=3)
+                out.append((kap, rng.standard_normal() / float(np.linalg.norm(kap)),
+                            rng.uniform(0.0, 2.0 * math.pi)))
+            return out
+        dA = [[np.zeros(shape) for _ in range(3)] for _ in range(3)]  # dA[i][j] = dA_i/dx_j
+        for i in range(3):
+            for kap, amp, phi in modes(6):
+                c = np.cos(2.0 * math.pi * sum(float(kap[j]) * X[j] for j in range(3)) + phi)
+                for j in range(3):
+                    dA[i][j] = dA[i][j] + amp * float(kap[j]) * c
+        u = dA[2][1] - dA[1][2]
+        v = dA[0][2] - dA[2][0]
+        w = dA[1][0] - dA[0][1]
+        p = np.zeros(shape)
+        for kap, amp, phi in modes(8):
+            p = p + amp * np.sin(2.0 * math.pi * sum(float(kap[j]) * X[j] for j in range(3)) + phi)
+        fields = [_f32(np.broadcast_to(q, shape) + noise()) for q in (u, v, w, p)]
+        consts = []
+    elif cfg_name in ("poisson_2d", "poisson_3d"):
+        nm, km = (16, 8) if len(shape) == 2 else (8, 4)
+        u = _fourier_sum(rng, X, nm, km, trig_choice=True) + noise()
+        f = _fourier_sum(rng, X, nm, km, trig_choice=True) + noise()
+        fields, consts = [_f32(u)], [_f32(f)]
+    elif cfg_name == "ns_2dt":
+        # decaying 2D Taylor-Green vortex (an exact NS solution) + N(0, 0.01^2)
+        t, x, y = X
+        nu = cfg.coeffs.nu
+        e1, e2 = np.exp(-2.0 * nu * t), np.exp(-4.0 * nu * t)
+        u = np.sin(x) * np.cos(y) * e1
+        v = -np.cos(x) * np.sin(y) * e1
+        p = 0.25 * (np.cos(2.0 * x) + np.cos(2.0 * y)) * e2
+        fields = [_f32(np.broadcast_to(q, shape) + noise()) for q in (u, v, p)]
+        consts = []
     else:  # pragma: no cover
         raise KeyError(cfg_name)
 
@@ -257,7 +330,8 @@ def normal_fields(op: int, shape: Sequence[int], seed: int,
     if coeffs is None:
         coeffs = {BURGERS_1DT: Coeffs(nu=0.01 / math.pi), HELMHOLTZ_2D: Coeffs(k=4 * math.pi),
                   HEAT_3D_BE: Coeffs(dt=1e-3, alpha=0.1), NS_2D_STEADY: Coeffs(nu=0.01),
-                  NS_3D_BE: Coeffs(nu=0.01, dt=1e-2)}[op]
+                  NS_3D_BE: Coeffs(nu=0.01, dt=1e-2), NS_3D_STEADY: Coeffs(nu=0.01),
+                  POISSON_2D: Coeffs(), POISSON_3D: Coeffs(), NS_2DT: Coeffs(nu=0.01)}[op]
     return Workload(f"normal_{OP_NAMES[op]}", op, shape, tuple(float(x) for x in h), coeffs,
                     fields, consts)
 

@@ -37,7 +37,19 @@ def residuals(op, h, co, F, C):
     if op == 3:  # implicit heat step
         u, u0 = F[0], C[0]
         return [(c0(u) - c0(u0)) / co.dt - co.alpha * sum(_d2(u, a, h) for a in range(d))]
-    if op in (4, 5):  # incompressible NS, velocity component b on axis b
+    if op in (7, 8):  # Poisson
+        u, f = F[0], C[0]
+        return [sum(_d2(u, a, h) for a in range(d)) - c0(f)]
+    if op == 9:  # NS on a space-time grid: axis 0 = t, velocity component b on axis b + 1
+        vel, p = F[:2], F[2]
+        out = []
+        for b in range(2):
+            r = _d1(vel[b], 0, h) + sum(c0(vel[a]) * _d1(vel[b], a + 1, h) for a in range(2)) \
+                + _d1(p, b + 1, h) - co.nu * sum(_d2(vel[b], a + 1, h) for a in range(2))
+            out.append(r)
+        out.append(sum(_d1(vel[a], a + 1, h) for a in range(2)))
+        return out
+    if op in (4, 5, 6):  # incompressible NS, velocity component b on axis b
         vel, p = F[:d], F[d]
         out = []
         for b in range(d):

@@ -24,7 +24,7 @@ from paper_2607_18020_amd import workloads as W
 from tests import golden
 from tests import _torch_fd
 
-OPS = [W.BURGERS_1DT, W.HELMHOLTZ_2D, W.HEAT_3D_BE, W.NS_2D_STEADY, W.NS_3D_BE]
+OPS = sorted(W.OPS)
 
 SHAPES = {2: (9, 12), 3: (8, 11, 10)}
 H = {2: (0.11, 0.07), 3: (0.13, 0.09, 0.06)}
@@ -34,6 +34,10 @@ COEF = {
     W.HEAT_3D_BE: W.Coeffs(dt=0.02, alpha=0.1),
     W.NS_2D_STEADY: W.Coeffs(nu=0.05),
     W.NS_3D_BE: W.Coeffs(nu=0.04, dt=0.05),
+    W.NS_3D_STEADY: W.Coeffs(nu=0.04),
+    W.POISSON_2D: W.Coeffs(),
+    W.POISSON_3D: W.Coeffs(),
+    W.NS_2DT: W.Coeffs(nu=0.05),
 }
 
 
@@ -92,6 +96,15 @@ def _symbol_residuals(op, co, modes, consts):
     if op == W.HEAT_3D_BE:
         (u, d1, d2), = modes
         return [(u - consts[0]) / co.dt - co.alpha * sum(d2)]
+    if op in (W.POISSON_2D, W.POISSON_3D):
+        (u, d1, d2), = modes
+        return [sum(d2) - consts[0]]
+    if op == W.NS_2DT:  # axis 0 = t; velocity component b on axis b + 1
+        vel, p = modes[:2], modes[2]
+        out = [vel[b][1][0] + sum(vel[a][0] * vel[b][1][a + 1] for a in range(2)) + p[1][b + 1]
+               - co.nu * (vel[b][2][1] + vel[b][2][2]) for b in range(2)]
+        out.append(sum(vel[a][1][a + 1] for a in range(2)))
+        return out
     d = len(modes) - 1
     vel, p = modes[:d], modes[d]
     out = []
@@ -161,8 +174,10 @@ def _mms_problem(op):
     F, C = pool[:nf], pool[nf:nf + nc]
     if op == W.HELMHOLTZ_2D:
         C = [pool[1]]
-    if op == W.HEAT_3D_BE:
+    if op in (W.HEAT_3D_BE, W.POISSON_3D):
         C = [pool[4]]
+    if op == W.POISSON_2D:
+        C = [pool[1]]
     D = sp.diff
     if op == W.BURGERS_1DT:
         u, = F
@@ -173,6 +188,15 @@ def _mms_problem(op):
     elif op == W.HEAT_3D_BE:
         u, = F
         R = [(u - C[0]) / co.dt - co.alpha * sum(D(u, xi, 2) for xi in xs)]
+    elif op in (W.POISSON_2D, W.POISSON_3D):
+        u, = F
+        R = [sum(D(u, xi, 2) for xi in xs) - C[0]]
+    elif op == W.NS_2DT:  # xs = (t, x, y)
+        vel, p = F[:2], F[2]
+        R = [D(vel[b], xs[0]) + sum(vel[a] * D(vel[b], xs[a + 1]) for a in range(2))
+             + D(p, xs[b + 1]) - co.nu * sum(D(vel[b], xi, 2) for xi in xs[1:])
+             for b in range(2)]
+        R.append(sum(D(vel[a], xs[a + 1]) for a in range(2)))
     else:
         vel, p = F[:ndim], F[ndim]
         R = []
@@ -301,7 +325,7 @@ def _kron_laplacian(shape, h):
     return sum(mats).tocsr()
 
 
-@pytest.mark.parametrize("op", [W.HELMHOLTZ_2D, W.HEAT_3D_BE])
+@pytest.mark.parametrize("op", [W.HELMHOLTZ_2D, W.HEAT_3D_BE, W.POISSON_2D, W.POISSON_3D])
 def test_linear_ops_match_kronecker_matrix(oracle_mod, op):
     import scipy.sparse as sps  # noqa: PLC0415
     ndim = W.OPS[op].ndim
@@ -317,6 +341,9 @@ def test_linear_ops_match_kronecker_matrix(oracle_mod, op):
     S = sps.identity(N).tocsr()[np.flatnonzero(inner.reshape(-1))]
     if op == W.HELMHOLTZ_2D:
         A = S @ (Lap + co.k ** 2 * I)
+        b = S @ C[0].reshape(-1)
+    elif op in (W.POISSON_2D, W.POISSON_3D):
+        A = S @ Lap
         b = S @ C[0].reshape(-1)
     else:
         A = S @ (I / co.dt - co.alpha * Lap)
@@ -393,18 +420,18 @@ def test_ns2d_u_gradient_matches_paper_equation(oracle_mod):
 # --------------------------------------------------------------------------- invariants
 
 
-@pytest.mark.parametrize("op", [W.NS_2D_STEADY, W.NS_3D_BE])
+@pytest.mark.parametrize("op", [W.NS_2D_STEADY, W.NS_3D_BE, W.NS_3D_STEADY, W.NS_2DT])
 def test_pressure_gradient_sums_to_zero(oracle_mod, op):
     ndim = W.OPS[op].ndim
     F, C = _rand_inputs(op, SHAPES[ndim], 600 + op)
     g = oracle_mod.grad(op, SHAPES[ndim], H[ndim], COEF[op], F, C)
-    gp = g[ndim]
+    gp = g[-1]
     # p enters only through centred first differences, whose rows sum to zero
     assert abs(gp.sum()) <= 1e-12 * np.abs(gp).sum()
     assert np.abs(gp).max() > 0
 
 
-@pytest.mark.parametrize("op", [W.HELMHOLTZ_2D, W.HEAT_3D_BE])
+@pytest.mark.parametrize("op", [W.HELMHOLTZ_2D, W.HEAT_3D_BE, W.POISSON_2D, W.POISSON_3D])
 def test_gradient_sum_equals_row_sum_times_G(oracle_mod, op):
     ndim = W.OPS[op].ndim
     shape, h, co = SHAPES[ndim], H[ndim], COEF[op]
@@ -414,7 +441,7 @@ def test_gradient_sum_equals_row_sum_times_G(oracle_mod, op):
     G = 2.0 * R / M
     g = oracle_mod.grad(op, shape, h, co, F, C)[0]
     # the Laplacian's rows sum to zero, so sum_n grad(n) = (row sum) * sum_m G(m)
-    row = co.k ** 2 if op == W.HELMHOLTZ_2D else 1.0 / co.dt
+    row = {W.HELMHOLTZ_2D: co.k ** 2, W.HEAT_3D_BE: 1.0 / co.dt}.get(op, 0.0)
     assert g.sum() == pytest.approx(row * G.sum(), rel=1e-10, abs=1e-12 * np.abs(g).sum())
 
 
@@ -452,7 +479,7 @@ def test_oracle_rejects_bad_arguments(oracle_mod):
     co = COEF[W.HEAT_3D_BE]
     F, C = _rand_inputs(W.HEAT_3D_BE, (4, 4, 4), 1)
     with pytest.raises(ValueError):
-        oracle_mod.op_info(9)
+        oracle_mod.op_info(len(W.OPS) + 1)
     with pytest.raises(ValueError):  # n < 3
         oracle_mod.loss(W.HEAT_3D_BE, (2, 4, 4), (1, 1, 1), co,
                         [np.zeros((2, 4, 4))], [np.zeros((2, 4, 4))])
