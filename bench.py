@@ -60,7 +60,7 @@ def parse():
 # fields the residual Jacobian depends on (what the explicit-sensitivity backward
 # reads besides G): none for the linear operators, the velocity but not the
 # pressure for NS
-JAC_FIELDS = {1: 1, 2: 0, 3: 0, 4: 2, 5: 3}
+JAC_FIELDS = {1: 1, 2: 0, 3: 0, 4: 2, 5: 3, 6: 3, 7: 0, 8: 0, 9: 2}
 
 
 def byte_model(wl, bc_mode=0, path="loss"):
@@ -107,7 +107,8 @@ def copy_gbps(torch, nbytes=1 << 30, reps=20):
 # the kernels one timed call queues, where it queues several
 TRAFFIC_KERNELS = {"value_and_grad": ("fill_f64", "bwd", "bc")}
 OP_KERNEL_TAG = {1: "OpBurgers", 2: "OpHelmholtz", 3: "OpHeat", 4: "OpNS<2, false>",
-                 5: "OpNS<3, true>"}
+                 5: "OpNS<3, true>", 6: "OpNS<3, false>", 7: "OpPoisson<2>", 8: "OpPoisson<3>",
+                 9: "OpNST"}
 
 
 def measured_traffic(cfg, op, kernels, path="loss"):

@@ -41,6 +41,17 @@
  *                                                         consts {u_prev, v_prev, w_prev}
  *       R_b = (c_b - c_b_prev)/dt + sum_a c_a D1_a c_b + D1_b p - nu sum_a D2_a c_b
  *       R_div = sum_a D1_a c_a
+ * Adjacent operators of the paper's operator table (Sec. 4), same kernels:
+ *   FPDE_NS_3D_STEADY (ndim 3)                            fields {u, v, w, p}  consts {}
+ *       R_b = sum_a c_a D1_a c_b + D1_b p - nu sum_a D2_a c_b ;  R_div as above
+ *   FPDE_POISSON_2D   (ndim 2)                            fields {u}        consts {f}
+ *   FPDE_POISSON_3D   (ndim 3)                            fields {u}        consts {f}
+ *       R = sum_a D2_a u - f
+ *   FPDE_NS_2DT       (ndim 3; space-time grid: axis 0 = t, axes 1, 2 = x, y;
+ *                      velocity component b on array axis b + 1)
+ *                                                         fields {u, v, p}  consts {}
+ *       R_b = D1_0 c_b + sum_a c_a D1_{a+1} c_b + D1_{b+1} p - nu sum_a D2_{a+1} c_b
+ *       R_div = sum_a D1_{a+1} c_a            (a, b = 0, 1; the time step is h[0])
  *
  * Common argument rules:
  *   - `fields`, `consts`, `residual_out`, `sens`, `grads` are HOST arrays holding
@@ -82,7 +93,11 @@ typedef enum fpde_op {
     FPDE_HELMHOLTZ_2D = 2,
     FPDE_HEAT_3D_BE = 3,
     FPDE_NS_2D_STEADY = 4,
-    FPDE_NS_3D_BE = 5
+    FPDE_NS_3D_BE = 5,
+    FPDE_NS_3D_STEADY = 6,
+    FPDE_POISSON_2D = 7,
+    FPDE_POISSON_3D = 8,
+    FPDE_NS_2DT = 9
 } fpde_op;
 
 /* Grid: rank, residual-set mode, sizes per array axis, spacings per axis.
@@ -104,7 +119,7 @@ typedef struct fpde_grid {
 typedef struct fpde_coeffs {
     double nu;     /* viscosity (Burgers, NS) */
     double k;      /* wave number (Helmholtz) */
-    double dt;     /* time step (heat, NS 3D); must be > 0 for those ops */
+    double dt;     /* time step (HEAT_3D_BE, NS_3D_BE); must be > 0 for those ops */
     double alpha;  /* diffusivity (heat) */
 } fpde_coeffs;
 

@@ -11,21 +11,6 @@
 namespace fpde {
 namespace {
 
-struct OpDesc {
-    int ndim, nf, nc, nr;
-};
-
-bool op_desc(int op, OpDesc* d) {
-    switch (op) {
-    case FPDE_BURGERS_1DT: *d = {2, 1, 0, 1}; return true;
-    case FPDE_HELMHOLTZ_2D: *d = {2, 1, 1, 1}; return true;
-    case FPDE_HEAT_3D_BE: *d = {3, 1, 1, 1}; return true;
-    case FPDE_NS_2D_STEADY: *d = {2, 3, 0, 3}; return true;
-    case FPDE_NS_3D_BE: *d = {3, 4, 3, 4}; return true;
-    default: return false;
-    }
-}
-
 // Launch geometry.  A workgroup owns a TX x TY column tile (TY = 1 for 2-D
 // grids, where a "plane" is one row) and marches a chunk of planes of axis 0.
 // 3-D grids: the chunk length is chosen once per call from the backward's
@@ -90,14 +75,63 @@ bool op_desc(int op, OpDesc* d) {
 constexpr int kTX3 = FPDE_TX3, kTX2 = FPDE_TX2, kTargetBlocks2 = FPDE_BLOCKS2;
 constexpr bool kBwdReverse = FPDE_BWD_REVERSE != 0;
 
-// forward tile TXF x TYf, backward tile TXB x TYb
-template <int TXF_, int TYF, int TYB, int MINB>
+// 3-D grids: forward tile TXF x TYf, backward tile TXB x TYb, explicit-sensitivity
+// backward tile TXV x TYV
+template <int TXF_, int TYF, int TYB, int MINB, int TXV_, int TYV_>
 struct Geo3 {
+    static constexpr bool D3 = true;
     static constexpr int TXF = TXF_, TYf = TYF, TXB = kTX3, TYb = TYB, MIN_BWD_BLOCKS = MINB;
+    static constexpr int TXV = TXV_, TYV = TYV_;
 };
-using GeoNS3 = Geo3<FPDE_NS3_FWD_TX, FPDE_NS3_FWD_TY, FPDE_NS3_BWD_TY, FPDE_NS3_MIN_BWD_BLOCKS>;
-using GeoHeat =
-    Geo3<FPDE_HEAT_FWD_TX, FPDE_HEAT_FWD_TY, FPDE_HEAT_BWD_TY, FPDE_HEAT_MIN_BWD_BLOCKS>;
+// 2-D grids: one-row tiles of kTX2 nodes for every kernel
+struct Geo2 {
+    static constexpr bool D3 = false;
+};
+// several fields with nonlinear coupling (NS)
+using GeoNS3 = Geo3<FPDE_NS3_FWD_TX, FPDE_NS3_FWD_TY, FPDE_NS3_BWD_TY, FPDE_NS3_MIN_BWD_BLOCKS,
+                    FPDE_VJP_TX3, FPDE_VJP_TY3>;
+// one field, a Laplacian (heat, Poisson)
+using GeoHeat = Geo3<FPDE_HEAT_FWD_TX, FPDE_HEAT_FWD_TY, FPDE_HEAT_BWD_TY,
+                     FPDE_HEAT_MIN_BWD_BLOCKS, FPDE_VJP_HEAT_TX, FPDE_VJP_HEAT_TY>;
+
+template <class OP_, class GEO_>
+struct OpTag {
+    using OP = OP_;    // point functions (fpde_ops.hpp)
+    using GEO = GEO_;  // launch shapes
+};
+
+// f(OpTag<...>{}) for the op, FPDE_ERR_ARG for an unknown op: the one table
+// that maps an op id to its point functions and launch shapes.
+template <class F>
+int with_op(int op, F&& f) {
+    switch (op) {
+    case FPDE_BURGERS_1DT: return f(OpTag<OpBurgers, Geo2>{});
+    case FPDE_HELMHOLTZ_2D: return f(OpTag<OpHelmholtz, Geo2>{});
+    case FPDE_HEAT_3D_BE: return f(OpTag<OpHeat, GeoHeat>{});
+    case FPDE_NS_2D_STEADY: return f(OpTag<OpNS2, Geo2>{});
+    case FPDE_NS_3D_BE: return f(OpTag<OpNS3, GeoNS3>{});
+    case FPDE_NS_3D_STEADY: return f(OpTag<OpNS3S, GeoNS3>{});
+    case FPDE_POISSON_2D: return f(OpTag<OpPoisson<2>, Geo2>{});
+    case FPDE_POISSON_3D: return f(OpTag<OpPoisson<3>, GeoHeat>{});
+    case FPDE_NS_2DT: return f(OpTag<OpNST, GeoNS3>{});
+    }
+    return FPDE_ERR_ARG;
+}
+
+struct OpDesc {
+    int ndim, nf, nc, nr;
+};
+
+bool op_desc(int op, OpDesc* d) {
+    return with_op(op, [&](auto tag) {
+        using OP = typename decltype(tag)::OP;
+        *d = {OP::DIM, OP::NF, OP::NC, OP::NR};
+        return FPDE_OK;
+    }) == FPDE_OK;
+}
+
+// ops with a time step dt among their coefficients
+bool uses_dt(int op) { return op == FPDE_HEAT_3D_BE || op == FPDE_NS_3D_BE; }
 
 struct Req {
     int op;
@@ -147,7 +181,7 @@ int validate_common(int op, const fpde_grid* g, const fpde_coeffs* c, const floa
         if (!finite_pos(g->h[a])) return FPDE_ERR_SPACING;
     if (!isfinite(c->nu) || !isfinite(c->k) || !isfinite(c->dt) || !isfinite(c->alpha))
         return FPDE_ERR_COEFF;
-    if ((op == FPDE_HEAT_3D_BE || op == FPDE_NS_3D_BE) && !(c->dt > 0.0)) return FPDE_ERR_COEFF;
+    if (uses_dt(op) && !(c->dt > 0.0)) return FPDE_ERR_COEFF;
 
     // float32 kernel coefficients, derived in float64
     KCoef K;
@@ -161,7 +195,7 @@ int validate_common(int op, const fpde_grid* g, const fpde_coeffs* c, const floa
     }
     K.nu = (float)c->nu;
     K.k2 = (float)(c->k * c->k);
-    K.inv_dt = (op == FPDE_HEAT_3D_BE || op == FPDE_NS_3D_BE) ? (float)(1.0 / c->dt) : 0.f;
+    K.inv_dt = uses_dt(op) ? (float)(1.0 / c->dt) : 0.f;
     K.alpha = (float)c->alpha;
     if (!isfinite(K.nu) || !isfinite(K.k2) || !isfinite(K.inv_dt) || !isfinite(K.alpha))
         return FPDE_ERR_COEFF;
@@ -303,55 +337,44 @@ int launch_vjp(const Req& r, bool acc, int target) {
 }
 
 int run_vjp(const Req& r, bool acc) {
-    constexpr int kTarget3 = FPDE_VJP_TARGET3;  // workgroups per launch (3-D)
-    switch (r.op) {
-    case FPDE_BURGERS_1DT: return launch_vjp<OpBurgers, kTX2, 1>(r, acc, kTargetBlocks2);
-    case FPDE_HELMHOLTZ_2D: return launch_vjp<OpHelmholtz, kTX2, 1>(r, acc, kTargetBlocks2);
-    case FPDE_HEAT_3D_BE:
-        return launch_vjp<OpHeat, FPDE_VJP_HEAT_TX, FPDE_VJP_HEAT_TY>(r, acc, kTarget3);
-    case FPDE_NS_2D_STEADY: return launch_vjp<OpNS2, kTX2, 1>(r, acc, kTargetBlocks2);
-    case FPDE_NS_3D_BE: return launch_vjp<OpNS3, FPDE_VJP_TX3, FPDE_VJP_TY3>(r, acc, kTarget3);
-    }
-    return FPDE_ERR_ARG;
+    return with_op(r.op, [&](auto tag) {
+        using OP = typename decltype(tag)::OP;
+        using GEO = typename decltype(tag)::GEO;
+        if constexpr (GEO::D3)
+            return launch_vjp<OP, GEO::TXV, GEO::TYV>(r, acc, FPDE_VJP_TARGET3);
+        else
+            return launch_vjp<OP, kTX2, 1>(r, acc, kTargetBlocks2);
+    });
 }
 
 int run_fwd(const Req& r, bool store, double* loss) {
-    switch (r.op) {
-    case FPDE_BURGERS_1DT: return launch_fwd<OpBurgers, kTX2, 1>(r, store, loss, zc2(r));
-    case FPDE_HELMHOLTZ_2D: return launch_fwd<OpHelmholtz, kTX2, 1>(r, store, loss, zc2(r));
-    case FPDE_HEAT_3D_BE:
-        return launch_fwd<OpHeat, GeoHeat::TXF, GeoHeat::TYf>(r, store, loss, zc3<GeoHeat>(r));
-    case FPDE_NS_2D_STEADY: return launch_fwd<OpNS2, kTX2, 1>(r, store, loss, zc2(r));
-    case FPDE_NS_3D_BE:
-        return launch_fwd<OpNS3, GeoNS3::TXF, GeoNS3::TYf>(r, store, loss, zc3<GeoNS3>(r));
-    }
-    return FPDE_ERR_ARG;
+    return with_op(r.op, [&](auto tag) {
+        using OP = typename decltype(tag)::OP;
+        using GEO = typename decltype(tag)::GEO;
+        if constexpr (GEO::D3)
+            return launch_fwd<OP, GEO::TXF, GEO::TYf>(r, store, loss, zc3<GEO>(r));
+        else
+            return launch_fwd<OP, kTX2, 1>(r, store, loss, zc2(r));
+    });
 }
 
 // loss: nullptr for the gradient alone, else also the loss (fused value and grad)
 int run_bwd(const Req& r, const double* dloss, double* loss = nullptr) {
-    switch (r.op) {
-    case FPDE_BURGERS_1DT: return launch_bwd<OpBurgers, kTX2, 1>(r, dloss, zc2(r), loss);
-    case FPDE_HELMHOLTZ_2D: return launch_bwd<OpHelmholtz, kTX2, 1>(r, dloss, zc2(r), loss);
-    case FPDE_HEAT_3D_BE:
-        return launch_bwd<OpHeat, GeoHeat::TXB, GeoHeat::TYb>(r, dloss, zc3<GeoHeat>(r), loss);
-    case FPDE_NS_2D_STEADY: return launch_bwd<OpNS2, kTX2, 1>(r, dloss, zc2(r), loss);
-    case FPDE_NS_3D_BE:
-        return launch_bwd<OpNS3, GeoNS3::TXB, GeoNS3::TYb>(r, dloss, zc3<GeoNS3>(r), loss);
-    }
-    return FPDE_ERR_ARG;
+    return with_op(r.op, [&](auto tag) {
+        using OP = typename decltype(tag)::OP;
+        using GEO = typename decltype(tag)::GEO;
+        if constexpr (GEO::D3)
+            return launch_bwd<OP, GEO::TXB, GEO::TYb>(r, dloss, zc3<GEO>(r), loss);
+        else
+            return launch_bwd<OP, kTX2, 1>(r, dloss, zc2(r), loss);
+    });
 }
 
 int run_bc(const Req& r, const double* dloss) {
     if (r.dims.per) return FPDE_OK;  // a periodic grid has no boundary: the march wrote every node
-    switch (r.op) {
-    case FPDE_BURGERS_1DT: return launch_bc<OpBurgers>(r, dloss);
-    case FPDE_HELMHOLTZ_2D: return launch_bc<OpHelmholtz>(r, dloss);
-    case FPDE_HEAT_3D_BE: return launch_bc<OpHeat>(r, dloss);
-    case FPDE_NS_2D_STEADY: return launch_bc<OpNS2>(r, dloss);
-    case FPDE_NS_3D_BE: return launch_bc<OpNS3>(r, dloss);
-    }
-    return FPDE_ERR_ARG;
+    return with_op(r.op, [&](auto tag) {
+        return launch_bc<typename decltype(tag)::OP>(r, dloss);
+    });
 }
 
 int prepare_grad_call(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,

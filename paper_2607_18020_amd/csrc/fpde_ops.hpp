@@ -241,5 +241,126 @@ struct OpNS {
 
 using OpNS2 = OpNS<2, false>;
 using OpNS3 = OpNS<3, true>;
+using OpNS3S = OpNS<3, false>;  // steady 3D NS
+
+// ---------------------------------------------------------------------------
+// Poisson: R = lap u - f   (self-adjoint: dL/du = lap R).
+template <int D>
+struct OpPoisson {
+    static constexpr int DIM = D, NF = 1, NC = 1, NR = 1, NG = 0, NFG = 0;
+
+    __device__ __forceinline__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
+        R[0] = lap<D>(f[0], K) - c[0];
+    }
+
+    __device__ __forceinline__ static void gather(const Star*, const Star* r, const KCoef& K, float* g) {
+        g[0] = lap<D>(r[0], K);
+    }
+    __device__ __forceinline__ static void gather_self(const Star*, const float*, const KCoef&, float*) {}
+    __device__ __forceinline__ static void gather_rest(const Star* f, const Star* r, const float*, const KCoef& K, float* g) {
+        gather(f, r, K, g);
+    }
+
+    template <int AX>
+    __device__ __forceinline__ static void bc_term(const Star* f, const float* c, const KCoef& K, float, float* g) {
+        float R[1];
+        residual(f, c, K, R);
+        g[0] = R[0] * K.ih2[AX];
+    }
+};
+
+// ---------------------------------------------------------------------------
+// Unsteady incompressible NS on a 2D+t space-time grid: array axis 0 is t
+// (a centred difference in time, step h_0), velocity component b on array axis
+// b + 1, pressure last.
+//   R_b = D1_0 c_b + sum_a c_a D1_{a+1} c_b + D1_{b+1} p - nu lap_xy c_b
+//   R_div = sum_a D1_{a+1} c_a                     (a, b over x and y)
+struct OpNST {
+    static constexpr int D = 2;  // spatial dimensions
+    static constexpr int DIM = 3, NF = D + 1, NC = 0, NR = D + 1, NG = D, NFG = D;
+
+    __device__ __forceinline__ static float lap_xy(const Star& s, const KCoef& K) {
+        float l = 0.f;
+#pragma unroll
+        for (int a = 1; a <= D; ++a) l += ((s.p[a] - s.c) + (s.m[a] - s.c)) * K.ih2[a];
+        return l;
+    }
+
+    __device__ __forceinline__ static void residual(const Star* f, const float*, const KCoef& K, float* R) {
+        float cs[D];  // c_a / (2 h_{a+1}), shared by the momentum equations
+#pragma unroll
+        for (int a = 0; a < D; ++a) cs[a] = f[a].c * K.i2h[a + 1];
+        double div = 0.0;
+#pragma unroll
+        for (int b = 0; b < D; ++b) {
+            float r = (f[b].p[0] - f[b].m[0]) * K.i2h[0];  // time derivative
+#pragma unroll
+            for (int a = 0; a < D; ++a) r = fmaf(cs[a], f[b].p[a + 1] - f[b].m[a + 1], r);
+            r = fmaf(f[D].p[b + 1] - f[D].m[b + 1], K.i2h[b + 1], r);
+            R[b] = fmaf(-K.nu, lap_xy(f[b], K), r);
+            div = fma((double)f[b].p[b + 1] - (double)f[b].m[b + 1], K.i2hd[b + 1], div);
+        }
+        R[D] = (float)div;
+    }
+
+    // dL/dc_q(n) = sum_b R_b(n) D1_{q+1} c_b(n) + (R_q(n-e_0) - R_q(n+e_0)) / (2 h_0)
+    //            + sum_a (R_q(n-e_{a+1}) c_a(n-e_{a+1}) - R_q(n+e_{a+1}) c_a(n+e_{a+1})) / (2 h_{a+1})
+    //            + (R_div(n-e_{q+1}) - R_div(n+e_{q+1})) / (2 h_{q+1}) - nu lap_xy R_q(n)
+    // dL/dp(n)   = sum_b (R_b(n-e_{b+1}) - R_b(n+e_{b+1})) / (2 h_{b+1})
+    __device__ __forceinline__ static void gather_self(const Star* f, const float* R, const KCoef& K, float* S) {
+#pragma unroll
+        for (int q = 0; q < D; ++q) {
+            float loc = R[0] * (f[0].p[q + 1] - f[0].m[q + 1]);
+#pragma unroll
+            for (int b = 1; b < D; ++b) loc = fmaf(R[b], f[b].p[q + 1] - f[b].m[q + 1], loc);
+            S[q] = loc * K.i2h[q + 1];
+        }
+    }
+
+    __device__ __forceinline__ static void gather_rest(const Star* f, const Star* r, const float* S, const KCoef& K, float* g) {
+        float gp = 0.f;
+#pragma unroll
+        for (int q = 0; q < D; ++q) {
+            float acc = fmaf(r[q].m[0] - r[q].p[0], K.i2h[0], S[q]);
+#pragma unroll
+            for (int a = 0; a < D; ++a)
+                acc = fmaf(fmaf(r[q].m[a + 1], f[a].m[a + 1], -(r[q].p[a + 1] * f[a].p[a + 1])),
+                           K.i2h[a + 1], acc);
+            acc = fmaf(r[D].m[q + 1] - r[D].p[q + 1], K.i2h[q + 1], acc);
+            g[q] = fmaf(-K.nu, lap_xy(r[q], K), acc);
+            gp = fmaf(r[q].m[q + 1] - r[q].p[q + 1], K.i2h[q + 1], gp);
+        }
+        g[D] = gp;
+    }
+
+    __device__ __forceinline__ static void gather(const Star* f, const Star* r, const KCoef& K, float* g) {
+        float R[NR], S[D];
+#pragma unroll
+        for (int b = 0; b < NR; ++b) R[b] = r[b].c;
+        gather_self(f, R, K, S);
+        gather_rest(f, r, S, K, g);
+    }
+
+    // n = m + t e_AX: only the neighbour terms of R_b(m) along AX reach n.
+    template <int AX>
+    __device__ __forceinline__ static void bc_term(const Star* f, const float* c, const KCoef& K, float t, float* g) {
+        float R[NR];
+        residual(f, c, K, R);
+        if (AX == 0) {  // time: only the time derivative of the velocities
+#pragma unroll
+            for (int q = 0; q < D; ++q) g[q] = R[q] * t * K.i2h[0];
+            g[D] = 0.f;
+        } else {
+            constexpr int S_ = AX - 1;  // the velocity component along AX
+#pragma unroll
+            for (int q = 0; q < D; ++q) {
+                float v = R[q] * (t * f[S_].c * K.i2h[AX] - K.nu * K.ih2[AX]);
+                if (q == S_) v += R[D] * t * K.i2h[AX];
+                g[q] = v;
+            }
+            g[D] = R[S_] * t * K.i2h[AX];
+        }
+    }
+};
 
 }  // namespace fpde
