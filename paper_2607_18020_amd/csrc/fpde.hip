@@ -18,8 +18,14 @@ namespace {
 // backward, so that the backward, which marches each chunk top down, starts on
 // the planes the forward read last (still in the memory-side infinity cache).
 // 2-D grids: chunks sized for about kTargetBlocks2 workgroups per launch.
-#ifndef FPDE_TX3
-#define FPDE_TX3 64
+// backward tile widths: a tile's x-halo columns sit in cache lines of the
+// neighbouring tiles, which L2 serves only while the two tiles march in step;
+// wider tiles have fewer such lines per node
+#ifndef FPDE_NS3_BWD_TX
+#define FPDE_NS3_BWD_TX 128
+#endif
+#ifndef FPDE_HEAT_BWD_TX
+#define FPDE_HEAT_BWD_TX 64
 #endif
 // forward tile widths (a tile's side-edge x-neighbours cost a cache line each)
 #ifndef FPDE_NS3_FWD_TX
@@ -32,7 +38,7 @@ namespace {
 #define FPDE_NS3_FWD_TY 8
 #endif
 #ifndef FPDE_NS3_BWD_TY
-#define FPDE_NS3_BWD_TY 16
+#define FPDE_NS3_BWD_TY 8
 #endif
 #ifndef FPDE_NS3_MIN_BWD_BLOCKS
 #define FPDE_NS3_MIN_BWD_BLOCKS 256
@@ -72,15 +78,15 @@ namespace {
 #ifndef FPDE_BWD_REVERSE
 #define FPDE_BWD_REVERSE 1
 #endif
-constexpr int kTX3 = FPDE_TX3, kTX2 = FPDE_TX2, kTargetBlocks2 = FPDE_BLOCKS2;
+constexpr int kTX2 = FPDE_TX2, kTargetBlocks2 = FPDE_BLOCKS2;
 constexpr bool kBwdReverse = FPDE_BWD_REVERSE != 0;
 
 // 3-D grids: forward tile TXF x TYf, backward tile TXB x TYb, explicit-sensitivity
 // backward tile TXV x TYV
-template <int TXF_, int TYF, int TYB, int MINB, int TXV_, int TYV_>
+template <int TXF_, int TYF, int TXB_, int TYB, int MINB, int TXV_, int TYV_>
 struct Geo3 {
     static constexpr bool D3 = true;
-    static constexpr int TXF = TXF_, TYf = TYF, TXB = kTX3, TYb = TYB, MIN_BWD_BLOCKS = MINB;
+    static constexpr int TXF = TXF_, TYf = TYF, TXB = TXB_, TYb = TYB, MIN_BWD_BLOCKS = MINB;
     static constexpr int TXV = TXV_, TYV = TYV_;
 };
 // 2-D grids: one-row tiles of kTX2 nodes for every kernel
@@ -88,10 +94,10 @@ struct Geo2 {
     static constexpr bool D3 = false;
 };
 // several fields with nonlinear coupling (NS)
-using GeoNS3 = Geo3<FPDE_NS3_FWD_TX, FPDE_NS3_FWD_TY, FPDE_NS3_BWD_TY, FPDE_NS3_MIN_BWD_BLOCKS,
-                    FPDE_VJP_TX3, FPDE_VJP_TY3>;
+using GeoNS3 = Geo3<FPDE_NS3_FWD_TX, FPDE_NS3_FWD_TY, FPDE_NS3_BWD_TX, FPDE_NS3_BWD_TY,
+                    FPDE_NS3_MIN_BWD_BLOCKS, FPDE_VJP_TX3, FPDE_VJP_TY3>;
 // one field, a Laplacian (heat, Poisson)
-using GeoHeat = Geo3<FPDE_HEAT_FWD_TX, FPDE_HEAT_FWD_TY, FPDE_HEAT_BWD_TY,
+using GeoHeat = Geo3<FPDE_HEAT_FWD_TX, FPDE_HEAT_FWD_TY, FPDE_HEAT_BWD_TX, FPDE_HEAT_BWD_TY,
                      FPDE_HEAT_MIN_BWD_BLOCKS, FPDE_VJP_HEAT_TX, FPDE_VJP_HEAT_TY>;
 
 template <class OP_, class GEO_>

@@ -18,7 +18,7 @@ from tests import gpu_helpers as H
 pytestmark = pytest.mark.gpu
 
 # (config, shape): several tiles along every axis plus ragged tails (2-D rows are
-# 256-node segments; 3-D tiles are 64 or 256 nodes wide in x; chunks of planes
+# 256-node segments; 3-D tiles are 64, 128 or 256 nodes wide in x; chunks of planes
 # along axis 0)
 SMALL = [
     ("burgers_1dt", (3, 3)), ("burgers_1dt", (5, 7)), ("burgers_1dt", (41, 300)),
