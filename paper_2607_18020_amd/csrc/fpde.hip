@@ -5,6 +5,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <type_traits>
+
 #include "fpde.h"
 #include "fpde_engine.hpp"
 
@@ -281,32 +283,41 @@ int hip_status() {
 
 // ---- launches, per op type
 
+// f(std::bool_constant<v>{}) for a runtime flag v: kernels take flags that
+// decide their per-step control flow (periodic wrap, ...) as template arguments
+template <class F>
+void with_flag(bool v, F&& f) {
+    if (v) f(std::true_type{});
+    else f(std::false_type{});
+}
+
 template <class OP, int TX, int TY>
 int launch_fwd(const Req& r, bool store, double* loss, int zc) {
     const Dims dm = tile_dims(r.dims, TX, TY, zc);
     hipLaunchKernelGGL(fill_f64_kernel, dim3(1), dim3(1), 0, r.stream, loss, 0.0);
-    if (store)
-        hipLaunchKernelGGL((fwd_kernel<OP, TX, TY, true>), dim3(dm.nblocks), dim3(TX * TY), 0,
-                           r.stream, r.P, dm, r.K, r.inv_M, loss);
-    else
-        hipLaunchKernelGGL((fwd_kernel<OP, TX, TY, false>), dim3(dm.nblocks), dim3(TX * TY), 0,
-                           r.stream, r.P, dm, r.K, r.inv_M, loss);
+    with_flag(store, [&](auto st) {
+        with_flag(dm.per, [&](auto per) {
+            hipLaunchKernelGGL((fwd_kernel<OP, TX, TY, decltype(st)::value, decltype(per)::value>),
+                               dim3(dm.nblocks), dim3(TX * TY), 0, r.stream, r.P, dm, r.K, r.inv_M,
+                               loss);
+        });
+    });
     return hip_status();
 }
 
 template <class OP, int TX, int TY>
 int launch_bwd(const Req& r, const double* dloss, int zc, double* loss) {
     const Dims dm = tile_dims(r.dims, TX, TY, zc);
-    if (loss) {  // value and gradient in one pass
-        hipLaunchKernelGGL(fill_f64_kernel, dim3(1), dim3(1), 0, r.stream, loss, 0.0);
-        hipLaunchKernelGGL((bwd_kernel<OP, TX, TY, kBwdReverse, true>), dim3(dm.nblocks),
-                           dim3(TX * TY), 0, r.stream, r.P, dm, r.K, dloss, r.two_over_M, r.inv_M,
-                           loss);
-    } else {
-        hipLaunchKernelGGL((bwd_kernel<OP, TX, TY, kBwdReverse, false>), dim3(dm.nblocks),
-                           dim3(TX * TY), 0, r.stream, r.P, dm, r.K, dloss, r.two_over_M, r.inv_M,
-                           nullptr);
-    }
+    // value and gradient in one pass when loss is given
+    if (loss) hipLaunchKernelGGL(fill_f64_kernel, dim3(1), dim3(1), 0, r.stream, loss, 0.0);
+    with_flag(loss != nullptr, [&](auto lo) {
+        with_flag(dm.per, [&](auto per) {
+            hipLaunchKernelGGL(
+                (bwd_kernel<OP, TX, TY, kBwdReverse, decltype(lo)::value, decltype(per)::value>),
+                dim3(dm.nblocks), dim3(TX * TY), 0, r.stream, r.P, dm, r.K, dloss, r.two_over_M,
+                r.inv_M, loss);
+        });
+    });
     return hip_status();
 }
 
@@ -333,12 +344,12 @@ int launch_vjp(const Req& r, bool acc, int target) {
     Dims base = r.dims;
     base.zlo = 0;
     const Dims dm = tile_dims(base, TX, TY, chunk_planes(base, TX, TY, target));
-    if (acc)
-        hipLaunchKernelGGL((vjp_kernel<OP, TX, TY, true>), dim3(dm.nblocks), dim3(TX * TY), 0,
-                           r.stream, r.P, dm, r.K);
-    else
-        hipLaunchKernelGGL((vjp_kernel<OP, TX, TY, false>), dim3(dm.nblocks), dim3(TX * TY), 0,
-                           r.stream, r.P, dm, r.K);
+    with_flag(acc, [&](auto ac) {
+        with_flag(dm.per, [&](auto per) {
+            hipLaunchKernelGGL((vjp_kernel<OP, TX, TY, decltype(ac)::value, decltype(per)::value>),
+                               dim3(dm.nblocks), dim3(TX * TY), 0, r.stream, r.P, dm, r.K);
+        });
+    });
     return hip_status();
 }
 

@@ -64,7 +64,8 @@ struct Dims {
     int nz, ny, nx;         // ny = 1 for 2-D grids
     int tiles_x, tiles_y;   // tiles_y = 1 for 2-D grids
     int zc, nblocks;        // planes per chunk, workgroups launched
-    int per;                // periodic wrap on every axis (residual at every node)
+    int per;                // periodic wrap on every axis (residual at every node); the
+                            // marching kernels take it as their template argument PER
     int zlo;                // first marched plane: 1, or 0 when periodic
 };
 
@@ -312,7 +313,7 @@ struct PlaneStream {
 // float64, reduced with DPP across the wavefront and through LDS across waves,
 // then added with ONE float64 atomic per workgroup.
 
-template <class OP, int TX, int TY, bool STORE_R>
+template <class OP, int TX, int TY, bool STORE_R, bool PER>
 __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims D, KCoef K,
                                                                     double inv_M, double* loss) {
     constexpr int DIM = OP::DIM, NF = OP::NF, NC = OP::NC, NR = OP::NR, NT = TX * TY;
@@ -338,9 +339,9 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
     const uint32_t pbytes = (uint32_t)D.ny * (uint32_t)D.nx * 4u;
     const bool inarr = gx < D.nx && gy < D.ny;
     const bool interior =
-        D.per ? inarr : gx >= 1 && gx <= D.nx - 2 && (DIM == 2 || (gy >= 1 && gy <= D.ny - 2));
+        PER ? inarr : gx >= 1 && gx <= D.nx - 2 && (DIM == 2 || (gy >= 1 && gy <= D.ny - 2));
     const uint32_t cb = inarr ? (uint32_t)(gy * D.nx + gx) * 4u : 0u;
-    auto zw = [&](int z) { return D.per ? wrap_idx(z, D.nz) : z; };  // plane index
+    auto zw = [&](int z) { return PER ? wrap_idx(z, D.nz) : z; };  // plane index
 
     PS ps;
     ps.init(t, [&](int i, int& lin) {
@@ -354,7 +355,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
             px = side == 0 ? tc.gx0 - 1 : tc.gx0 + TX;
             if (side > 1) return false;
         }
-        if (D.per) {  // every position is a node of the wrapped grid
+        if (PER) {  // every position is a node of the wrapped grid
             px = wrap_idx(px, D.nx);
             py = wrap_idx(py, D.ny);
         }
@@ -378,7 +379,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
     // node: the first and the last chunk write their zeros.  (Whole rows are
     // written, boundary columns included, so that no cache line of R is stored
     // in part.)
-    if (STORE_R && !D.per) {
+    if (STORE_R && !PER) {
         const uint32_t so = inarr ? cb : kDropOff;
 #pragma unroll
         for (int b = 0; b < NR; ++b) {
@@ -469,7 +470,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
 // the equations, float64 accumulation, one float64 atomic per workgroup onto
 // *loss, which the host zeroes first): the fields are read once for both.
 
-template <class OP, int TX, int TY, bool REV, bool LOSS>
+template <class OP, int TX, int TY, bool REV, bool LOSS, bool PER>
 __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims D, KCoef K,
                                                                     const double* dloss,
                                                                     double two_over_M,
@@ -496,7 +497,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     const int z0 = tc.z0, z1 = tc.z1, L = z1 - z0;
     auto ph = [&](int w) {  // (wrapped into the grid when periodic)
         const int p = REV ? z1 - 1 - w : z0 + w;
-        return D.per ? wrap_idx(p, D.nz) : p;
+        return PER ? wrap_idx(p, D.nz) : p;
     };
     const int gx = tc.gx0 + tx, gy = (DIM == 3) ? tc.gy0 + ty : 0;
     const uint32_t pbytes = (uint32_t)D.ny * (uint32_t)D.nx * 4u;
@@ -506,13 +507,13 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     // periodic grid the wrapped one (a ragged tile's first lane past the last
     // column holds the residual that column's gather needs as its x+1 term)
     const uint32_t cbr =
-        D.per ? (uint32_t)(wrap_idx(gy, D.ny) * D.nx + wrap_idx(gx, D.nx)) * 4u : cb;
+        PER ? (uint32_t)(wrap_idx(gy, D.ny) * D.nx + wrap_idx(gx, D.nx)) * 4u : cb;
     const float scale = (float)(two_over_M * (*dloss));
 
     PS ps;
     ps.init(t, [&](int i, int& lin) {
         int py = (DIM == 3) ? tc.gy0 - HY + i / FLX : 0, px = tc.gx0 - 2 + i % FLX;
-        if (D.per) {  // every position is a node of the wrapped grid
+        if (PER) {  // every position is a node of the wrapped grid
             px = wrap_idx(px, D.nx);
             py = wrap_idx(py, D.ny);
         }
@@ -531,16 +532,16 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     // residual-set test and their const offsets are fixed for the whole march
     const int oly = ty + RHY, olx = tx + 1;
     const bool own_om =
-        D.per || (gx >= 1 && gx <= D.nx - 2 && (DIM == 2 || (gy >= 1 && gy <= D.ny - 2)));
+        PER || (gx >= 1 && gx <= D.nx - 2 && (DIM == 2 || (gy >= 1 && gy <= D.ny - 2)));
     const bool has_ring = t < Ring<TX, TY, DIM>::COUNT;
     int rly = 0, rlx = 0;
     if (has_ring) Ring<TX, TY, DIM>::pos(t, rly, rlx);
     const int rgy = (DIM == 3) ? tc.gy0 - RHY + rly : 0, rgx = tc.gx0 - 1 + rlx;
-    const bool ring_om = has_ring && (D.per || (rgx >= 1 && rgx <= D.nx - 2 &&
+    const bool ring_om = has_ring && (PER || (rgx >= 1 && rgx <= D.nx - 2 &&
                                                 (DIM == 2 || (rgy >= 1 && rgy <= D.ny - 2))));
     const uint32_t rcb =
         !ring_om ? 0u
-        : D.per  ? (uint32_t)(wrap_idx(rgy, D.ny) * D.nx + wrap_idx(rgx, D.nx)) * 4u
+        : PER  ? (uint32_t)(wrap_idx(rgy, D.ny) * D.nx + wrap_idx(rgx, D.nx)) * 4u
                  : (uint32_t)(rgy * D.nx + rgx) * 4u;
 
     // R at physical plane zr, at node fi of a field slot and ri of an R tile, from
@@ -565,7 +566,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
             }
         }
         OP::residual(s, cc, K, R);
-        const bool om = om_xy && (D.per || (zr >= 1 && zr <= D.nz - 2));
+        const bool om = om_xy && (PER || (zr >= 1 && zr <= D.nz - 2));
 #pragma unroll
         for (int b = 0; b < NR; ++b) {
             R[b] = om ? R[b] : 0.f;
@@ -615,7 +616,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
             const float v = bld(plane_rsrc(P.f[f], zok ? pz : 0, pbytes), cbr);
-            fzm2[f] = ((inarr || D.per) && zok) ? v : 0.f;
+            fzm2[f] = ((inarr || PER) && zok) ? v : 0.f;
         }
     }
     load_consts(ph(0), true);
@@ -646,7 +647,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
 #pragma unroll
         for (int j = 0; j < NC; ++j) cc[j] = bld(plane_rsrc(P.c[j], pz, pbytes), cbr);
         OP::residual(s, cc, K, rzm);
-        const bool om = own_om && (D.per || (pz >= 1 && pz <= D.nz - 2));
+        const bool om = own_om && (PER || (pz >= 1 && pz <= D.nz - 2));
 #pragma unroll
         for (int b = 0; b < NR; ++b) rzm[b] = om ? rzm[b] : 0.f;
     }
@@ -755,7 +756,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
 // which the loads enforce with out-of-range offsets, whatever the arrays hold
 // there).
 
-template <class OP, int TX, int TY, bool ACC>
+template <class OP, int TX, int TY, bool ACC, bool PER>
 __global__ __launch_bounds__(TX* TY, FPDE_VJP_MINW) void vjp_kernel(Ptrs P, Dims D, KCoef K) {
     constexpr int DIM = OP::DIM, NF = OP::NF, NR = OP::NR, NT = TX * TY;
     constexpr int NFG = OP::NFG;  // fields the Jacobian depends on (the others are not read)
@@ -776,7 +777,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_VJP_MINW) void vjp_kernel(Ptrs P, Dims
     const uint32_t pbytes = (uint32_t)D.ny * (uint32_t)D.nx * 4u;
     const bool inarr = gx < D.nx && gy < D.ny;
     const uint32_t cb = inarr ? (uint32_t)(gy * D.nx + gx) * 4u : 0u;
-    auto zw = [&](int z) { return D.per ? wrap_idx(z, D.nz) : z; };  // plane index
+    auto zw = [&](int z) { return PER ? wrap_idx(z, D.nz) : z; };  // plane index
 
     // slot element -> grid position (the forward's layout); for the
     // sensitivities, positions off the residual set read as 0
@@ -791,12 +792,12 @@ __global__ __launch_bounds__(TX* TY, FPDE_VJP_MINW) void vjp_kernel(Ptrs P, Dims
             px = side == 0 ? tc.gx0 - 1 : tc.gx0 + TX;
             if (side > 1) return false;
         }
-        if (D.per) {
+        if (PER) {
             px = wrap_idx(px, D.nx);
             py = wrap_idx(py, D.ny);
         }
         lin = py * D.nx + px;
-        if (omega && !D.per)
+        if (omega && !PER)
             return px >= 1 && px <= D.nx - 2 && (DIM == 2 || (py >= 1 && py <= D.ny - 2));
         return px >= 0 && px < D.nx && py >= 0 && py < D.ny;
     };
@@ -810,7 +811,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_VJP_MINW) void vjp_kernel(Ptrs P, Dims
 #pragma unroll
         for (int a = 0; a < NA; ++a) dst[a] = &sF(slot)[a][0];
         if constexpr (NFG > 0) psf.template load<NFG>(P.f, pz, D.nz, pbytes, dst);
-        const bool gok = D.per || (pz >= 1 && pz <= D.nz - 2);
+        const bool gok = PER || (pz >= 1 && pz <= D.nz - 2);
         psg.template load<NR>(P.s, gok ? pz : -1, D.nz, pbytes, dst + NFG);
     };
     float gq[2][NF];  // accumulate mode: the stored gradients of the next plane
