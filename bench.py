@@ -134,8 +134,9 @@ def measured_traffic(cfg, op, kernels, path="loss"):
     return round(total)
 
 
-def cpu_baseline(W, wl_full, cfg, seed, planes, bc_mode=0, path="loss"):
-    """The oracle (single thread, float64) on a slab of the same workload."""
+def cpu_baseline(W, wl_full, cfg, seed, planes, bc_mode=0, path="loss", min_s=10.0):
+    """The oracle (single thread, float64) on a slab of the same workload, timed
+    over repeated passes totalling at least min_s seconds."""
     import numpy as np  # noqa: PLC0415
     import oracle  # noqa: PLC0415  (CPU baseline leg only)
     shape = wl_full.shape
@@ -152,21 +153,29 @@ def cpu_baseline(W, wl_full, cfg, seed, planes, bc_mode=0, path="loss"):
     if path == "residual":
         G = [np.ascontiguousarray(g[sl], dtype=np.float64)
              for g in W.sensitivities(wl_full.op, shape, seed + 1)]
-        t0 = time.perf_counter()
-        oracle.residual(*args, bc_mode=bc_mode)
-        oracle.vjp(*args, G, bc_mode=bc_mode)
+
+        def one():
+            oracle.residual(*args, bc_mode=bc_mode)
+            oracle.vjp(*args, G, bc_mode=bc_mode)
         what = "residuals + transposed-Jacobian action"
     else:
-        t0 = time.perf_counter()
-        oracle.loss(*args, bc_mode=bc_mode)
-        oracle.grad(*args, dloss=1.0, bc_mode=bc_mode)
+        def one():
+            oracle.loss(*args, bc_mode=bc_mode)
+            oracle.grad(*args, dloss=1.0, bc_mode=bc_mode)
         what = "loss + full gradient"
-    dt = time.perf_counter() - t0
+    # repeated until at least min_s of CPU work has been timed (one pass at least)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        one()
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_s:
+            break
     npts = int(np.prod(sshape))
-    return {"value": npts / dt, "unit": "grid-points/s", "cores": 1, "kind": "oracle",
+    return {"value": npts * reps / dt, "unit": "grid-points/s", "cores": 1, "kind": "oracle",
             "sample": f"{cfg} seed {seed}: first {planes} planes along axis 0 "
                       f"({'x'.join(map(str, sshape))} = {npts} nodes), {what}, "
-                      f"float64, single thread, {dt:.2f} s"}
+                      f"float64, single thread, {reps} passes in {dt:.2f} s"}
 
 
 def main():
