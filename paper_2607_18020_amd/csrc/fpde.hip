@@ -57,6 +57,15 @@ namespace {
 #ifndef FPDE_TX2
 #define FPDE_TX2 256
 #endif
+// 2-D forward rows: the loss atomics of a short launch arrive together and are
+// serialised on one address, so the forward uses fewer, wider workgroups
+#ifndef FPDE_TX2_FWD
+#define FPDE_TX2_FWD 1024
+#endif
+// 2-D one-pass value and gradient (the backward with the loss atomics)
+#ifndef FPDE_TX2_VG
+#define FPDE_TX2_VG 512
+#endif
 // explicit-sensitivity backward tiles (3-D)
 #ifndef FPDE_VJP_TX3
 #define FPDE_VJP_TX3 64
@@ -80,7 +89,8 @@ namespace {
 #ifndef FPDE_BWD_REVERSE
 #define FPDE_BWD_REVERSE 1
 #endif
-constexpr int kTX2 = FPDE_TX2, kTargetBlocks2 = FPDE_BLOCKS2;
+constexpr int kTX2 = FPDE_TX2, kTX2F = FPDE_TX2_FWD, kTX2V = FPDE_TX2_VG,
+              kTargetBlocks2 = FPDE_BLOCKS2;
 constexpr bool kBwdReverse = FPDE_BWD_REVERSE != 0;
 
 // 3-D grids: forward tile TXF x TYf, backward tile TXB x TYb, explicit-sensitivity
@@ -371,7 +381,7 @@ int run_fwd(const Req& r, bool store, double* loss) {
         if constexpr (GEO::D3)
             return launch_fwd<OP, GEO::TXF, GEO::TYf>(r, store, loss, zc3<GEO>(r));
         else
-            return launch_fwd<OP, kTX2, 1>(r, store, loss, zc2(r));
+            return launch_fwd<OP, kTX2F, 1>(r, store, loss, zc2(r));
     });
 }
 
@@ -383,7 +393,8 @@ int run_bwd(const Req& r, const double* dloss, double* loss = nullptr) {
         if constexpr (GEO::D3)
             return launch_bwd<OP, GEO::TXB, GEO::TYb>(r, dloss, zc3<GEO>(r), loss);
         else
-            return launch_bwd<OP, kTX2, 1>(r, dloss, zc2(r), loss);
+            return loss ? launch_bwd<OP, kTX2V, 1>(r, dloss, zc2(r), loss)
+                        : launch_bwd<OP, kTX2, 1>(r, dloss, zc2(r), loss);
     });
 }
 

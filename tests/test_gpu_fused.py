@@ -18,6 +18,8 @@ CASES = [
     ("heat_3d", (3, 3, 3)), ("heat_3d", (5, 6, 7)), ("heat_3d", (19, 21, 70)),
     ("heat_3d", (9, 10, 300)),
     ("ns_2d", (6, 257)), ("ns_2d", (71, 600)),
+    # rows wider than one 512-node segment of the one-pass kernel, ragged tail
+    ("ns_2d", (5, 1300)), ("helmholtz_2d", (7, 1030)),
     ("ns_3d_tgv", (3, 3, 3)), ("ns_3d_tgv", (4, 9, 66)), ("ns_3d_tgv", (19, 21, 70)),
     ("ns_3d_tgv", (40, 17, 129)), ("ns_3d_tgv", (7, 9, 300)), ("ns_3d_tgv", (42, 256, 256)),
 ]

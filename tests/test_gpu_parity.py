@@ -18,7 +18,7 @@ from tests import gpu_helpers as H
 pytestmark = pytest.mark.gpu
 
 # (config, shape): several tiles along every axis plus ragged tails (2-D rows are
-# 256-node segments; 3-D tiles are 64, 128 or 256 nodes wide in x; chunks of planes
+# 256-, 512- or 1024-node segments; 3-D tiles are 64, 128 or 256 nodes wide in x; chunks of planes
 # along axis 0)
 SMALL = [
     ("burgers_1dt", (3, 3)), ("burgers_1dt", (5, 7)), ("burgers_1dt", (41, 300)),
@@ -36,6 +36,8 @@ SMALL = [
     # the unrolled march, its tail and the seams between chunks are all exercised
     ("heat_3d", (42, 256, 256)), ("ns_3d_tgv", (42, 256, 256)), ("ns_3d_tgv", (75, 130, 200)),
     ("ns_2d", (700, 513)),
+    # 2-D rows wider than one 1024-node forward row segment, ragged last segment
+    ("ns_2d", (5, 2500)), ("helmholtz_2d", (9, 1100)), ("burgers_1dt", (6, 3000)),
 ]
 
 
