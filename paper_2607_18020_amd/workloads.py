@@ -336,6 +336,24 @@ def normal_fields(op: int, shape: Sequence[int], seed: int,
                     fields, consts)
 
 
+def normal_fields_f32(op: int, shape: Sequence[int], seed: int,
+                      h: Optional[Sequence[float]] = None,
+                      coeffs: Optional[Coeffs] = None) -> Workload:
+    """Standard-normal inputs drawn directly in float32 (a seeded stream of its
+    own, distinct from normal_fields): for grids of billions of nodes, where
+    drawing in float64 first would double the host memory and time."""
+    wl = normal_fields(op, (3,) * OPS[op].ndim, seed, None, coeffs)  # coefficients only
+    shape = tuple(int(s) for s in shape)
+    rng = np.random.default_rng(seed)
+    spec = OPS[op]
+    fields = [rng.standard_normal(shape, dtype=np.float32) for _ in spec.fields]
+    consts = [rng.standard_normal(shape, dtype=np.float32) for _ in spec.consts]
+    if h is None:
+        h = tuple(1.0 / (s - 1) for s in shape)
+    return Workload(f"normal32_{OP_NAMES[op]}", op, shape, tuple(float(x) for x in h),
+                    wl.coeffs if coeffs is None else coeffs, fields, consts)
+
+
 def sensitivities(op: int, shape: Sequence[int], seed: int) -> List[np.ndarray]:
     """Upstream residual sensitivities G_b (one standard-normal float32 array
     per residual, full size) for the explicit-sensitivity backward."""

@@ -139,8 +139,13 @@ def test_validation_status_codes(B, fn):
         assert _call(B, fn, op3, s3, consts=[_addr(10), _addr(11), 0]) == ARG
     # misaligned field
     assert _call(B, fn, op3, s3, fields=[_addr(0), _addr(1, 2), _addr(2), _addr(3)]) == ALIGN
-    # periodic mode is reserved
+    # an unknown boundary mode
     assert _call(B, fn, op3, s3, bc_mode=7) == ARG
+    # size limits: a plane of the non-marching axes below 2^29 nodes, every n_a below 2^31
+    assert _call(B, fn, op3, (3, 1 << 14, 1 << 15)) == SHAPE
+    assert _call(B, fn, op3, (3, 1 << 15, 1 << 14)) == SHAPE
+    assert _call(B, fn, op2, (3, 1 << 29)) == SHAPE
+    assert _call(B, fn, op2, (1 << 31, 5)) == SHAPE
 
 
 def test_output_checks(B):
