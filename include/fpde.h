@@ -102,7 +102,7 @@ typedef enum fpde_op {
 
 /* Grid: rank, residual-set mode, sizes per array axis, spacings per axis.
  * bc_mode 0: the interior residual set Omega above; 1: periodic wrap on every
- * axis (the survey's reading B of the Taylor-Green grid); other values are
+ * axis (the fully periodic reading of the Taylor-Green grid); other values are
  * rejected with FPDE_ERR_ARG.  Entries past ndim are ignored.
  * Limits: every n_a >= 3 and n_a < 2^31; a plane of the non-marching axes
  * (n[1]*n[2] for ndim 3, n[1] for ndim 2) holds fewer than 2^29 nodes. */
@@ -175,14 +175,17 @@ int fpde_bc_correct(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
  * the residuals (dL/dq = (2/M) J^T R), which the backward recomputes anyway, so
  * the forward pass of Sec. 2.1 folds into it when the upstream derivative
  * dloss is known before the call (1.0 for L itself): the backward kernel also
- * sums the squares of the residuals it evaluates.
+ * sums the squares of the residuals it evaluates.  Its march covers every plane
+ * of axis 0, the end planes too: there the transposed stencil with the
+ * residuals off Omega taken as zero is exactly the boundary term that
+ * fpde_bc_correct writes (equal up to the float32 rounding order).
  *   dloss  device pointer to one double, as in fpde_residual_bwd.
  *   loss   device pointer to one double; OVERWRITTEN with L (not dloss * L);
  *          must not overlap any other argument array (FPDE_ERR_ARG).
  *   grads  host array of n_fields device pointers; OVERWRITTEN at every node.
- * Other arguments and errors as fpde_residual_bwd.  Queues 3 kernels (2 on a
- * periodic grid): a one-element fill zeroing *loss, the backward march (one
- * float64 atomic add per workgroup onto *loss) and the boundary correction. */
+ * Other arguments and errors as fpde_residual_bwd.  Queues 2 kernels: a
+ * one-element fill zeroing *loss, then the backward march (one float64 atomic
+ * add per workgroup onto *loss). */
 int fpde_residual_value_and_grad(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
                                  const float* const* fields, const float* const* consts,
                                  const double* dloss, double* loss, float* const* grads,

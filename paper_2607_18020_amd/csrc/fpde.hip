@@ -385,8 +385,13 @@ int run_fwd(const Req& r, bool store, double* loss) {
     });
 }
 
-// loss: nullptr for the gradient alone, else also the loss (fused value and grad)
-int run_bwd(const Req& r, const double* dloss, double* loss = nullptr) {
+// loss: nullptr for the gradient alone (planes 1 .. n0-2; the boundary kernel
+// writes the end planes), else also the loss (fused value and grad), marching
+// every plane: at the end planes the gather with the residuals off the residual
+// set taken as zero is their exact boundary term, so no boundary kernel follows
+int run_bwd(const Req& r0, const double* dloss, double* loss = nullptr) {
+    Req r = r0;
+    if (loss) r.dims.zlo = 0;
     return with_op(r.op, [&](auto tag) {
         using OP = typename decltype(tag)::OP;
         using GEO = typename decltype(tag)::GEO;
@@ -491,9 +496,7 @@ extern "C" int fpde_residual_value_and_grad(int op, const fpde_grid* grid,
             return FPDE_ERR_ARG;
     for (int j = 0; j < r.d.nc; ++j)
         if (overlaps(loss, sizeof(double), consts[j], bytes)) return FPDE_ERR_ARG;
-    st = run_bwd(r, dloss, loss);
-    if (st != FPDE_OK) return st;
-    return run_bc(r, dloss);
+    return run_bwd(r, dloss, loss);
 }
 
 extern "C" int fpde_residual_vjp(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,

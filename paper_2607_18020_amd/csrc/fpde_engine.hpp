@@ -66,7 +66,8 @@ struct Dims {
     int zc, nblocks;        // planes per chunk, workgroups launched
     int per;                // periodic wrap on every axis (residual at every node); the
                             // marching kernels take it as their template argument PER
-    int zlo;                // first marched plane: 1, or 0 when periodic
+    int zlo;                // first marched plane: 1, or 0 when periodic or when the
+                            // backward march also covers the end planes (value and grad)
 };
 
 // i in [-n, 2n) wrapped into [0, n) (periodic grids; a ragged tile reaches past n)
@@ -577,7 +578,10 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     // consts of the R-tile positions, for the plane whose residuals come next
     // (loaded one step ahead so that their latency hides behind a step)
     float cown[NC1], cring[NC1];
+    // (a march over every plane, end planes included, reaches past the grid: such
+    // planes read as 0, and their residuals are masked to 0 anyway)
     auto load_consts = [&](int zr, bool ok) __attribute__((always_inline)) {  // zr uniform
+        ok = ok && zr >= 0 && zr < D.nz;
 #pragma unroll
         for (int j = 0; j < NC; ++j) {
             const __amdgpu_buffer_rsrc_t r = plane_rsrc_if(P.c[j], zr, pbytes, ok);
@@ -642,10 +646,11 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
             }
             fzm[f] = s[f].c;
         }
-        const int pz = ph(-1);  // in [0, nz): z0 - 1 >= 0 and z1 <= nz - 1, or wrapped
+        const int pz = ph(-1);  // past the grid when the march covers the end planes
+        const bool pok = pz >= 0 && pz < D.nz;
         float cc[NC1];
 #pragma unroll
-        for (int j = 0; j < NC; ++j) cc[j] = bld(plane_rsrc(P.c[j], pz, pbytes), cbr);
+        for (int j = 0; j < NC; ++j) cc[j] = bld(plane_rsrc_if(P.c[j], pz, pbytes, pok), cbr);
         OP::residual(s, cc, K, rzm);
         const bool om = own_om && (PER || (pz >= 1 && pz <= D.nz - 2));
 #pragma unroll
