@@ -105,7 +105,7 @@ def copy_gbps(torch, nbytes=1 << 30, reps=20):
 
 
 # the kernels one timed call queues, where it queues several
-TRAFFIC_KERNELS = {"value_and_grad": ("fill_f64", "bwd", "bc")}
+TRAFFIC_KERNELS = {"value_and_grad": ("fill_f64", "bwd")}
 OP_KERNEL_TAG = {1: "OpBurgers", 2: "OpHelmholtz", 3: "OpHeat", 4: "OpNS<2, false>",
                  5: "OpNS<3, true>", 6: "OpNS<3, false>", 7: "OpPoisson<2>", 8: "OpPoisson<3>",
                  9: "OpNST"}
@@ -306,7 +306,7 @@ def main():
                    "seed": args.seed,
                    "step": {"loss": "fwd+loss, bwd, bc on one stream",
                             "residual": "fwd writing residuals, explicit-sensitivity vjp",
-                            "fused": "one-pass loss + gradient (fill, bwd march with loss, bc)"
+                            "fused": "one-pass loss + gradient (fill, bwd march with loss over every plane)"
                             }[args.path],
                    "path": args.path, "bc_mode": bcm},
         "hbm_gbps": round(gbps, 1),
