@@ -12,6 +12,10 @@ Byte model (each input read once per pass, each output written once):
   them again and write one gradient per field, so one step moves
   (2 (NF + NC) + NF) * 4 bytes per grid node (72 B/node for the 3D NS case).
 
+Beside the warm figure (steps back to back, as a training loop calls the
+operator), "flushed" times steps one by one after writing 512 MB between them,
+so that every input comes from HBM rather than the 256 MB memory-side cache.
+
 --path fused times fpde_residual_value_and_grad, the same loss and gradient
 from one read of the inputs ((2 NF + NC) * 4 B/node: 44 for the 3D NS case).
 
@@ -54,6 +58,10 @@ def parse():
                         "and gradient")
     p.add_argument("--sample-every", type=int, default=10,
                    help="per-kernel HIP events on every n-th timed step (the others carry none)")
+    p.add_argument("--flushed-steps", type=int, default=20,
+                   help="after the timed region, steps timed one by one with 512 MB written "
+                        "between them (outside the events), so that no input is left in the "
+                        "caches; reported beside the warm figure (0: skip)")
     return p.parse_args()
 
 
@@ -82,6 +90,28 @@ def byte_model(wl, bc_mode=0, path="loss"):
         "bwd": (nf + nc) * 4 * N + nf * 4 * M,
         "per_node": (2 * (nf + nc) + nf) * 4,
     }
+
+
+def flushed_steps(torch, step, stream, n, flush_bytes=512 << 20):
+    """Each of n steps timed alone (events on the step's stream) after a 512 MB
+    write that evicts the 256 MB memory-side cache and L2, the write outside
+    the events: the step's inputs then come from HBM.  Median and quartiles of
+    the per-step milliseconds."""
+    import statistics  # noqa: PLC0415
+    buf = torch.empty(flush_bytes // 4, dtype=torch.float32, device="cuda")
+    ms = []
+    for i in range(n):
+        buf.fill_(float(i))
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        step()
+        b.record(stream)
+        b.synchronize()
+        ms.append(a.elapsed_time(b))
+    del buf
+    q = statistics.quantiles(ms, n=4) if len(ms) > 1 else [ms[0]] * 3
+    return {"steps": n, "ms_per_step_median": round(q[1], 4), "ms_q1": round(q[0], 4),
+            "ms_q3": round(q[2], 4), "flush_bytes": flush_bytes}
 
 
 def copy_gbps(torch, nbytes=1 << 30, reps=20):
@@ -284,6 +314,10 @@ def main():
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                 "traffic": measured_traffic(cfg, wl.op, TRAFFIC_KERNELS.get(dom, (dom,)), args.path),
                 "algorithmic_bytes_per_launch": bm[dom], "avg_launch_us": round(per[dom], 2)}
+    flushed = None
+    if args.flushed_steps > 0:
+        flushed = flushed_steps(torch, step, stream, args.flushed_steps)
+        flushed["grid_points_per_s"] = N / (flushed["ms_per_step_median"] * 1e-3)
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(W, wl, cfg, args.seed, args.cpu_planes, bcm, args.path)
@@ -315,6 +349,7 @@ def main():
         "kernel_us": {k: round(v, 2) for k, v in per.items()},
         "kernel_us_sampled_steps": len(sampled),
         "copy_gbps": round(copy_gbps(torch), 1),
+        "flushed": flushed,
         "roofline": roofline,
         "cpu_baseline": cpu,
     }

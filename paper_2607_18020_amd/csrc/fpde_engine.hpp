@@ -531,7 +531,6 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     // residual positions of this thread on the R tile: its own column and, for
     // the first threads, one node of the ring; their in-plane part of the
     // residual-set test and their const offsets are fixed for the whole march
-    const int oly = ty + RHY, olx = tx + 1;
     const bool own_om =
         PER || (gx >= 1 && gx <= D.nx - 2 && (DIM == 2 || (gy >= 1 && gy <= D.ny - 2)));
     const bool has_ring = t < Ring<TX, TY, DIM>::COUNT;
@@ -589,12 +588,10 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
             cring[j] = bld(r, rcb);
         }
     };
-    // R on the whole R tile; the own column's values are returned in Rown
+    // positions in a field slot and in an R tile: the own node, and the ring node
     const int fown = (ty + HY) * FLX + tx + 2;   // own node in a field slot
     const int rown = (ty + RHY) * RLX + tx + 1;  // own node in an R tile
     const int fring = (rly + HY - RHY) * FLX + rlx + 1, rring = rly * RLX + rlx;  // ring node
-    (void)oly;
-    (void)olx;
 
     // R on the whole R tile; the own column's R and gather self terms are returned
     // in Rown, Sown.  fo, ro, fr, rr: a step's copies of fown, rown, fring, rring
