@@ -106,10 +106,18 @@ def _ptr_array(tensors):
 
 
 def _check_tensors(tensors, shape, what):
+    dev = None
     for t in tensors:
         if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != torch.float32 \
                 or not t.is_contiguous() or tuple(t.shape) != tuple(shape):
             raise ValueError(f"{what}: need contiguous float32 CUDA tensors of shape {tuple(shape)}")
+        dev = t.device if dev is None else dev
+        if t.device != dev:
+            raise ValueError(f"{what}: tensors on different devices ({dev}, {t.device})")
+    # the kernels run on the current HIP device
+    if dev is not None and dev.index != torch.cuda.current_device():
+        raise ValueError(f"{what}: tensors on {dev}, current device is "
+                         f"cuda:{torch.cuda.current_device()}")
 
 
 def _stream(stream) -> int:
@@ -125,6 +133,9 @@ def fpde_residual_fwd(op: int, fields, consts, h, coeffs, *, residual_out=None,
     dev = fields[0].device
     if loss is None:
         loss = torch.empty((), dtype=torch.float64, device=dev)
+    if loss.dtype != torch.float64 or loss.device != dev or loss.numel() != 1:
+        raise ValueError("fpde_residual_fwd: loss must be a one-element float64 tensor on the "
+                         "fields' device")
     res_arr = None
     if residual_out is not None:
         _check_tensors(residual_out, shape, "fpde_residual_fwd residual_out")
@@ -146,8 +157,8 @@ def _grad_call(fn, name, op, fields, consts, h, coeffs, dloss, grads, bc_mode, s
     _check_tensors(grads, shape, name + " grads")
     if not isinstance(dloss, torch.Tensor):
         dloss = torch.tensor(float(dloss), dtype=torch.float64, device=fields[0].device)
-    if dloss.dtype != torch.float64 or not dloss.is_cuda or dloss.numel() != 1:
-        raise ValueError(f"{name}: dloss must be a one-element float64 CUDA tensor")
+    if dloss.dtype != torch.float64 or dloss.device != fields[0].device or dloss.numel() != 1:
+        raise ValueError(f"{name}: dloss must be a one-element float64 tensor on the fields' device")
     g, c = make_grid(shape, h, bc_mode), make_coeffs(coeffs)
     st = fn(int(op), ctypes.byref(g), ctypes.byref(c), _ptr_array(fields),
             _ptr_array(consts) if len(consts) else None, dloss.data_ptr(), _ptr_array(grads),
@@ -178,8 +189,9 @@ def fpde_residual_value_and_grad(op: int, fields, consts, h, coeffs, dloss=1.0, 
     (loss, grads): the float64 loss L and dloss * dL/dq for every field."""
     if loss is None:
         loss = torch.empty((), dtype=torch.float64, device=fields[0].device)
-    if loss.dtype != torch.float64 or not loss.is_cuda or loss.numel() != 1:
-        raise ValueError("fpde_residual_value_and_grad: loss must be a one-element float64 CUDA tensor")
+    if loss.dtype != torch.float64 or loss.device != fields[0].device or loss.numel() != 1:
+        raise ValueError("fpde_residual_value_and_grad: loss must be a one-element float64 "
+                         "tensor on the fields' device")
 
     def fn(op_, g, c, fp, cp_, dl, gp, st):
         return _load().fpde_residual_value_and_grad(op_, g, c, fp, cp_, dl, loss.data_ptr(), gp, st)

@@ -1,0 +1,60 @@
+"""The Python binding's argument checks (marshalling only): tensors that the C
+ABI cannot take are refused before any call, with ValueError; ABI status codes
+come back as FpdeError."""
+from __future__ import annotations
+
+import pytest
+
+from paper_2607_18020_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs():
+    import torch  # noqa: PLC0415
+    wl = W.make("ns_3d_tgv", seed=42, shape=(6, 7, 70))
+    f = [torch.from_numpy(x).cuda() for x in wl.fields]
+    c = [torch.from_numpy(x).cuda() for x in wl.consts]
+    return wl, f, c
+
+
+def test_binding_refuses_unusable_tensors():
+    import torch  # noqa: PLC0415
+    from paper_2607_18020_amd import binding as B  # noqa: PLC0415
+    wl, f, c = _inputs()
+    with pytest.raises(ValueError):  # a host tensor
+        B.fpde_residual_fwd(wl.op, [f[0].cpu()] + f[1:], c, wl.h, wl.coeffs)
+    with pytest.raises(ValueError):  # float64
+        B.fpde_residual_fwd(wl.op, [f[0].double()] + f[1:], c, wl.h, wl.coeffs)
+    with pytest.raises(ValueError):  # not contiguous
+        B.fpde_residual_fwd(wl.op, [f[0].transpose(1, 2).contiguous().transpose(1, 2)] + f[1:],
+                            c, wl.h, wl.coeffs)
+    with pytest.raises(ValueError):  # shapes differ
+        B.fpde_residual_fwd(wl.op, f, [c[0][:, :, :-1].contiguous()] + c[1:], wl.h, wl.coeffs)
+    with pytest.raises(ValueError):  # loss of the wrong type
+        B.fpde_residual_fwd(wl.op, f, c, wl.h, wl.coeffs,
+                            loss=torch.empty((), dtype=torch.float32, device="cuda"))
+    dl_host = torch.ones((), dtype=torch.float64)
+    with pytest.raises(ValueError):  # dloss on the host
+        B.fpde_residual_bwd(wl.op, f, c, wl.h, wl.coeffs, dl_host)
+    with pytest.raises(ValueError):  # value-and-grad loss on the host
+        B.fpde_residual_value_and_grad(wl.op, f, c, wl.h, wl.coeffs, 1.0,
+                                       loss=torch.empty((), dtype=torch.float64))
+    with pytest.raises(ValueError):  # accumulate into nothing
+        B.fpde_residual_vjp(wl.op, f, wl.h, wl.coeffs, [torch.zeros_like(f[0])] * 4,
+                            accumulate=True)
+
+
+def test_binding_reports_abi_status():
+    import torch  # noqa: PLC0415
+    from paper_2607_18020_amd import binding as B  # noqa: PLC0415
+    wl, f, c = _inputs()
+    # grads aliasing a field: the library refuses with FPDE_ERR_ARG and queues nothing
+    with pytest.raises(B.FpdeError) as e:
+        B.fpde_residual_bwd(wl.op, f, c, wl.h, wl.coeffs, 1.0, grads=[f[0]] + f[1:])
+    assert e.value.status == -1
+    # a spacing of zero: FPDE_ERR_SPACING
+    with pytest.raises(B.FpdeError) as e:
+        B.fpde_residual_fwd(wl.op, f, c, (wl.h[0], 0.0, wl.h[2]), wl.coeffs)
+    assert e.value.status == -3
+    torch.cuda.synchronize()
