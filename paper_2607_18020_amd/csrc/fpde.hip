@@ -31,13 +31,13 @@ namespace {
 #endif
 // forward tile widths (a tile's side-edge x-neighbours cost a cache line each)
 #ifndef FPDE_NS3_FWD_TX
-#define FPDE_NS3_FWD_TX 64
+#define FPDE_NS3_FWD_TX 128
 #endif
 #ifndef FPDE_HEAT_FWD_TX
 #define FPDE_HEAT_FWD_TX 256
 #endif
 #ifndef FPDE_NS3_FWD_TY
-#define FPDE_NS3_FWD_TY 8
+#define FPDE_NS3_FWD_TY 4
 #endif
 #ifndef FPDE_NS3_BWD_TY
 #define FPDE_NS3_BWD_TY 8
