@@ -62,6 +62,11 @@ namespace {
 #ifndef FPDE_TX2_FWD
 #define FPDE_TX2_FWD 1024
 #endif
+// 2-D forward register queue: rows held per lane (the centre row, its two
+// neighbours, and Q - 3 rows in flight)
+#ifndef FPDE_FWD2_Q
+#define FPDE_FWD2_Q 6
+#endif
 // 2-D one-pass value and gradient (the backward with the loss atomics)
 #ifndef FPDE_TX2_VG
 #define FPDE_TX2_VG 512
@@ -315,6 +320,21 @@ int launch_fwd(const Req& r, bool store, double* loss, int zc) {
     return hip_status();
 }
 
+// 2-D forward: the register-queue kernel (no LDS, no barrier)
+template <class OP, int TX>
+int launch_fwd2(const Req& r, bool store, double* loss, int zc) {
+    const Dims dm = tile_dims(r.dims, TX, 1, zc);
+    hipLaunchKernelGGL(fill_f64_kernel, dim3(1), dim3(1), 0, r.stream, loss, 0.0);
+    with_flag(store, [&](auto st) {
+        with_flag(dm.per, [&](auto per) {
+            hipLaunchKernelGGL(
+                (fwd2_kernel<OP, TX, FPDE_FWD2_Q, decltype(st)::value, decltype(per)::value>),
+                dim3(dm.nblocks), dim3(TX), 0, r.stream, r.P, dm, r.K, r.inv_M, loss);
+        });
+    });
+    return hip_status();
+}
+
 template <class OP, int TX, int TY>
 int launch_bwd(const Req& r, const double* dloss, int zc, double* loss) {
     const Dims dm = tile_dims(r.dims, TX, TY, zc);
@@ -381,7 +401,7 @@ int run_fwd(const Req& r, bool store, double* loss) {
         if constexpr (GEO::D3)
             return launch_fwd<OP, GEO::TXF, GEO::TYf>(r, store, loss, zc3<GEO>(r));
         else
-            return launch_fwd<OP, kTX2F, 1>(r, store, loss, zc2(r));
+            return launch_fwd2<OP, kTX2F>(r, store, loss, zc2(r));
     });
 }
 
