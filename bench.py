@@ -237,34 +237,24 @@ def main():
 
     bcm = args.bc_mode
 
-    def fwd():
-        B.fpde_residual_fwd(op, fields, consts, h, co, loss=loss, bc_mode=bcm, stream=stream)
-
-    def bwd():
-        B.fpde_residual_bwd(op, fields, consts, h, co, dl, grads=grads, bc_mode=bcm, stream=stream)
-
-    def bc():
-        B.fpde_bc_correct(op, fields, consts, h, co, dl, grads=grads, bc_mode=bcm, stream=stream)
-
+    # the entry points bound once to the resident tensors: each step issues only
+    # the C calls (marshalling them in Python every time costs more host time
+    # than a small grid's GPU time)
+    kw = dict(bc_mode=bcm, stream=stream)
+    fwd = B.bind("fwd", op, fields, consts, h, co, loss=loss, **kw)
+    bwd = B.bind("bwd", op, fields, consts, h, co, dloss=dl, grads=grads, **kw)
+    bc = B.bind("bc", op, fields, consts, h, co, dloss=dl, grads=grads, **kw)
     kernels = (("fwd", fwd), ("bwd", bwd), ("bc", bc))
     if args.path == "residual":
         R = [torch.empty_like(fields[0]) for _ in wl.spec.residuals]
         sens = [torch.from_numpy(g).to(dev) for g in W.sensitivities(op, wl.shape, args.seed + 1)]
-
-        def fwd_r():
-            B.fpde_residual_fwd(op, fields, consts, h, co, residual_out=R, loss=loss, bc_mode=bcm,
-                                stream=stream)
-
-        def vjp():
-            B.fpde_residual_vjp(op, fields, h, co, sens, grads=grads, bc_mode=bcm, stream=stream)
-
+        fwd_r = B.bind("fwd", op, fields, consts, h, co, residual_out=R, loss=loss, **kw)
+        vjp = B.bind("vjp", op, fields, None, h, co, sens=sens, grads=grads, **kw)
         kernels = (("fwd", fwd_r), ("vjp", vjp))
     if args.path == "fused":
-        def value_and_grad():
-            B.fpde_residual_value_and_grad(op, fields, consts, h, co, dl, loss=loss, grads=grads,
-                                           bc_mode=bcm, stream=stream)
-
-        kernels = (("value_and_grad", value_and_grad),)  # (fill, march, bc: one call)
+        value_and_grad = B.bind("value_and_grad", op, fields, consts, h, co, dloss=dl, loss=loss,
+                                grads=grads, **kw)
+        kernels = (("value_and_grad", value_and_grad),)  # (fill and march: one call)
     names = [n for n, _ in kernels]
 
     def step():

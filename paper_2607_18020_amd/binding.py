@@ -222,6 +222,90 @@ def fpde_residual_vjp(op: int, fields, h, coeffs, sens, *, grads=None, accumulat
     return grads
 
 
+# ---------------------------------------------------------------------------
+# Pre-marshalled calls.  Each call above validates its tensors and builds its
+# ctypes arguments in Python, tens of microseconds of host time: more than the
+# GPU time of the operator on small grids, where a loop of calls is then bound
+# by the host.  bind(...) does that work once for fixed tensors and returns a
+# callable that issues only the C call (which still validates its arguments).
+# The callable keeps references to every tensor it was bound to, so their
+# storage stays valid; their values may change between calls.
+
+class BoundCall:
+    """One entry point bound to fixed tensors, coefficients and stream."""
+
+    def __init__(self, name, fn, args, keep, result):
+        self.name, self._fn, self._args, self._keep, self.result = name, fn, args, keep, result
+
+    def __call__(self):
+        st = self._fn(*self._args)
+        if st != FPDE_OK:
+            raise FpdeError(st, self.name)
+        return self.result
+
+
+def bind(entry: str, op: int, fields, consts, h, coeffs, *, dloss=None, grads=None, loss=None,
+         residual_out=None, sens=None, accumulate: bool = False, bc_mode: int = 0, stream=None):
+    """Bind one entry point ("fwd", "bwd", "bc", "value_and_grad" or "vjp") to
+    fixed tensors; the returned BoundCall queues the call each time it is
+    called and returns what the unbound function returns (loss, grads or
+    (loss, grads))."""
+    shape = tuple(fields[0].shape)
+    dev = fields[0].device
+    consts = list(consts) if consts is not None else []
+    _check_tensors(list(fields) + consts, shape, f"bind {entry}")
+    g, c = make_grid(shape, h, bc_mode), make_coeffs(coeffs)
+    fa = _ptr_array(fields)
+    ca = _ptr_array(consts) if len(consts) else None
+    sh = _stream(stream)
+    lib = _load()
+    keep = [g, c, fa, ca, list(fields), consts]
+    if entry in ("fwd", "value_and_grad"):
+        if loss is None:
+            loss = torch.empty((), dtype=torch.float64, device=dev)
+        if loss.dtype != torch.float64 or loss.device != dev or loss.numel() != 1:
+            raise ValueError(f"bind {entry}: loss must be a one-element float64 tensor on the "
+                             "fields' device")
+        keep.append(loss)
+    if entry == "fwd":
+        ra = None
+        if residual_out is not None:
+            _check_tensors(residual_out, shape, "bind fwd residual_out")
+            ra = _ptr_array(residual_out)
+            keep += [ra, list(residual_out)]
+        args = (int(op), ctypes.byref(g), ctypes.byref(c), fa, ca, ra, loss.data_ptr(), sh)
+        return BoundCall("fpde_residual_fwd", lib.fpde_residual_fwd, args, keep, loss)
+    if grads is None:
+        grads = [torch.empty_like(f) for f in fields]
+    _check_tensors(grads, shape, f"bind {entry} grads")
+    ga = _ptr_array(grads)
+    keep += [ga, list(grads)]
+    if entry == "vjp":
+        _check_tensors(sens, shape, "bind vjp sensitivities")
+        sa = _ptr_array(sens)
+        keep += [sa, list(sens)]
+        args = (int(op), ctypes.byref(g), ctypes.byref(c), fa, sa, int(bool(accumulate)), ga, sh)
+        return BoundCall("fpde_residual_vjp", lib.fpde_residual_vjp, args, keep, grads)
+    if not isinstance(dloss, torch.Tensor):
+        dloss = torch.tensor(1.0 if dloss is None else float(dloss), dtype=torch.float64,
+                             device=dev)
+    if dloss.dtype != torch.float64 or dloss.device != dev or dloss.numel() != 1:
+        raise ValueError(f"bind {entry}: dloss must be a one-element float64 tensor on the "
+                         "fields' device")
+    keep.append(dloss)
+    if entry == "value_and_grad":
+        args = (int(op), ctypes.byref(g), ctypes.byref(c), fa, ca, dloss.data_ptr(),
+                loss.data_ptr(), ga, sh)
+        return BoundCall("fpde_residual_value_and_grad", lib.fpde_residual_value_and_grad, args,
+                         keep, (loss, grads))
+    if entry not in ("bwd", "bc"):
+        raise ValueError(f"bind: unknown entry point {entry!r}")
+    fn = lib.fpde_residual_bwd if entry == "bwd" else lib.fpde_bc_correct
+    name = "fpde_residual_bwd" if entry == "bwd" else "fpde_bc_correct"
+    args = (int(op), ctypes.byref(g), ctypes.byref(c), fa, ca, dloss.data_ptr(), ga, sh)
+    return BoundCall(name, fn, args, keep, grads)
+
+
 class Residual(torch.autograd.Function):
     """Drop-in differentiable residual op: forward = the fused stencil writing
     the residual arrays (zero off the residual set), backward = the

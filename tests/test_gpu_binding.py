@@ -58,3 +58,40 @@ def test_binding_reports_abi_status():
         B.fpde_residual_fwd(wl.op, f, c, (wl.h[0], 0.0, wl.h[2]), wl.coeffs)
     assert e.value.status == -3
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("cfg", ["ns_3d_tgv", "ns_2d"])
+def test_bound_calls_match_unbound(cfg):
+    """bind(...) only moves the marshalling out of the call: the same kernels on
+    the same tensors, so the same results (gradients bitwise; the loss up to
+    the order of its float64 atomics)."""
+    import torch  # noqa: PLC0415
+    from paper_2607_18020_amd import binding as B  # noqa: PLC0415
+    wl = W.make(cfg, seed=44, shape=(9, 20, 70) if cfg == "ns_3d_tgv" else (30, 300))
+    f = [torch.from_numpy(x).cuda() for x in wl.fields]
+    c = [torch.from_numpy(x).cuda() for x in wl.consts]
+    dl = torch.tensor(0.75, dtype=torch.float64, device="cuda")
+    L0 = B.fpde_residual_fwd(wl.op, f, c, wl.h, wl.coeffs)
+    g0 = B.fpde_residual_bwd(wl.op, f, c, wl.h, wl.coeffs, dl)
+    B.fpde_bc_correct(wl.op, f, c, wl.h, wl.coeffs, dl, grads=g0)
+    Lv0, gv0 = B.fpde_residual_value_and_grad(wl.op, f, c, wl.h, wl.coeffs, dl)
+    sens = [torch.from_numpy(x).cuda() for x in W.sensitivities(wl.op, wl.shape, 3)]
+    gj0 = B.fpde_residual_vjp(wl.op, f, wl.h, wl.coeffs, sens)
+    fwd = B.bind("fwd", wl.op, f, c, wl.h, wl.coeffs)
+    bwd = B.bind("bwd", wl.op, f, c, wl.h, wl.coeffs, dloss=dl)
+    bc = B.bind("bc", wl.op, f, c, wl.h, wl.coeffs, dloss=dl, grads=bwd.result)
+    vg = B.bind("value_and_grad", wl.op, f, c, wl.h, wl.coeffs, dloss=dl)
+    vj = B.bind("vjp", wl.op, f, None, wl.h, wl.coeffs, sens=sens)
+    for _ in range(3):  # repeated calls reuse the bound arguments
+        L1 = fwd()
+        g1 = bwd()
+        bc()
+        Lv1, gv1 = vg()
+        gj1 = vj()
+        torch.cuda.synchronize()
+        assert abs(L1.item() - L0.item()) <= 1e-12 * abs(L0.item())
+        assert abs(Lv1.item() - Lv0.item()) <= 1e-12 * abs(Lv0.item())
+        for a, b in zip(g1 + gv1 + gj1, g0 + gv0 + gj0):
+            assert torch.equal(a, b)
+    with pytest.raises(ValueError):
+        B.bind("nonsense", wl.op, f, c, wl.h, wl.coeffs)
