@@ -38,6 +38,9 @@ SMALL = [
     ("ns_2d", (700, 513)),
     # 2-D rows wider than one 1024-node forward row segment, ragged last segment
     ("ns_2d", (5, 2500)), ("helmholtz_2d", (9, 1100)), ("burgers_1dt", (6, 3000)),
+    # tall 2-D grids: chunks of 14 or more rows, several passes of the forward's
+    # unrolled row queue and its tail
+    ("ns_2d", (13400, 40)), ("helmholtz_2d", (15000, 20)), ("burgers_1dt", (20000, 30)),
 ]
 
 

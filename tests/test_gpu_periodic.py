@@ -22,6 +22,8 @@ CASES = [
     ("ns_2d", (6, 257)), ("ns_2d", (71, 600)),
     ("ns_3d_tgv", (3, 3, 3)), ("ns_3d_tgv", (4, 9, 66)), ("ns_3d_tgv", (19, 21, 70)),
     ("ns_3d_tgv", (40, 17, 129)), ("ns_3d_tgv", (7, 9, 300)), ("ns_3d_tgv", (42, 256, 256)),
+    # tall 2-D grids: chunks of 14 rows, several passes of the unrolled row queue
+    ("ns_2d", (13400, 40)), ("burgers_1dt", (20000, 30)),
 ]
 
 
