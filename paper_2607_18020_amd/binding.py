@@ -7,6 +7,7 @@ fallback: importing fails loudly when libfpde.so has not been built.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 from typing import Optional, Sequence
@@ -15,6 +16,9 @@ import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libfpde.so")
+# the checking build of the same sources (LDS poisoned with NaN, other tilings);
+# tests only
+CHECK_LIB_PATH = os.path.join(_HERE, "libfpde_check.so")
 
 FPDE_OK = 0
 STATUS_NAMES = {0: "FPDE_OK", -1: "FPDE_ERR_ARG", -2: "FPDE_ERR_SHAPE", -3: "FPDE_ERR_SPACING",
@@ -73,6 +77,20 @@ def _load():
 def lib():
     """The loaded ctypes library (raises ImportError if it is not built)."""
     return _load()
+
+
+@contextlib.contextmanager
+def library(path: str):
+    """Within the block, the calls of this module go to another build of the C
+    ABI at ``path`` (the tests compare the checking build with the product)."""
+    global _lib, LIB_PATH
+    saved = (_lib, LIB_PATH)
+    _lib, LIB_PATH = None, path
+    try:
+        _load()
+        yield
+    finally:
+        _lib, LIB_PATH = saved
 
 
 def op_info(op: int):

@@ -185,6 +185,26 @@ using IC = std::integral_constant<int, V>;
         else return NAME##3;                                                         \
     }
 
+// Checking build (FPDE_LDS_POISON): every LDS array of a marching kernel is
+// filled with NaN before the march, so that a read of a location no load or
+// residual evaluation has written shows up as NaN in the outputs.
+#ifndef FPDE_LDS_POISON
+#define FPDE_LDS_POISON 0
+#endif
+__device__ __forceinline__ void poison_lds(float* p, int n) {
+    if (FPDE_LDS_POISON)
+        for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = __int_as_float(0x7fc00000);
+}
+#define FPDE_POISON_RING(NAME)                                              \
+    do {                                                                    \
+        if (FPDE_LDS_POISON) {                                              \
+            poison_lds(&NAME##0[0][0], (int)(sizeof(NAME##0) / 4));         \
+            poison_lds(&NAME##1[0][0], (int)(sizeof(NAME##1) / 4));         \
+            poison_lds(&NAME##2[0][0], (int)(sizeof(NAME##2) / 4));         \
+            poison_lds(&NAME##3[0][0], (int)(sizeof(NAME##3) / 4));         \
+        }                                                                   \
+    } while (0)
+
 // Descriptor words must sit in SGPRs.  Their inputs are wave-uniform by
 // construction (kernel arguments and march counters), but after control flow
 // joins the compiler can lose track of that and wrap each load in a
@@ -335,6 +355,8 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
     FPDE_SLOT_RING(float, sF, NF, PS::FSZS);
 
     const int t = threadIdx.x, tx = t % TX, ty = t / TX;
+    FPDE_POISON_RING(sF);
+    if (FPDE_LDS_POISON) __syncthreads();
     const TileCoord tc = tile_coord<TX, TY>(D);
     const int z0 = tc.z0, z1 = tc.z1, L = z1 - z0;
     const int gx = tc.gx0 + tx, gy = (DIM == 3) ? tc.gy0 + ty : 0;
@@ -612,6 +634,9 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     constexpr int kLds = (4 * NF * PS::FSZS + 2 * NR * RLY * RLX) * 4;
 
     const int t = threadIdx.x, tx = t % TX, ty = t / TX;
+    FPDE_POISON_RING(sF);
+    poison_lds(&sR[0][0][0], (int)(sizeof(sR) / 4));
+    if (FPDE_LDS_POISON) __syncthreads();
     const TileCoord tc = tile_coord<TX, TY>(D);
     const int z0 = tc.z0, z1 = tc.z1, L = z1 - z0;
     auto ph = [&](int w) {  // (wrapped into the grid when periodic)
@@ -891,6 +916,8 @@ __global__ __launch_bounds__(TX* TY, FPDE_VJP_MINW) void vjp_kernel(Ptrs P, Dims
     FPDE_SLOT_RING(float, sF, NA, PS::FSZS);
 
     const int t = threadIdx.x, tx = t % TX, ty = t / TX;
+    FPDE_POISON_RING(sF);
+    if (FPDE_LDS_POISON) __syncthreads();
     const TileCoord tc = tile_coord<TX, TY>(D);  // (D.zlo = 0: every plane)
     const int z0 = tc.z0, z1 = tc.z1, L = z1 - z0;
     const int gx = tc.gx0 + tx, gy = (DIM == 3) ? tc.gy0 + ty : 0;
