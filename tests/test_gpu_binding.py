@@ -95,3 +95,38 @@ def test_bound_calls_match_unbound(cfg):
             assert torch.equal(a, b)
     with pytest.raises(ValueError):
         B.bind("nonsense", wl.op, f, c, wl.h, wl.coeffs)
+
+
+def test_calls_on_side_streams_run_concurrently_and_agree():
+    """Every call is queued on the stream it is given: two problems queued on two
+    side streams (default priority) at once give the results of the same calls
+    on the current stream."""
+    import torch  # noqa: PLC0415
+    from paper_2607_18020_amd import binding as B  # noqa: PLC0415
+    wls = [W.make("ns_3d_tgv", seed=45, shape=(30, 40, 130)),
+           W.make("heat_3d", seed=46, shape=(30, 40, 130))]
+    ins = [([torch.from_numpy(x).cuda() for x in wl.fields],
+            [torch.from_numpy(x).cuda() for x in wl.consts]) for wl in wls]
+    ref = []
+    for wl, (f, c) in zip(wls, ins):
+        L = B.fpde_residual_fwd(wl.op, f, c, wl.h, wl.coeffs)
+        g = B.fpde_residual_bwd(wl.op, f, c, wl.h, wl.coeffs, 1.0)
+        B.fpde_bc_correct(wl.op, f, c, wl.h, wl.coeffs, 1.0, grads=g)
+        ref.append((L, g))
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    out = []
+    for s in streams:  # inputs were written on the current stream
+        s.wait_stream(torch.cuda.current_stream())
+    for wl, (f, c), s in zip(wls, ins, streams):
+        with torch.cuda.stream(s):  # (dloss filled on the stream that reads it)
+            dl = torch.ones((), dtype=torch.float64, device="cuda")
+            L = B.fpde_residual_fwd(wl.op, f, c, wl.h, wl.coeffs, stream=s)
+            g = B.fpde_residual_bwd(wl.op, f, c, wl.h, wl.coeffs, dl, stream=s)
+            B.fpde_bc_correct(wl.op, f, c, wl.h, wl.coeffs, dl, grads=g, stream=s)
+        out.append((L, g))
+    torch.cuda.synchronize()
+    for (L0, g0), (L1, g1) in zip(ref, out):
+        assert abs(L1.item() - L0.item()) <= 1e-12 * abs(L0.item())
+        for a, b in zip(g0, g1):
+            assert torch.equal(a, b)
