@@ -6,7 +6,8 @@
 // row segment) and marches a chunk of planes along axis 0.  Each plane region
 // streams from memory straight into a ring of LDS slots, so every input element
 // is read from HBM once per chunk plus the halo; the 7-point star of a node is
-// read from the slots of planes z-1, z, z+1.
+// read from the slots of planes z-1, z, z+1.  (The 2-D forward keeps its rows in
+// a per-lane register queue instead: fwd2_kernel.)
 //
 // Forward: one residual per interior node, sum of squares accumulated in a
 // per-thread float64 register, reduced with DPP across the wavefront and through
@@ -17,12 +18,14 @@
 // that the gather needs are recomputed, never read: at step z the workgroup
 // evaluates R(z+1) on the tile plus a one-node ring into an LDS tile, so the
 // gather for plane z reads R(z) (in-plane star, LDS), R(z+1) and R(z-1) of its
-// own column (registers).  Every node of the visited planes 1..nz-2 is written
-// exactly once (boundary columns included: there the residuals off the residual
-// set are zero, which the LDS tiles already hold); no atomics.
+// own column (registers).  Every node of the visited planes is written exactly
+// once (boundary columns included: there the residuals off the residual set are
+// zero, which the LDS tiles already hold); no atomics.  The planes visited are
+// 1..nz-2, or all of them on a periodic grid and in the one-pass value and
+// gradient (the end planes' terms then come from the same gather).
 //
 // Boundary correction: a 1-D launch over the two end planes of axis 0, the
-// boundary nodes the march does not visit (Sec. 2.3).
+// boundary nodes the three-call backward does not visit (Sec. 2.3).
 //
 // Workgroup-to-tile order is XCD-aware: consecutive workgroup ids are spread
 // round-robin over the 8 XCDs, so the id is remapped such that each XCD gets a
