@@ -71,6 +71,30 @@ def test_parity_normal_inputs_seeds(oracle_mod, op, seed):
     H.assert_parity(wl, R, L, g, Rr, Lr, gr, what=f"op{op} seed{seed}")
 
 
+# degenerate coefficients: inviscid Burgers and NS (nu = 0), Helmholtz at k = 0
+# (the Laplace operator), heat without diffusion (alpha = 0: pointwise), a huge
+# time step (the time term all but vanishes), unequal spacings
+DEGENERATE = [
+    (W.BURGERS_1DT, (33, 130), W.Coeffs(nu=0.0), None),
+    (W.HELMHOLTZ_2D, (33, 130), W.Coeffs(k=0.0), None),
+    (W.HEAT_3D_BE, (9, 20, 70), W.Coeffs(dt=1e-3, alpha=0.0), None),
+    (W.HEAT_3D_BE, (9, 20, 70), W.Coeffs(dt=1e6, alpha=0.1), (0.05, 0.02, 0.01)),
+    (W.NS_2D_STEADY, (33, 130), W.Coeffs(nu=0.0), (0.03, 0.01)),
+    (W.NS_3D_BE, (9, 20, 70), W.Coeffs(nu=0.0, dt=1e-2), (0.1, 0.05, 0.02)),
+    (W.NS_3D_BE, (9, 20, 70), W.Coeffs(nu=0.01, dt=1e6), None),
+]
+
+
+@pytest.mark.parametrize("case", range(len(DEGENERATE)))
+def test_parity_degenerate_coefficients(oracle_mod, case):
+    op, shape, co, h = DEGENERATE[case]
+    wl = W.normal_fields(op, shape, 50 + case, h=h, coeffs=co)
+    print(f"case degenerate op={op} {shape} {co} h={h}", flush=True)
+    R, L, g = H.run_gpu(wl, dloss=1.0)
+    Rr, Lr, gr = oracle_mod.on_workload(wl, dloss=1.0)
+    H.assert_parity(wl, R, L, g, Rr, Lr, gr, what=f"degenerate op{op} {co}")
+
+
 @pytest.mark.parametrize("cfg", ["ns_2d", "ns_3d_tgv", "burgers_1dt"])
 def test_dloss_scaling_and_call_order(oracle_mod, cfg):
     """dloss scales the gradient; bwd and bc write disjoint nodes (either order)."""
