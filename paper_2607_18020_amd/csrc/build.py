@@ -31,7 +31,8 @@ FLAGS = [
 
 
 # The checking library (tests only): LDS filled with NaN before every march, and
-# other tile shapes, chunk lengths and 2-D row widths than the product library,
+# other tile shapes, chunk lengths and 2-D row widths than the product library
+# (and the register-queue forward for heat and 3-D Poisson),
 # so that a read of an LDS location nothing wrote turns into NaN, and so that
 # the gradients can be compared bit for bit across tilings (a gather-form
 # backward evaluates every node the same way whatever tile holds it).
@@ -42,7 +43,7 @@ CHECK_FLAGS = [
     "-DFPDE_NS3_MIN_BWD_BLOCKS=512", "-DFPDE_HEAT_FWD_TX=128", "-DFPDE_HEAT_BWD_TX=128",
     "-DFPDE_HEAT_MIN_BWD_BLOCKS=256", "-DFPDE_VJP_TY3=8", "-DFPDE_VJP_HEAT_TX=64",
     "-DFPDE_TX2=128", "-DFPDE_TX2_FWD=256", "-DFPDE_TX2_VG=256", "-DFPDE_BLOCKS2=512",
-    "-DFPDE_FWD2_Q=4",
+    "-DFPDE_FWD2_Q=4", "-DFPDE_HEAT_FWD_QUEUE=1",
 ]
 
 _NOISE = "is not a recognized feature for this target"

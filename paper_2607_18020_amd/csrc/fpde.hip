@@ -62,10 +62,17 @@ namespace {
 #ifndef FPDE_TX2_FWD
 #define FPDE_TX2_FWD 1024
 #endif
-// 2-D forward register queue: rows held per lane (the centre row, its two
-// neighbours, and Q - 3 rows in flight)
+// register-queue forward: planes held per lane (the centre plane, its two
+// neighbours, and Q - 3 planes in flight)
 #ifndef FPDE_FWD2_Q
 #define FPDE_FWD2_Q 6
+#endif
+// 3-D operators with one stencil field (heat, Poisson) can use the
+// register-queue forward too (five loads per node and plane fit the registers);
+// the LDS march is faster there (heat 256^3: 29 against 32 us), so the product
+// keeps it and the checking build takes the queue, as a second algorithm
+#ifndef FPDE_HEAT_FWD_QUEUE
+#define FPDE_HEAT_FWD_QUEUE 0
 #endif
 // 2-D one-pass value and gradient (the backward with the loss atomics)
 #ifndef FPDE_TX2_VG
@@ -100,22 +107,25 @@ constexpr bool kBwdReverse = FPDE_BWD_REVERSE != 0;
 
 // 3-D grids: forward tile TXF x TYf, backward tile TXB x TYb, explicit-sensitivity
 // backward tile TXV x TYV
-template <int TXF_, int TYF, int TXB_, int TYB, int MINB, int TXV_, int TYV_>
+template <int TXF_, int TYF, int TXB_, int TYB, int MINB, int TXV_, int TYV_, bool QF = false>
 struct Geo3 {
     static constexpr bool D3 = true;
+    static constexpr bool FWD_QUEUE = QF;  // forward: fwdq_kernel (else the LDS march)
     static constexpr int TXF = TXF_, TYf = TYF, TXB = TXB_, TYb = TYB, MIN_BWD_BLOCKS = MINB;
     static constexpr int TXV = TXV_, TYV = TYV_;
 };
 // 2-D grids: one-row tiles of kTX2 nodes for every kernel
 struct Geo2 {
     static constexpr bool D3 = false;
+    static constexpr bool FWD_QUEUE = true;  // (the 2-D forward is always fwdq_kernel)
 };
 // several fields with nonlinear coupling (NS)
 using GeoNS3 = Geo3<FPDE_NS3_FWD_TX, FPDE_NS3_FWD_TY, FPDE_NS3_BWD_TX, FPDE_NS3_BWD_TY,
                     FPDE_NS3_MIN_BWD_BLOCKS, FPDE_VJP_TX3, FPDE_VJP_TY3>;
 // one field, a Laplacian (heat, Poisson)
 using GeoHeat = Geo3<FPDE_HEAT_FWD_TX, FPDE_HEAT_FWD_TY, FPDE_HEAT_BWD_TX, FPDE_HEAT_BWD_TY,
-                     FPDE_HEAT_MIN_BWD_BLOCKS, FPDE_VJP_HEAT_TX, FPDE_VJP_HEAT_TY>;
+                     FPDE_HEAT_MIN_BWD_BLOCKS, FPDE_VJP_HEAT_TX, FPDE_VJP_HEAT_TY,
+                     FPDE_HEAT_FWD_QUEUE != 0>;
 
 template <class OP_, class GEO_>
 struct OpTag {
@@ -320,16 +330,16 @@ int launch_fwd(const Req& r, bool store, double* loss, int zc) {
     return hip_status();
 }
 
-// 2-D forward: the register-queue kernel (no LDS, no barrier)
-template <class OP, int TX>
-int launch_fwd2(const Req& r, bool store, double* loss, int zc) {
-    const Dims dm = tile_dims(r.dims, TX, 1, zc);
+// the register-queue forward (no LDS, no barrier)
+template <class OP, int TX, int TY>
+int launch_fwdq(const Req& r, bool store, double* loss, int zc) {
+    const Dims dm = tile_dims(r.dims, TX, TY, zc);
     hipLaunchKernelGGL(fill_f64_kernel, dim3(1), dim3(1), 0, r.stream, loss, 0.0);
     with_flag(store, [&](auto st) {
         with_flag(dm.per, [&](auto per) {
             hipLaunchKernelGGL(
-                (fwd2_kernel<OP, TX, FPDE_FWD2_Q, decltype(st)::value, decltype(per)::value>),
-                dim3(dm.nblocks), dim3(TX), 0, r.stream, r.P, dm, r.K, r.inv_M, loss);
+                (fwdq_kernel<OP, TX, TY, FPDE_FWD2_Q, decltype(st)::value, decltype(per)::value>),
+                dim3(dm.nblocks), dim3(TX * TY), 0, r.stream, r.P, dm, r.K, r.inv_M, loss);
         });
     });
     return hip_status();
@@ -398,10 +408,12 @@ int run_fwd(const Req& r, bool store, double* loss) {
     return with_op(r.op, [&](auto tag) {
         using OP = typename decltype(tag)::OP;
         using GEO = typename decltype(tag)::GEO;
-        if constexpr (GEO::D3)
+        if constexpr (GEO::D3 && GEO::FWD_QUEUE)
+            return launch_fwdq<OP, GEO::TXF, GEO::TYf>(r, store, loss, zc3<GEO>(r));
+        else if constexpr (GEO::D3)
             return launch_fwd<OP, GEO::TXF, GEO::TYf>(r, store, loss, zc3<GEO>(r));
         else
-            return launch_fwd2<OP, kTX2F>(r, store, loss, zc2(r));
+            return launch_fwdq<OP, kTX2F, 1>(r, store, loss, zc2(r));
     });
 }
 

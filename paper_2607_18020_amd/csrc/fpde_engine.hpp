@@ -6,8 +6,8 @@
 // row segment) and marches a chunk of planes along axis 0.  Each plane region
 // streams from memory straight into a ring of LDS slots, so every input element
 // is read from HBM once per chunk plus the halo; the 7-point star of a node is
-// read from the slots of planes z-1, z, z+1.  (The 2-D forward keeps its rows in
-// a per-lane register queue instead: fwd2_kernel.)
+// read from the slots of planes z-1, z, z+1.  (The register-queue forward,
+// fwdq_kernel, keeps its planes in per-lane registers instead.)
 //
 // Forward: one residual per interior node, sum of squares accumulated in a
 // per-thread float64 register, reduced with DPP across the wavefront and through
@@ -484,70 +484,85 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
 }
 
 // ---------------------------------------------------------------------------
-// Forward on 2-D grids: residuals of one chunk of rows (axis 0) + fused sum of
-// squares, with no LDS and no barrier.  A workgroup owns TX consecutive
-// columns; each lane marches its column down the chunk and keeps, for every
-// field, the values at x - 1, x and x + 1 of Q rows in a register queue, the
-// row evaluated, its two neighbours and Q - 3 rows in flight: a row is loaded
-// Q - 3 steps before it becomes the centre row.  A 2-D row is a few kilobytes,
-// so a march with one barrier per row waits for each row's latency in turn;
-// here each wave keeps several rows of loads in flight on its own.  The x - 1
-// and x + 1 loads fall in the cache lines of the neighbouring lanes' centre
-// loads, so HBM sees each field once.  Rows outside the chunk's stencil and
-// outside the grid are read through empty descriptors (0, no access).
+// Register-queue forward (2-D grids, and 3-D operators with one stencil field):
+// residuals of one chunk of planes + fused sum of squares, with no LDS and no
+// barrier.  A workgroup owns a TX x TY tile of columns (TY = 1 on 2-D grids,
+// where a plane is a row); each lane marches its column down the chunk and
+// keeps, for every field, the centre and in-plane neighbours of its column
+// (x -+ 1, and y -+ 1 on 3-D grids) for Q planes in a register queue: the plane
+// evaluated, its two neighbours and Q - 3 planes in flight, each loaded Q - 3
+// steps before it becomes the centre plane.  Where a plane region is a few
+// kilobytes, a march with one barrier per plane waits for each plane's latency
+// in turn; here each wave keeps several planes of loads in flight on its own.
+// The neighbour loads fall in the cache lines of neighbouring lanes' (x) or
+// waves' (y) centre loads, so HBM sees each field once.  Planes outside the
+// chunk's stencil and outside the grid are read through empty descriptors (0,
+// no access).
 
 template <class F, int... I>
 __device__ __forceinline__ void unroll_seq(F&& f, std::integer_sequence<int, I...>) {
     (f(IC<I>{}), ...);
 }
 
-template <class OP, int TX, int Q, bool STORE_R, bool PER>
-__global__ __launch_bounds__(TX) void fwd2_kernel(Ptrs P, Dims D, KCoef K, double inv_M,
-                                                  double* loss) {
-    constexpr int NF = OP::NF, NC = OP::NC, NR = OP::NR, NC1 = NC > 0 ? NC : 1;
-    static_assert(OP::DIM == 2, "2-D grids only");
-    static_assert(Q >= 4, "rows z - 1, z, z + 1 and at least one row in flight");
-    constexpr uint32_t kOff = 0x80000000u;  // past every row's range: reads 0
-    const int t = threadIdx.x;
-    const TileCoord tc = tile_coord<TX, 1>(D);
+template <class OP, int TX, int TY, int Q, bool STORE_R, bool PER>
+__global__ __launch_bounds__(TX* TY) void fwdq_kernel(Ptrs P, Dims D, KCoef K, double inv_M,
+                                                      double* loss) {
+    constexpr int DIM = OP::DIM, NF = OP::NF, NC = OP::NC, NR = OP::NR, NT = TX * TY;
+    constexpr int NC1 = NC > 0 ? NC : 1;
+    constexpr int NV = 2 * DIM - 1;  // centre, x -+ 1 [, y -+ 1]
+    static_assert(DIM == 3 || TY == 1, "2-D grids use one-row tiles");
+    static_assert(Q >= 4, "planes z - 1, z, z + 1 and at least one plane in flight");
+    constexpr uint32_t kOff = 0x80000000u;  // past every plane's range: reads 0
+    const int t = threadIdx.x, tx = t % TX, ty = t / TX;
+    const TileCoord tc = tile_coord<TX, TY>(D);
     const int z0 = tc.z0, z1 = tc.z1, L = z1 - z0;
-    const int gx = tc.gx0 + t;
-    const uint32_t pbytes = (uint32_t)D.nx * 4u;
-    const bool inarr = gx < D.nx;
-    const bool interior = PER ? inarr : gx >= 1 && gx <= D.nx - 2;
-    // byte offsets of x - 1, x, x + 1 within a row
-    const uint32_t oc = inarr ? (uint32_t)gx * 4u : kOff;
-    uint32_t om, op;
-    if (PER) {
-        om = inarr ? (uint32_t)wrap_idx(gx - 1, D.nx) * 4u : kOff;
-        op = inarr ? (uint32_t)wrap_idx(gx + 1, D.nx) * 4u : kOff;
-    } else {
-        om = inarr && gx >= 1 ? (uint32_t)(gx - 1) * 4u : kOff;
-        op = gx + 1 < D.nx ? (uint32_t)(gx + 1) * 4u : kOff;
+    const int gx = tc.gx0 + tx, gy = (DIM == 3) ? tc.gy0 + ty : 0;
+    const uint32_t pbytes = (uint32_t)D.ny * (uint32_t)D.nx * 4u;
+    const bool inarr = gx < D.nx && gy < D.ny;
+    const bool interior =
+        PER ? inarr : gx >= 1 && gx <= D.nx - 2 && (DIM == 2 || (gy >= 1 && gy <= D.ny - 2));
+    // byte offsets of the centre and in-plane neighbours within a plane
+    auto at = [&](int y, int x) -> uint32_t {
+        if (!inarr) return kOff;
+        if (PER) {
+            x = wrap_idx(x, D.nx);
+            y = wrap_idx(y, D.ny);
+        } else if (x < 0 || x >= D.nx || y < 0 || y >= D.ny) {
+            return kOff;
+        }
+        return (uint32_t)(y * D.nx + x) * 4u;
+    };
+    uint32_t off[NV];
+    off[0] = at(gy, gx);
+    off[1] = at(gy, gx - 1);
+    off[2] = at(gy, gx + 1);
+    if constexpr (DIM == 3) {
+        off[3] = at(gy - 1, gx);
+        off[4] = at(gy + 1, gx);
     }
 
-    // the queue: row z0 - 1 + k lives in slot k % Q
-    float qc[Q][NF], qm[Q][NF], qp[Q][NF], qk[Q][NC1];
-    auto load_row = [&](int z, auto slot) __attribute__((always_inline)) {  // z uniform
+    // the queue: plane z0 - 1 + k lives in slot k % Q
+    float qv[Q][NF][NV], qk[Q][NC1];
+    auto load_plane = [&](int z, auto slot) __attribute__((always_inline)) {  // z uniform
         constexpr int S_ = decltype(slot)::value;
-        // the rows the chunk's residuals read: z0 - 1 .. z1
+        // the planes the chunk's residuals read: z0 - 1 .. z1
         const bool ok = z >= z0 - 1 && z <= z1 && (PER || (z >= 0 && z < D.nz));
         const int zr = PER ? wrap_idx(z, D.nz) : z;
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
             const __amdgpu_buffer_rsrc_t r = plane_rsrc_if(P.f[f], zr, pbytes, ok);
-            qc[S_][f] = bld(r, oc);
-            qm[S_][f] = bld(r, om);
-            qp[S_][f] = bld(r, op);
+#pragma unroll
+            for (int v = 0; v < NV; ++v) qv[S_][f][v] = bld(r, off[v]);
         }
 #pragma unroll
-        for (int j = 0; j < NC; ++j) qk[S_][j] = bld(plane_rsrc_if(P.c[j], zr, pbytes, ok), oc);
+        for (int j = 0; j < NC; ++j)
+            qk[S_][j] = bld(plane_rsrc_if(P.c[j], zr, pbytes, ok), off[0]);
     };
 
-    // the end rows of axis 0 hold no residual node: the first and the last chunk
+    // the end planes of axis 0 hold no residual node: the first and the last chunk
     // write their zeros (every column, so that no cache line of R is stored in part)
     if (STORE_R && !PER) {
-        const uint32_t so = inarr ? oc : kDropOff;
+        const uint32_t so = inarr ? off[0] : kDropOff;
 #pragma unroll
         for (int b = 0; b < NR; ++b) {
             if (z0 == 1) bst<kStream>(plane_rsrc(P.out[b], 0, pbytes), so, 0.f);
@@ -556,23 +571,27 @@ __global__ __launch_bounds__(TX) void fwd2_kernel(Ptrs P, Dims D, KCoef K, doubl
     }
 
     unroll_seq([&](auto k) __attribute__((always_inline)) {
-        load_row(z0 - 1 + decltype(k)::value, k);
+        load_plane(z0 - 1 + decltype(k)::value, k);
     }, std::make_integer_sequence<int, Q - 1>{});
 
     double acc = 0.0;
     auto step = [&](auto jc, int w) __attribute__((always_inline)) {
         constexpr int J = decltype(jc)::value;  // w % Q
         constexpr int SM = J % Q, SC = (J + 1) % Q, SP = (J + 2) % Q, SN = (J + Q - 1) % Q;
-        // row z + Q - 2 goes to the slot of row z - 2, read last in the previous step
-        load_row(z0 + w + Q - 2, IC<SN>{});
+        // plane z + Q - 2 goes to the slot of plane z - 2, read last in the previous step
+        load_plane(z0 + w + Q - 2, IC<SN>{});
         Star st[NF];
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
-            st[f].c = qc[SC][f];
-            st[f].m[0] = qc[SM][f];
-            st[f].p[0] = qc[SP][f];
-            st[f].m[1] = qm[SC][f];
-            st[f].p[1] = qp[SC][f];
+            st[f].c = qv[SC][f][0];
+            st[f].m[0] = qv[SM][f][0];
+            st[f].p[0] = qv[SP][f][0];
+            st[f].m[DIM - 1] = qv[SC][f][1];
+            st[f].p[DIM - 1] = qv[SC][f][2];
+            if constexpr (DIM == 3) {
+                st[f].m[1] = qv[SC][f][3];
+                st[f].p[1] = qv[SC][f][4];
+            }
         }
         float R[NR];
         OP::residual(st, qk[SC], K, R);
@@ -580,8 +599,8 @@ __global__ __launch_bounds__(TX) void fwd2_kernel(Ptrs P, Dims D, KCoef K, doubl
 #pragma unroll
         for (int b = 0; b < NR; ++b) ss = fmaf(R[b], R[b], ss);
         acc += (double)(interior ? ss : 0.f);
-        if (STORE_R) {  // every node of the row: R on the residual set, 0 off it
-            const uint32_t so = inarr ? oc : kDropOff;
+        if (STORE_R) {  // every node of the plane: R on the residual set, 0 off it
+            const uint32_t so = inarr ? off[0] : kDropOff;
             const int z = PER ? wrap_idx(z0 + w, D.nz) : z0 + w;
 #pragma unroll
             for (int b = 0; b < NR; ++b)
@@ -597,7 +616,7 @@ __global__ __launch_bounds__(TX) void fwd2_kernel(Ptrs P, Dims D, KCoef K, doubl
     unroll_seq([&](auto j) __attribute__((always_inline)) {
         if (w + decltype(j)::value < L) step(j, w + decltype(j)::value);
     }, std::make_integer_sequence<int, Q - 1>{});
-    block_atomic_sum<TX>(acc * inv_M, loss);
+    block_atomic_sum<NT>(acc * inv_M, loss);
 }
 
 // ---------------------------------------------------------------------------

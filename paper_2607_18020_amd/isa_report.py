@@ -26,7 +26,7 @@ from typing import Dict, List
 
 from paper_2607_18020_amd.csrc import build as B
 
-KERNEL_PREFIXES = ("fwd_kernel", "fwd2_kernel", "bwd_kernel", "vjp_kernel", "bc_kernel",
+KERNEL_PREFIXES = ("fwd_kernel", "fwdq_kernel", "bwd_kernel", "vjp_kernel", "bc_kernel",
                    "fill_f64_kernel")
 
 
@@ -125,7 +125,7 @@ def _template_args(name: str) -> List[str]:
 def reduces_loss(name: str) -> bool:
     """The kernels that add a float64 partial loss per workgroup: every forward,
     and the backward with its LOSS flag (bwd_kernel<OP, TX, TY, REV, LOSS, PER>)."""
-    if name.startswith(("fwd_kernel", "fwd2_kernel")):
+    if name.startswith(("fwd_kernel", "fwdq_kernel")):
         return True
     return name.startswith("bwd_kernel") and _template_args(name)[4] == "true"
 

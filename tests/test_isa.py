@@ -45,6 +45,6 @@ def test_ns3d_kernels(kernels):
 
 
 def test_2d_forward_has_no_lds_march(kernels):
-    k = kernels["fwd2_kernel<OpNS<2, false>, 1024, 6, false, false>"]
+    k = kernels["fwdq_kernel<OpNS<2, false>, 1024, 1, 6, false, false>"]
     assert k["lds_dma"] == 0 and k["atomic"] == 1 and k["dpp"] >= 6
     assert k["barrier"] <= 2  # only the workgroup sum of the loss
