@@ -146,6 +146,9 @@ def test_validation_status_codes(B, fn):
     assert _call(B, fn, op3, (3, 1 << 15, 1 << 14)) == SHAPE
     assert _call(B, fn, op2, (3, 1 << 29)) == SHAPE
     assert _call(B, fn, op2, (1 << 31, 5)) == SHAPE
+    # every launch shape stays below 2^31 workgroups (so the node count below 2^36)
+    assert _call(B, fn, op2, (1 << 26, 1 << 10)) == SHAPE
+    assert _call(B, fn, op3, (1 << 20, 1 << 10, 1 << 10)) == SHAPE
 
 
 def test_output_checks(B):
