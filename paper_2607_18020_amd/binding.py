@@ -143,6 +143,15 @@ def _stream(stream) -> int:
     return s.cuda_stream
 
 
+def _used_on(stream, *tensors):
+    """Tensors allocated here (on the current stream) and read or written by a
+    call queued on another stream: tell the caching allocator, so that their
+    memory is not handed out again before that stream has run the call."""
+    if stream is not None and stream != torch.cuda.current_stream():
+        for t in tensors:
+            t.record_stream(stream)
+
+
 def fpde_residual_fwd(op: int, fields, consts, h, coeffs, *, residual_out=None,
                       loss: Optional[torch.Tensor] = None, bc_mode: int = 0, stream=None):
     """Queue the fused forward stencil + loss; returns the float64 loss tensor."""
@@ -151,6 +160,7 @@ def fpde_residual_fwd(op: int, fields, consts, h, coeffs, *, residual_out=None,
     dev = fields[0].device
     if loss is None:
         loss = torch.empty((), dtype=torch.float64, device=dev)
+        _used_on(stream, loss)
     if loss.dtype != torch.float64 or loss.device != dev or loss.numel() != 1:
         raise ValueError("fpde_residual_fwd: loss must be a one-element float64 tensor on the "
                          "fields' device")
@@ -172,9 +182,11 @@ def _grad_call(fn, name, op, fields, consts, h, coeffs, dloss, grads, bc_mode, s
     _check_tensors(list(fields) + list(consts), shape, name)
     if grads is None:
         grads = [torch.empty_like(f) for f in fields]
+        _used_on(stream, *grads)
     _check_tensors(grads, shape, name + " grads")
     if not isinstance(dloss, torch.Tensor):
         dloss = torch.tensor(float(dloss), dtype=torch.float64, device=fields[0].device)
+        _used_on(stream, dloss)
     if dloss.dtype != torch.float64 or dloss.device != fields[0].device or dloss.numel() != 1:
         raise ValueError(f"{name}: dloss must be a one-element float64 tensor on the fields' device")
     g, c = make_grid(shape, h, bc_mode), make_coeffs(coeffs)
@@ -207,6 +219,7 @@ def fpde_residual_value_and_grad(op: int, fields, consts, h, coeffs, dloss=1.0, 
     (loss, grads): the float64 loss L and dloss * dL/dq for every field."""
     if loss is None:
         loss = torch.empty((), dtype=torch.float64, device=fields[0].device)
+        _used_on(stream, loss)
     if loss.dtype != torch.float64 or loss.device != fields[0].device or loss.numel() != 1:
         raise ValueError("fpde_residual_value_and_grad: loss must be a one-element float64 "
                          "tensor on the fields' device")
@@ -230,6 +243,7 @@ def fpde_residual_vjp(op: int, fields, h, coeffs, sens, *, grads=None, accumulat
         if accumulate:
             raise ValueError("fpde_residual_vjp: accumulate needs grads")
         grads = [torch.empty_like(f) for f in fields]
+        _used_on(stream, *grads)
     _check_tensors(grads, shape, "fpde_residual_vjp grads")
     g, c = make_grid(shape, h, bc_mode), make_coeffs(coeffs)
     st = _load().fpde_residual_vjp(int(op), ctypes.byref(g), ctypes.byref(c), _ptr_array(fields),
@@ -281,6 +295,7 @@ def bind(entry: str, op: int, fields, consts, h, coeffs, *, dloss=None, grads=No
     if entry in ("fwd", "value_and_grad"):
         if loss is None:
             loss = torch.empty((), dtype=torch.float64, device=dev)
+            _used_on(stream, loss)
         if loss.dtype != torch.float64 or loss.device != dev or loss.numel() != 1:
             raise ValueError(f"bind {entry}: loss must be a one-element float64 tensor on the "
                              "fields' device")
@@ -295,6 +310,7 @@ def bind(entry: str, op: int, fields, consts, h, coeffs, *, dloss=None, grads=No
         return BoundCall("fpde_residual_fwd", lib.fpde_residual_fwd, args, keep, loss)
     if grads is None:
         grads = [torch.empty_like(f) for f in fields]
+        _used_on(stream, *grads)
     _check_tensors(grads, shape, f"bind {entry} grads")
     ga = _ptr_array(grads)
     keep += [ga, list(grads)]
@@ -307,6 +323,7 @@ def bind(entry: str, op: int, fields, consts, h, coeffs, *, dloss=None, grads=No
     if not isinstance(dloss, torch.Tensor):
         dloss = torch.tensor(1.0 if dloss is None else float(dloss), dtype=torch.float64,
                              device=dev)
+        _used_on(stream, dloss)
     if dloss.dtype != torch.float64 or dloss.device != dev or dloss.numel() != 1:
         raise ValueError(f"bind {entry}: dloss must be a one-element float64 tensor on the "
                          "fields' device")

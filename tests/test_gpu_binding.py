@@ -130,3 +130,37 @@ def test_calls_on_side_streams_run_concurrently_and_agree():
         assert abs(L1.item() - L0.item()) <= 1e-12 * abs(L0.item())
         for a, b in zip(g0, g1):
             assert torch.equal(a, b)
+
+
+def test_side_stream_calls_keep_the_buffers_they_allocate():
+    """The dloss scalar made from a Python float, and the loss and grads that the
+    binding allocates for a call queued on another stream, stay reserved for that
+    stream until it has run the call: new tensors filled on the current stream
+    while the side stream is still busy do not take their memory."""
+    import torch  # noqa: PLC0415
+    from paper_2607_18020_amd import binding as B  # noqa: PLC0415
+    wl = W.make("ns_3d_tgv", seed=47, shape=(20, 30, 70))
+    f = [torch.from_numpy(x).cuda() for x in wl.fields]
+    c = [torch.from_numpy(x).cuda() for x in wl.consts]
+    dl = torch.full((), 0.5, dtype=torch.float64, device="cuda")
+    L0 = B.fpde_residual_fwd(wl.op, f, c, wl.h, wl.coeffs)
+    g0 = B.fpde_residual_bwd(wl.op, f, c, wl.h, wl.coeffs, dl)
+    B.fpde_bc_correct(wl.op, f, c, wl.h, wl.coeffs, dl, grads=g0)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):  # keep the side stream busy for a while
+        busy = torch.empty(1 << 26, device="cuda")
+        for _ in range(4):
+            busy.fill_(1.0)
+    # queued on s from the current stream's context
+    L1 = B.fpde_residual_fwd(wl.op, f, c, wl.h, wl.coeffs, stream=s)
+    g1 = B.fpde_residual_bwd(wl.op, f, c, wl.h, wl.coeffs, 0.5, stream=s)
+    B.fpde_bc_correct(wl.op, f, c, wl.h, wl.coeffs, 0.5, grads=g1, stream=s)
+    junk = [torch.full((), 1e30, dtype=torch.float64, device="cuda") for _ in range(64)]
+    junk += [torch.full_like(f[0], 1e30) for _ in range(4)]
+    torch.cuda.synchronize()
+    del busy, junk
+    assert abs(L1.item() - L0.item()) <= 1e-12 * abs(L0.item())
+    for a, b in zip(g0, g1):
+        assert torch.equal(a, b)
