@@ -13,8 +13,10 @@ Byte model (each input read once per pass, each output written once):
   (2 (NF + NC) + NF) * 4 bytes per grid node (72 B/node for the 3D NS case).
 
 Beside the warm figure (steps back to back, as a training loop calls the
-operator), "flushed" times steps one by one after writing 512 MB between them,
-so that every input comes from HBM rather than the 256 MB memory-side cache.
+operator), "flushed" times steps one by one after reading 512 MB between them,
+so that every input comes from HBM rather than the 256 MB memory-side cache;
+"flushed_dirty" writes the 512 MB instead, so that the step also pays for
+writing back the dirty lines that the write leaves in the caches.
 
 --path fused times fpde_residual_value_and_grad, the same loss and gradient
 from one read of the inputs ((2 NF + NC) * 4 B/node: 44 for the 3D NS case).
@@ -59,9 +61,9 @@ def parse():
     p.add_argument("--sample-every", type=int, default=10,
                    help="per-kernel HIP events on every n-th timed step (the others carry none)")
     p.add_argument("--flushed-steps", type=int, default=20,
-                   help="after the timed region, steps timed one by one with 512 MB written "
-                        "between them (outside the events), so that no input is left in the "
-                        "caches; reported beside the warm figure (0: skip)")
+                   help="after the timed region, steps timed one by one with 512 MB read "
+                        "(then written) between them (outside the events), so that no input is "
+                        "left in the caches; reported beside the warm figure (0: skip)")
     return p.parse_args()
 
 
@@ -92,16 +94,23 @@ def byte_model(wl, bc_mode=0, path="loss"):
     }
 
 
-def flushed_steps(torch, step, stream, n, flush_bytes=512 << 20):
-    """Each of n steps timed alone (events on the step's stream) after a 512 MB
-    write that evicts the 256 MB memory-side cache and L2, the write outside
-    the events: the step's inputs then come from HBM.  Median and quartiles of
-    the per-step milliseconds."""
+def flushed_steps(torch, step, stream, n, flush_bytes=512 << 20, dirty=False):
+    """Each of n steps timed alone (events on the step's stream) after a sweep
+    over 512 MB that evicts the 256 MB memory-side cache and L2, the sweep
+    outside the events: the step's inputs then come from HBM.  The sweep reads
+    the buffer (the caches then hold clean lines), or with dirty=True writes it
+    (the caches then hold dirty lines, written back while the step runs).
+    Median and quartiles of the per-step milliseconds."""
     import statistics  # noqa: PLC0415
     buf = torch.empty(flush_bytes // 4, dtype=torch.float32, device="cuda")
+    buf.fill_(1.0)
     ms = []
     for i in range(n):
-        buf.fill_(float(i))
+        with torch.cuda.stream(stream):
+            if dirty:
+                buf.fill_(float(i))
+            else:
+                torch.sum(buf)
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record(stream)
         step()
@@ -111,7 +120,8 @@ def flushed_steps(torch, step, stream, n, flush_bytes=512 << 20):
     del buf
     q = statistics.quantiles(ms, n=4) if len(ms) > 1 else [ms[0]] * 3
     return {"steps": n, "ms_per_step_median": round(q[1], 4), "ms_q1": round(q[0], 4),
-            "ms_q3": round(q[2], 4), "flush_bytes": flush_bytes}
+            "ms_q3": round(q[2], 4), "flush_bytes": flush_bytes,
+            "flush": "write" if dirty else "read"}
 
 
 def copy_gbps(torch, nbytes=1 << 30, reps=20):
@@ -304,10 +314,12 @@ def main():
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                 "traffic": measured_traffic(cfg, wl.op, TRAFFIC_KERNELS.get(dom, (dom,)), args.path),
                 "algorithmic_bytes_per_launch": bm[dom], "avg_launch_us": round(per[dom], 2)}
-    flushed = None
+    flushed = flushed_dirty = None
     if args.flushed_steps > 0:
         flushed = flushed_steps(torch, step, stream, args.flushed_steps)
         flushed["grid_points_per_s"] = N / (flushed["ms_per_step_median"] * 1e-3)
+        flushed_dirty = flushed_steps(torch, step, stream, args.flushed_steps, dirty=True)
+        flushed_dirty["grid_points_per_s"] = N / (flushed_dirty["ms_per_step_median"] * 1e-3)
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(W, wl, cfg, args.seed, args.cpu_planes, bcm, args.path)
@@ -340,6 +352,7 @@ def main():
         "kernel_us_sampled_steps": len(sampled),
         "copy_gbps": round(copy_gbps(torch), 1),
         "flushed": flushed,
+        "flushed_dirty": flushed_dirty,
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
