@@ -85,7 +85,7 @@ typedef enum fpde_status {
     FPDE_ERR_COEFF = -4,       /* non-finite coefficient, or dt <= 0 for a time-stepping op */
     FPDE_ERR_ALIGN = -5,       /* a device pointer not 4-byte aligned */
     FPDE_ERR_HIP = -6,         /* the HIP runtime reported an error while queueing */
-    FPDE_ERR_UNSUPPORTED = -7  /* valid request this build does not implement (none at present) */
+    FPDE_ERR_UNSUPPORTED = -7  /* valid request this library version does not implement (none at present) */
 } fpde_status;
 
 typedef enum fpde_op {

@@ -569,7 +569,7 @@ extern "C" const char* fpde_status_string(int status) {
     case FPDE_ERR_COEFF: return "FPDE_ERR_COEFF: non-finite coefficient or dt <= 0";
     case FPDE_ERR_ALIGN: return "FPDE_ERR_ALIGN: misaligned device pointer";
     case FPDE_ERR_HIP: return "FPDE_ERR_HIP: HIP runtime error while queueing work";
-    case FPDE_ERR_UNSUPPORTED: return "FPDE_ERR_UNSUPPORTED: request not implemented by this build";
+    case FPDE_ERR_UNSUPPORTED: return "FPDE_ERR_UNSUPPORTED: request not implemented by this library version";
     default: return "unknown fpde status";
     }
 }
