@@ -46,7 +46,10 @@ def parse():
     p = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=100)
-    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=None,
+                   help="untimed warm-up steps (default: as many as take 0.5 s of GPU time, "
+                        "at least 50: under sustained load the GPU needs ~0.1 s to reach its "
+                        "steady clocks, and 20 steps of a 0.24 ms step read ~7%% slow)")
     p.add_argument("--config", default="ns_3d_tgv")
     p.add_argument("--seed", type=int, default=42)
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -271,8 +274,17 @@ def main():
         for _, fn in kernels:
             fn()
 
-    for _ in range(args.warmup):
-        step()
+    if args.warmup is not None:
+        for _ in range(args.warmup):
+            step()
+        warmup = args.warmup
+    else:  # steps in batches of 50 until 0.5 s of them have run
+        warmup, t0 = 0, time.perf_counter()
+        while warmup < 50 or time.perf_counter() - t0 < 0.5:
+            for _ in range(50):
+                step()
+            warmup += 50
+            torch.cuda.synchronize()
     torch.cuda.synchronize()
 
     # Timed region: K steps between two events.  A timestamp between two kernels
@@ -329,7 +341,7 @@ def main():
         "unit": "grid-points/s",
         "n_gpus": 1,
         "steps": K,
-        "warmup": args.warmup,
+        "warmup": warmup,
         "ms_per_step": ms,
         "higher_is_better": True,
         "scaling": "weak",
