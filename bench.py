@@ -47,9 +47,9 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=100)
     p.add_argument("--warmup", type=int, default=None,
-                   help="untimed warm-up steps (default: as many as take 0.5 s of GPU time, "
-                        "at least 50: under sustained load the GPU needs ~0.1 s to reach its "
-                        "steady clocks, and 20 steps of a 0.24 ms step read ~7%% slow)")
+                   help="untimed warm-up steps (default: as many as take 0.5 s, at least 50: "
+                        "a step back to back with others settles only after ~150 steps; after "
+                        "20, the timed NS-3D steps read ~6%% slow)")
     p.add_argument("--config", default="ns_3d_tgv")
     p.add_argument("--seed", type=int, default=42)
     p.add_argument("--no-cpu-baseline", action="store_true")
