@@ -3,6 +3,7 @@ ABI cannot take are refused before any call, with ValueError; ABI status codes
 come back as FpdeError."""
 from __future__ import annotations
 
+import numpy as np
 import pytest
 
 from paper_2607_18020_amd import workloads as W
@@ -164,3 +165,58 @@ def test_side_stream_calls_keep_the_buffers_they_allocate():
     assert abs(L1.item() - L0.item()) <= 1e-12 * abs(L0.item())
     for a, b in zip(g0, g1):
         assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("cfg", ["ns_3d_tgv", "ns_2d", "heat_3d"])
+def test_arrays_at_any_4_byte_offset(cfg):
+    """The ABI asks only for 4-byte-aligned arrays: inputs, outputs and the
+    sensitivities placed 4, 8 and 12 bytes past a 256-byte boundary (views into
+    larger buffers) give bitwise the results of freshly allocated arrays, for
+    every entry point."""
+    import torch  # noqa: PLC0415
+    from paper_2607_18020_amd import binding as B  # noqa: PLC0415
+    shape = (11, 20, 133) if len(W.CONFIGS[cfg].shape) == 3 else (37, 300)
+    wl = W.make(cfg, seed=48, shape=shape)
+    n = int(np.prod(shape))
+    nf = len(wl.fields)
+    nr = len(wl.spec.residuals)
+    sens_np = W.sensitivities(wl.op, shape, 49)
+
+    def placed(k, src=None):
+        buf = torch.empty(n + 64, dtype=torch.float32, device="cuda")
+        v = buf[k:k + n].view(shape)
+        if src is not None:
+            v.copy_(torch.from_numpy(src))
+        return buf, v
+
+    def run(off):
+        keep = []
+        def arr(src=None):
+            if off is None:
+                return torch.from_numpy(src).cuda() if src is not None else \
+                    torch.empty(shape, dtype=torch.float32, device="cuda")
+            b, v = placed(off, src)
+            keep.append(b)
+            return v
+        f = [arr(x) for x in wl.fields]
+        c = [arr(x) for x in wl.consts]
+        R = [arr() for _ in range(nr)]
+        L = B.fpde_residual_fwd(wl.op, f, c, wl.h, wl.coeffs, residual_out=R)
+        g = [arr() for _ in range(nf)]
+        B.fpde_residual_bwd(wl.op, f, c, wl.h, wl.coeffs, 1.0, grads=g)
+        B.fpde_bc_correct(wl.op, f, c, wl.h, wl.coeffs, 1.0, grads=g)
+        gv = [arr() for _ in range(nf)]
+        Lv, _ = B.fpde_residual_value_and_grad(wl.op, f, c, wl.h, wl.coeffs, 1.0, grads=gv)
+        s = [arr(x) for x in sens_np]
+        gs = [arr() for _ in range(nf)]
+        B.fpde_residual_vjp(wl.op, f, wl.h, wl.coeffs, s, grads=gs)
+        torch.cuda.synchronize()
+        out = [x.cpu() for x in R + g + gv + gs]
+        return out, L.item(), Lv.item()
+
+    ref, L0, Lv0 = run(None)
+    for off in (1, 2, 3):
+        print(f"case {cfg} {shape} arrays at +{4 * off} bytes", flush=True)
+        out, L, Lv = run(off)
+        assert all(torch.equal(a, b) for a, b in zip(ref, out))
+        assert abs(L - L0) <= 1e-12 * abs(L0) and abs(Lv - Lv0) <= 1e-12 * abs(Lv0)
