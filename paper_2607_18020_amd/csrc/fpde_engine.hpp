@@ -42,9 +42,9 @@
 #include "fpde_ops.hpp"
 
 // Minimum waves per SIMD requested from the compiler for the marching kernels
-// (bounds their VGPR budget; 1 leaves the compiler free).
-// minimum waves per SIMD (the second launch bound): 4 lets two 8-wave forward
-// workgroups share a CU, with at most 128 VGPRs each
+// (the second launch bound, which caps their VGPRs; 1 leaves the compiler free).
+// The forward asks for 4, so that two 8-wave workgroups share a CU with at most
+// 128 VGPRs each.
 #ifndef FPDE_FWD_MINW
 #define FPDE_FWD_MINW 4
 #endif
@@ -334,9 +334,10 @@ struct PlaneStream {
 // (tile rows plus one row above and below, and the side-edge x-neighbours)
 // streams from memory straight into a 4-slot LDS ring; the 7-point star of
 // every field is read from the slots of planes z-1, z, z+1.  One barrier per
-// step: plane z+2 streams into the slot of plane z-2 while plane z is evaluated.  The sum of squares is accumulated per thread in
-// float64, reduced with DPP across the wavefront and through LDS across waves,
-// then added with ONE float64 atomic per workgroup.
+// step: plane z+2 streams into the slot of plane z-2 while plane z is
+// evaluated.  The sum of squares is accumulated per thread in float64, reduced
+// with DPP across the wavefront and through LDS across waves, then added with
+// ONE float64 atomic per workgroup.
 
 template <class OP, int TX, int TY, bool STORE_R, bool PER>
 __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims D, KCoef K,
