@@ -12,8 +12,10 @@ Byte model (each input read once per pass, each output written once):
   them again and write one gradient per field, so one step moves
   (2 (NF + NC) + NF) * 4 bytes per grid node (72 B/node for the 3D NS case).
 
-Beside the warm figure (steps back to back, as a training loop calls the
-operator), "flushed" times steps one by one after reading 512 MB between them,
+The reported figure is the first of --runs runs of K back-to-back steps;
+"runs" gives the median and quartiles over all of them (the paper's protocol
+takes the median of five).  Beside the warm figure (steps back to back, as a
+training loop calls the operator), "flushed" times steps one by one after reading 512 MB between them,
 so that every input comes from HBM rather than the 256 MB memory-side cache;
 "flushed_dirty" writes the 512 MB instead, so that the step also pays for
 writing back the dirty lines that the write leaves in the caches.
@@ -63,6 +65,9 @@ def parse():
                         "and gradient")
     p.add_argument("--sample-every", type=int, default=10,
                    help="per-kernel HIP events on every n-th timed step (the others carry none)")
+    p.add_argument("--runs", type=int, default=5,
+                   help="the K timed steps are the first of this many runs of K steps; the "
+                        "line adds the median and quartiles of ms per step over the runs")
     p.add_argument("--flushed-steps", type=int, default=20,
                    help="after the timed region, steps timed one by one with 512 MB read "
                         "(then written) between them (outside the events), so that no input is "
@@ -326,6 +331,22 @@ def main():
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                 "traffic": measured_traffic(cfg, wl.op, TRAFFIC_KERNELS.get(dom, (dom,)), args.path),
                 "algorithmic_bytes_per_launch": bm[dom], "avg_launch_us": round(per[dom], 2)}
+    # the same K steps timed again (no per-kernel events), for a median and
+    # quartiles over runs beside the one figure the line reports
+    run_ms = [ms]
+    for _ in range(max(0, args.runs - 1)):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(K):
+            step()
+        b.record(stream)
+        b.synchronize()
+        run_ms.append(a.elapsed_time(b) / K)
+    import statistics  # noqa: PLC0415
+    q = statistics.quantiles(run_ms, n=4) if len(run_ms) > 1 else [ms] * 3
+    runs = {"n": len(run_ms), "ms_per_step_median": round(q[1], 5), "ms_q1": round(q[0], 5),
+            "ms_q3": round(q[2], 5), "ms_per_step": [round(x, 5) for x in run_ms]}
     flushed = flushed_dirty = None
     if args.flushed_steps > 0:
         flushed = flushed_steps(torch, step, stream, args.flushed_steps)
@@ -363,6 +384,7 @@ def main():
         "kernel_us": {k: round(v, 2) for k, v in per.items()},
         "kernel_us_sampled_steps": len(sampled),
         "copy_gbps": round(copy_gbps(torch), 1),
+        "runs": runs,
         "flushed": flushed,
         "flushed_dirty": flushed_dirty,
         "roofline": roofline,
