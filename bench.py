@@ -138,9 +138,11 @@ def copy_gbps(torch, nbytes=1 << 30, reps=20):
     counters for the traffic figure."""
     src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
     dst = torch.empty_like(src)
-    for _ in range(3):
-        torch.mul(src, 1.0, out=dst)
-    torch.cuda.synchronize()
+    t0 = time.perf_counter()  # warm up for 0.25 s, as the steps do (after idle host work)
+    while time.perf_counter() - t0 < 0.25:
+        for _ in range(10):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     a.record()
     for _ in range(reps):
