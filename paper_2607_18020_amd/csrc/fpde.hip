@@ -370,9 +370,9 @@ int zc2(const Req& r) { return chunk_planes(r.dims, kTX2, 1, kTargetBlocks2); }
 
 template <class OP>
 int launch_bc(const Req& r, const double* dloss) {
-    const long long nodes = 2LL * r.dims.ny * r.dims.nx;  // the two end planes of axis 0
-    long long nb = (nodes + 255) / 256;
-    if (nb > 65535LL * 16) nb = 65535LL * 16;
+    // the two end planes of axis 0: one workgroup per 256-node segment of each row
+    // (fewer than 2^31 of them: the node count of a plane is below 2^29)
+    const long long nb = 2LL * r.dims.ny * ((r.dims.nx + 255) / 256);
     hipLaunchKernelGGL((bc_kernel<OP>), dim3((unsigned)nb), dim3(256), 0, r.stream, r.P, r.dims,
                        r.K, dloss, r.two_over_M);
     return hip_status();

@@ -1067,59 +1067,56 @@ __global__ __launch_bounds__(TX* TY, FPDE_VJP_MINW) void vjp_kernel(Ptrs P, Dims
 // residuals taken as zero off the residual set, which is exactly their
 // correction term.)
 
-template <class OP>
-__device__ __forceinline__ void bc_node0(const Ptrs& P, const KCoef& K, const long long* str,
-                                         long long node, bool low, float* g) {
-    constexpr int DIM = OP::DIM, NF = OP::NF, NC = OP::NC;
-    const float t = low ? -1.f : 1.f;  // node = m + t e_0
-    const long long m = low ? node + str[0] : node - str[0];
-    Star s[NF];
-#pragma unroll
-    for (int f = 0; f < NF; ++f) {
-        const float* q = P.f[f];
-        s[f].c = q[m];
-#pragma unroll
-        for (int a = 0; a < DIM; ++a) {
-            s[f].m[a] = q[m - str[a]];
-            s[f].p[a] = q[m + str[a]];
-        }
-    }
-    float cc[NC > 0 ? NC : 1];
-#pragma unroll
-    for (int j = 0; j < NC; ++j) cc[j] = P.c[j][m];
-    OP::template bc_term<0>(s, cc, K, t, g);
-}
-
+// One workgroup per 256-node segment of one row (axis 1 for 3-D grids; the
+// single row of a 2-D grid's plane) of one end plane, so that a workgroup's rows
+// are uniform: an edge row holds only zeros and loads nothing.  Every load goes
+// through a plane's buffer descriptor with a 32-bit byte offset.
 template <class OP>
 __global__ __launch_bounds__(256) void bc_kernel(Ptrs P, Dims D, KCoef K, const double* dloss,
                                                  double two_over_M) {
-    constexpr int DIM = OP::DIM, NF = OP::NF;
-    const float scale = (float)(two_over_M * (*dloss));
-    const long long nz = D.nz, ny = D.ny, nx = D.nx;
-    const long long plane = ny * nx;
-    const long long total = 2 * plane;
-    const long long str[3] = {plane, (DIM == 3) ? nx : 1, 1};
-    for (long long idx = blockIdx.x * 256LL + threadIdx.x; idx < total;
-         idx += (long long)gridDim.x * 256LL) {
-        const bool low = idx < plane;
-        const long long r = low ? idx : idx - plane;
-        const long long node = (low ? 0 : (nz - 1) * plane) + r;
-        const long long i1 = (DIM == 3) ? r / nx : r;
-        const long long i2 = r % nx;
-        const bool edge = (DIM == 3) ? (i1 == 0 || i1 == ny - 1 || i2 == 0 || i2 == nx - 1)
-                                     : (i1 == 0 || i1 == nx - 1);
-        float g[NF];
-        if (!edge) {
-            bc_node0<OP>(P, K, str, node, low, g);
+    constexpr int DIM = OP::DIM, NF = OP::NF, NC = OP::NC;
+    const int segs = (D.nx + 255) / 256;
+    int blk = blockIdx.x;
+    const int seg = blk % segs;
+    blk /= segs;
+    const int i1 = blk % D.ny;           // row of the plane (0 for 2-D grids)
+    const bool low = blk / D.ny == 0;    // plane 0, else plane nz - 1
+    const int i2 = seg * 256 + (int)threadIdx.x;
+    if (i2 >= D.nx) return;
+    const int zn = low ? 0 : D.nz - 1;   // the node's plane
+    const int zm = low ? 1 : D.nz - 2;   // its inward neighbour's (the residual's) plane
+    const uint32_t pbytes = (uint32_t)D.ny * (uint32_t)D.nx * 4u;
+    const uint32_t off = (uint32_t)(i1 * D.nx + i2) * 4u;
+    const bool edge_row = DIM == 3 && (i1 == 0 || i1 == D.ny - 1);
+    float g[NF];
 #pragma unroll
-            for (int f = 0; f < NF; ++f) g[f] *= scale;
-        } else {
+    for (int f = 0; f < NF; ++f) g[f] = 0.f;
+    if (!edge_row && i2 >= 1 && i2 <= D.nx - 2) {
+        const uint32_t dy = (uint32_t)D.nx * 4u;
+        Star st[NF];
 #pragma unroll
-            for (int f = 0; f < NF; ++f) g[f] = 0.f;
+        for (int f = 0; f < NF; ++f) {
+            const __amdgpu_buffer_rsrc_t rc = plane_rsrc(P.f[f], zm, pbytes);
+            st[f].c = bld(rc, off);
+            st[f].m[0] = bld(plane_rsrc(P.f[f], zm - 1, pbytes), off);
+            st[f].p[0] = bld(plane_rsrc(P.f[f], zm + 1, pbytes), off);
+            st[f].m[DIM - 1] = bld(rc, off - 4u);
+            st[f].p[DIM - 1] = bld(rc, off + 4u);
+            if (DIM == 3) {
+                st[f].m[1] = bld(rc, off - dy);
+                st[f].p[1] = bld(rc, off + dy);
+            }
         }
+        float cc[NC > 0 ? NC : 1];
 #pragma unroll
-        for (int f = 0; f < NF; ++f) __builtin_nontemporal_store(g[f], &P.out[f][node]);
+        for (int j = 0; j < NC; ++j) cc[j] = bld(plane_rsrc(P.c[j], zm, pbytes), off);
+        OP::template bc_term<0>(st, cc, K, low ? -1.f : 1.f, g);  // node = m + t e_0
+        const float scale = (float)(two_over_M * (*dloss));
+#pragma unroll
+        for (int f = 0; f < NF; ++f) g[f] *= scale;
     }
+#pragma unroll
+    for (int f = 0; f < NF; ++f) bst<kStream>(plane_rsrc(P.out[f], zn, pbytes), off, g[f]);
 }
 
 }  // namespace fpde
