@@ -155,7 +155,7 @@ int fpde_residual_bwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
                       const float* const* fields, const float* const* consts,
                       const double* dloss, float* const* grads, void* stream);
 
-/* Boundary-gradient correction (Sec. 2.3, App. A.5): a 1-D launch over the
+/* Boundary-gradient correction (Sec. 2.3, App. A.5): one launch over the
  * boundary nodes the backward march does not visit, the end planes i_0 = 0 and
  * i_0 = n_0 - 1.  A node whose only boundary coordinate is i_0 receives the
  * terms of its single inward neighbour's residuals; a node with a second

@@ -24,8 +24,8 @@
 // 1..nz-2, or all of them on a periodic grid and in the one-pass value and
 // gradient (the end planes' terms then come from the same gather).
 //
-// Boundary correction: a 1-D launch over the two end planes of axis 0, the
-// boundary nodes the three-call backward does not visit (Sec. 2.3).
+// Boundary correction: one workgroup per row segment of the two end planes of
+// axis 0, the boundary nodes the three-call backward does not visit (Sec. 2.3).
 //
 // Workgroup-to-tile order is XCD-aware: consecutive workgroup ids are spread
 // round-robin over the 8 XCDs, so the id is remapped such that each XCD gets a
