@@ -184,9 +184,12 @@ def measured_traffic(cfg, op, kernels, path="loss"):
     return round(total)
 
 
-def cpu_baseline(W, wl_full, cfg, seed, planes, bc_mode=0, path="loss", min_s=10.0):
+def cpu_baseline(W, wl_full, cfg, seed, planes, bc_mode=0, path="loss", min_s=10.0, gpu=None):
     """The oracle (single thread, float64) on a slab of the same workload, timed
-    over repeated passes totalling at least min_s seconds."""
+    over repeated passes totalling at least min_s seconds.  When the slab is the
+    whole grid and gpu = (loss, grads) of the timed steps is given (the loss and
+    fused paths), the oracle's last pass also checks them: "parity" holds the
+    loss's relative error and each gradient's max|err| / max|ref|."""
     import numpy as np  # noqa: PLC0415
     import oracle  # noqa: PLC0415  (CPU baseline leg only)
     shape = wl_full.shape
@@ -210,22 +213,31 @@ def cpu_baseline(W, wl_full, cfg, seed, planes, bc_mode=0, path="loss", min_s=10
         what = "residuals + transposed-Jacobian action"
     else:
         def one():
-            oracle.loss(*args, bc_mode=bc_mode)
-            oracle.grad(*args, dloss=1.0, bc_mode=bc_mode)
+            return (oracle.loss(*args, bc_mode=bc_mode),
+                    oracle.grad(*args, dloss=1.0, bc_mode=bc_mode))
         what = "loss + full gradient"
     # repeated until at least min_s of CPU work has been timed (one pass at least)
     reps, t0 = 0, time.perf_counter()
     while True:
-        one()
+        out = one()
         reps += 1
         dt = time.perf_counter() - t0
         if dt >= min_s:
             break
     npts = int(np.prod(sshape))
-    return {"value": npts * reps / dt, "unit": "grid-points/s", "cores": 1, "kind": "oracle",
-            "sample": f"{cfg} seed {seed}: first {planes} planes along axis 0 "
-                      f"({'x'.join(map(str, sshape))} = {npts} nodes), {what}, "
-                      f"float64, single thread, {reps} passes in {dt:.2f} s"}
+    res = {"value": npts * reps / dt, "unit": "grid-points/s", "cores": 1, "kind": "oracle",
+           "sample": f"{cfg} seed {seed}: first {planes} planes along axis 0 "
+                     f"({'x'.join(map(str, sshape))} = {npts} nodes), {what}, "
+                     f"float64, single thread, {reps} passes in {dt:.2f} s"}
+    if gpu is not None and out is not None and planes == shape[0]:
+        L_ref, g_ref = out
+        L_gpu, g_gpu = gpu
+        res["parity"] = {
+            "loss_rel_err": abs(L_gpu - L_ref) / abs(L_ref),
+            "grad_max_rel_err": [float(np.abs(a.astype(np.float64) - b).max() / np.abs(b).max())
+                                 for a, b in zip(g_gpu, g_ref)],
+            "bars": {"loss": 1e-5, "grad": 1e-4}}
+    return res
 
 
 def main():
@@ -357,7 +369,10 @@ def main():
         flushed_dirty["grid_points_per_s"] = N / (flushed_dirty["ms_per_step_median"] * 1e-3)
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(W, wl, cfg, args.seed, args.cpu_planes, bcm, args.path)
+        gpu_out = None
+        if args.path in ("loss", "fused"):  # the last timed step's loss and gradient
+            gpu_out = (float(loss.item()), [g.cpu().numpy() for g in grads])
+        cpu = cpu_baseline(W, wl, cfg, args.seed, args.cpu_planes, bcm, args.path, gpu=gpu_out)
     out = {
         "metric": METRIC,
         "value": N * K / total_s,
