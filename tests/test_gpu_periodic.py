@@ -84,8 +84,10 @@ def test_periodic_bwd_writes_every_node_and_bc_nothing():
         assert all(torch.isnan(x).all() for x in g)
 
 
-def test_periodic_full_size_ns3d(oracle_mod):
-    """The 256^3 Taylor-Green workload on the wrapped grid, every node."""
-    wl = W.make("ns_3d_tgv", seed=42)
-    print(f"case periodic full ns_3d_tgv {wl.shape}", flush=True)
+@pytest.mark.parametrize("seed", [42, 43, 44, 45, 46])
+def test_periodic_full_size_ns3d(oracle_mod, seed):
+    """The 256^3 Taylor-Green workload on the wrapped grid, every node, for the
+    paper's seeds."""
+    wl = W.make("ns_3d_tgv", seed=seed)
+    print(f"case periodic full ns_3d_tgv {wl.shape} seed {seed}", flush=True)
     _compare(oracle_mod, wl, 1.0, "periodic full ns_3d_tgv")
