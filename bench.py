@@ -12,13 +12,27 @@ Byte model (each input read once per pass, each output written once):
   them again and write one gradient per field, so one step moves
   (2 (NF + NC) + NF) * 4 bytes per grid node (72 B/node for the 3D NS case).
 
-The reported figure is the first of --runs runs of K back-to-back steps;
-"runs" gives the median and quartiles over all of them (the paper's protocol
-takes the median of five).  Beside the warm figure (steps back to back, as a
-training loop calls the operator), "flushed" times steps one by one after reading 512 MB between them,
-so that every input comes from HBM rather than the 256 MB memory-side cache;
-"flushed_dirty" writes the 512 MB instead, so that the step also pays for
-writing back the dirty lines that the write leaves in the caches.
+Protocol (the paper's: median of five runs, Sec. 4.1):
+  1. W untimed warm-up steps;
+  2. --runs runs of K back-to-back steps, each between two HIP events and
+     nothing else: `value` and `ms_per_step` are the MEDIAN run, all runs are
+     listed under "runs";
+  3. a separate pass per kernel of the step: K steps with HIP events around
+     that kernel only; its median over the K steps is the kernel's duration
+     ("kernel_us"), from which `roofline` is computed for the dominant kernel;
+  4. "flushed": steps timed one by one after reading 512 MB between them (every
+     input then comes from HBM rather than the 256 MB memory-side cache);
+     "flushed_dirty" writes the 512 MB instead, so the step also pays for
+     writing back the dirty lines the write leaves in the caches;
+  5. "workloads" (default config only; --no-workloads skips it): the same
+     median-of-runs step time for the other workloads and paths, each with a
+     whole-grid parity check against the oracle;
+  6. "cpu_baseline": the oracle on all host cores (whole-grid passes, threads
+     each running the unchanged single-threaded oracle on an overlapping slab
+     of axis 0) and on one core, the last pass checking the GPU's loss and
+     gradient ("parity").
+The process exits with status 3 after printing the line if any parity check
+exceeds its bar.
 
 --path fused times fpde_residual_value_and_grad, the same loss and gradient
 from one read of the inputs ((2 NF + NC) * 4 B/node: 44 for the 3D NS case).
@@ -33,6 +47,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -42,6 +57,12 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0
 METRIC = "grid-points/s and achieved HBM GB/s (% of peak) for residual fwd+bwd"
+BARS = {"loss": 1e-5, "residual": 1e-5, "grad": 1e-4}  # max|err| / max|ref|
+DEFAULT_CONFIG = "ns_3d_tgv"
+# (config, path, bc_mode) of the "workloads" object, beside the headline case
+EXTRA_CASES = (("burgers_1dt", "loss", 0), ("helmholtz_2d", "loss", 0), ("heat_3d", "loss", 0),
+               ("ns_2d", "loss", 0), ("ns_3d_tgv", "fused", 0), ("ns_3d_tgv", "residual", 0),
+               ("ns_3d_tgv", "loss", 1))
 
 
 def parse():
@@ -49,12 +70,12 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=100)
     p.add_argument("--warmup", type=int, default=None,
-                   help="untimed warm-up steps (default: as many as take 0.5 s, at least 50: "
-                        "a step back to back with others settles only after ~150 steps; after "
-                        "20, the timed NS-3D steps read ~6%% slow)")
-    p.add_argument("--config", default="ns_3d_tgv")
+                   help="untimed warm-up steps (default: as many as take 0.5 s, at least 50)")
+    p.add_argument("--config", default=DEFAULT_CONFIG)
     p.add_argument("--seed", type=int, default=42)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-workloads", action="store_true",
+                   help="skip the other workloads and paths (the 'workloads' object)")
     p.add_argument("--cpu-planes", type=int, default=0,
                    help="planes of the oracle sample along axis 0 (0: sized automatically)")
     p.add_argument("--bc-mode", type=int, default=0, choices=(0, 1),
@@ -63,15 +84,11 @@ def parse():
                    help="loss: fwd+loss, bwd, bc (the benchmark); residual: fwd writing R, "
                         "then the explicit-sensitivity backward; fused: the one-pass value "
                         "and gradient")
-    p.add_argument("--sample-every", type=int, default=10,
-                   help="per-kernel HIP events on every n-th timed step (the others carry none)")
     p.add_argument("--runs", type=int, default=5,
-                   help="the K timed steps are the first of this many runs of K steps; the "
-                        "line adds the median and quartiles of ms per step over the runs")
+                   help="runs of K timed steps; the line reports the median run")
     p.add_argument("--flushed-steps", type=int, default=20,
-                   help="after the timed region, steps timed one by one with 512 MB read "
-                        "(then written) between them (outside the events), so that no input is "
-                        "left in the caches; reported beside the warm figure (0: skip)")
+                   help="steps timed one by one with 512 MB read (then written) between them, "
+                        "outside the events (0: skip)")
     return p.parse_args()
 
 
@@ -102,34 +119,151 @@ def byte_model(wl, bc_mode=0, path="loss"):
     }
 
 
-def flushed_steps(torch, step, stream, n, flush_bytes=512 << 20, dirty=False):
-    """Each of n steps timed alone (events on the step's stream) after a sweep
-    over 512 MB that evicts the 256 MB memory-side cache and L2, the sweep
-    outside the events: the step's inputs then come from HBM.  The sweep reads
-    the buffer (the caches then hold clean lines), or with dirty=True writes it
-    (the caches then hold dirty lines, written back while the step runs).
-    Median and quartiles of the per-step milliseconds."""
-    import statistics  # noqa: PLC0415
-    buf = torch.empty(flush_bytes // 4, dtype=torch.float32, device="cuda")
-    buf.fill_(1.0)
-    ms = []
-    for i in range(n):
-        with torch.cuda.stream(stream):
-            if dirty:
-                buf.fill_(float(i))
-            else:
-                torch.sum(buf)
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        step()
-        b.record(stream)
-        b.synchronize()
-        ms.append(a.elapsed_time(b))
-    del buf
-    q = statistics.quantiles(ms, n=4) if len(ms) > 1 else [ms[0]] * 3
-    return {"steps": n, "ms_per_step_median": round(q[1], 4), "ms_q1": round(q[0], 4),
-            "ms_q3": round(q[2], 4), "flush_bytes": flush_bytes,
-            "flush": "write" if dirty else "read"}
+def _quartiles(xs):
+    if len(xs) == 1:
+        return xs[0], xs[0], xs[0]
+    q = statistics.quantiles(xs, n=4)
+    return q[0], statistics.median(xs), q[2]
+
+
+# --------------------------------------------------------------------------- the GPU side
+
+
+class Case:
+    """One workload and path bound to resident device tensors: `calls` are the
+    (name, bound entry point) pairs one step queues on one stream."""
+
+    def __init__(self, torch, B, W, cfg, seed, path, bc_mode):
+        self.torch, self.cfg, self.path, self.bc_mode = torch, cfg, path, bc_mode
+        self.wl = wl = W.make(cfg, seed=seed)
+        dev = torch.device("cuda:0")
+        self.fields = [torch.from_numpy(f).to(dev) for f in wl.fields]
+        self.consts = [torch.from_numpy(c).to(dev) for c in wl.consts]
+        # every output written once before the first step (no first-touch inside the timing)
+        self.grads = [torch.zeros_like(f) for f in self.fields]
+        self.loss = torch.zeros((), dtype=torch.float64, device=dev)
+        self.dl = torch.ones((), dtype=torch.float64, device=dev)
+        self.stream = s = torch.cuda.current_stream()
+        op, h, co, f, c = wl.op, wl.h, wl.coeffs, self.fields, self.consts
+        kw = dict(bc_mode=bc_mode, stream=s)
+        self.R = self.sens = None
+        if path == "residual":
+            self.R = [torch.zeros_like(f[0]) for _ in wl.spec.residuals]
+            self.sens = [torch.from_numpy(g).to(dev)
+                         for g in W.sensitivities(op, wl.shape, seed + 1)]
+            self.calls = (("fwd", B.bind("fwd", op, f, c, h, co, residual_out=self.R,
+                                         loss=self.loss, **kw)),
+                          ("vjp", B.bind("vjp", op, f, None, h, co, sens=self.sens,
+                                         grads=self.grads, **kw)))
+        elif path == "fused":
+            self.calls = (("value_and_grad", B.bind("value_and_grad", op, f, c, h, co,
+                                                    dloss=self.dl, loss=self.loss,
+                                                    grads=self.grads, **kw)),)
+        else:
+            self.calls = (("fwd", B.bind("fwd", op, f, c, h, co, loss=self.loss, **kw)),
+                          ("bwd", B.bind("bwd", op, f, c, h, co, dloss=self.dl, grads=self.grads,
+                                         **kw)),
+                          ("bc", B.bind("bc", op, f, c, h, co, dloss=self.dl, grads=self.grads,
+                                        **kw)))
+        self.names = [n for n, _ in self.calls]
+        self.bm = byte_model(wl, bc_mode, path)
+
+    def step(self):
+        for _, fn in self.calls:
+            fn()
+
+    def _event(self):
+        return self.torch.cuda.Event(enable_timing=True)
+
+    def warm(self, steps=None, seconds=0.5):
+        """`steps` untimed steps, or (steps None) batches of 50 for `seconds`."""
+        torch = self.torch
+        if steps is not None:
+            for _ in range(steps):
+                self.step()
+            torch.cuda.synchronize()
+            return steps
+        n, t0 = 0, time.perf_counter()
+        while n < 50 or time.perf_counter() - t0 < seconds:
+            for _ in range(50):
+                self.step()
+            n += 50
+            torch.cuda.synchronize()
+        return n
+
+    def runs(self, K, n):
+        """n runs of K back-to-back steps, two events each: ms per step of every run."""
+        torch = self.torch
+        out = []
+        for _ in range(n):
+            a, b = self._event(), self._event()
+            torch.cuda.synchronize()
+            a.record(self.stream)
+            for _ in range(K):
+                self.step()
+            b.record(self.stream)
+            b.synchronize()
+            out.append(a.elapsed_time(b) / K)
+        return out
+
+    def kernel_medians(self, K):
+        """For each call of the step, K steps with events around that call only:
+        its median duration in microseconds."""
+        torch = self.torch
+        med = {}
+        for i, name in enumerate(self.names):
+            ev = [(self._event(), self._event()) for _ in range(K)]
+            torch.cuda.synchronize()
+            for k in range(K):
+                for j, (_, fn) in enumerate(self.calls):
+                    if j == i:
+                        ev[k][0].record(self.stream)
+                        fn()
+                        ev[k][1].record(self.stream)
+                    else:
+                        fn()
+            torch.cuda.synchronize()
+            med[name] = statistics.median(a.elapsed_time(b) for a, b in ev) * 1e3
+        return med
+
+    def flushed(self, n, flush_bytes=512 << 20, dirty=False):
+        """Each of n steps timed alone after a sweep over 512 MB that evicts the
+        memory-side cache and L2 (the sweep outside the events): reading the
+        buffer leaves clean lines, writing it dirty ones that are written back
+        while the step runs.  Median and quartiles of ms per step."""
+        torch = self.torch
+        buf = torch.empty(flush_bytes // 4, dtype=torch.float32, device="cuda")
+        buf.fill_(1.0)
+        ms = []
+        for i in range(n):
+            with torch.cuda.stream(self.stream):
+                if dirty:
+                    buf.fill_(float(i))
+                else:
+                    torch.sum(buf)
+            a, b = self._event(), self._event()
+            a.record(self.stream)
+            self.step()
+            b.record(self.stream)
+            b.synchronize()
+            ms.append(a.elapsed_time(b))
+        del buf
+        q1, q2, q3 = _quartiles(ms)
+        return {"steps": n, "ms_per_step_median": round(q2, 4), "ms_q1": round(q1, 4),
+                "ms_q3": round(q3, 4), "flush_bytes": flush_bytes,
+                "flush": "write" if dirty else "read",
+                "grid_points_per_s": self.wl.n_points / (q2 * 1e-3)}
+
+    def outputs(self):
+        """(loss, grads, residuals) of the last step, on the host."""
+        self.torch.cuda.synchronize()
+        R = [r.cpu().numpy() for r in self.R] if self.R is not None else None
+        return float(self.loss.item()), [g.cpu().numpy() for g in self.grads], R
+
+    def release(self):
+        for name in ("fields", "consts", "grads", "R", "sens", "calls"):
+            setattr(self, name, None)
+        self.torch.cuda.empty_cache()
 
 
 def copy_gbps(torch, nbytes=1 << 30, reps=20):
@@ -184,60 +318,197 @@ def measured_traffic(cfg, op, kernels, path="loss"):
     return round(total)
 
 
-def cpu_baseline(W, wl_full, cfg, seed, planes, bc_mode=0, path="loss", min_s=10.0, gpu=None):
-    """The oracle (single thread, float64) on a slab of the same workload, timed
-    over repeated passes totalling at least min_s seconds.  When the slab is the
-    whole grid and gpu = (loss, grads) of the timed steps is given (the loss and
-    fused paths), the oracle's last pass also checks them: "parity" holds the
-    loss's relative error and each gradient's max|err| / max|ref|."""
-    import numpy as np  # noqa: PLC0415
-    import oracle  # noqa: PLC0415  (CPU baseline leg only)
-    shape = wl_full.shape
-    if planes <= 0:
-        # a slab of at most ~40M nodes (the whole grid for every configured
-        # workload; tens of seconds of single-thread oracle work at most)
-        per_plane = int(np.prod(shape[1:]))
-        planes = max(3, min(shape[0], 40_000_000 // per_plane))
-    sl = (slice(0, planes),) + tuple(slice(None) for _ in shape[1:])
-    fields = [np.ascontiguousarray(f[sl], dtype=np.float64) for f in wl_full.fields]
-    consts = [np.ascontiguousarray(c[sl], dtype=np.float64) for c in wl_full.consts]
-    sshape = fields[0].shape
-    args = (wl_full.op, sshape, wl_full.h, wl_full.coeffs, fields, consts)
-    if path == "residual":
-        G = [np.ascontiguousarray(g[sl], dtype=np.float64)
-             for g in W.sensitivities(wl_full.op, shape, seed + 1)]
+# --------------------------------------------------------------------------- the CPU side
 
-        def one():
-            oracle.residual(*args, bc_mode=bc_mode)
-            oracle.vjp(*args, G, bc_mode=bc_mode)
-        what = "residuals + transposed-Jacobian action"
+
+def _rel(a, b):
+    import numpy as np  # noqa: PLC0415
+    s = float(np.abs(b).max())
+    e = float(np.abs(np.asarray(a, dtype=np.float64) - b).max())
+    return e / s if s > 0 else e
+
+
+def _oracle_whole(wl, bc_mode, path, seed, W):
+    """The oracle on the whole grid (float64, single thread): what the GPU path
+    computes for this case, for the parity check."""
+    import oracle  # noqa: PLC0415  (CPU baseline / parity leg only)
+    args = (wl.op, wl.shape, wl.h, wl.coeffs, wl.fields, wl.consts)
+    if path == "residual":
+        G = W.sensitivities(wl.op, wl.shape, seed + 1)
+        return {"R": oracle.residual(*args, bc_mode=bc_mode),
+                "grads": oracle.vjp(*args, G, bc_mode=bc_mode)}
+    return {"loss": oracle.loss(*args, bc_mode=bc_mode),
+            "grads": oracle.grad(*args, dloss=1.0, bc_mode=bc_mode)}
+
+
+def parity_of(gpu, ref):
+    """Max errors of the GPU outputs (loss, grads, R) against the oracle's,
+    relative to max|ref|, with the bars and a verdict."""
+    L, g, R = gpu
+    out = {}
+    if "loss" in ref:
+        out["loss_rel_err"] = abs(L - ref["loss"]) / abs(ref["loss"])
+    if "R" in ref and R is not None:
+        out["residual_max_rel_err"] = [_rel(a, b) for a, b in zip(R, ref["R"])]
+    out["grad_max_rel_err"] = [_rel(a, b) for a, b in zip(g, ref["grads"])]
+    ok = out.get("loss_rel_err", 0.0) <= BARS["loss"] and \
+        all(e <= BARS["residual"] for e in out.get("residual_max_rel_err", [])) and \
+        all(e <= BARS["grad"] for e in out["grad_max_rel_err"])
+    out["bars"] = BARS
+    out["ok"] = bool(ok)
+    return out
+
+
+def _slab_pass(oracle, wl, bc_mode, a, b):
+    """Loss part and gradient of planes [a, b) of axis 0 from the unchanged
+    single-threaded oracle on the slab [a - 2, b + 2) (wrapped on a periodic
+    grid): the gradient at a node depends on the inputs within two nodes, so the
+    slab's gradient on [a, b) is the whole grid's (with the whole grid's 1/M).
+    Returns (sum of R^2 over the residual nodes of [a, b), gradient of [a, b))."""
+    import numpy as np  # noqa: PLC0415
+    n0 = wl.shape[0]
+    if bc_mode == 1:
+        idx = np.arange(a - 2, b + 2) % n0
+        lo = 2
     else:
-        def one():
-            return (oracle.loss(*args, bc_mode=bc_mode),
-                    oracle.grad(*args, dloss=1.0, bc_mode=bc_mode))
-        what = "loss + full gradient"
-    # repeated until at least min_s of CPU work has been timed (one pass at least)
+        s, e = max(0, a - 2), min(n0, b + 2)
+        idx = np.arange(s, e)
+        lo = a - s
+    F = [np.ascontiguousarray(f[idx], dtype=np.float64) for f in wl.fields]
+    C = [np.ascontiguousarray(c[idx], dtype=np.float64) for c in wl.consts]
+    sshape = F[0].shape
+    args = (wl.op, sshape, wl.h, wl.coeffs, F, C)
+    M_full = wl.n_points if bc_mode == 1 else wl.n_residual_points
+    M_slab = int(np.prod(sshape)) if bc_mode == 1 else int(np.prod([n - 2 for n in sshape]))
+    R = oracle.residual(*args, bc_mode=bc_mode)
+    own = slice(lo, lo + (b - a))
+    ss = sum(float(np.sum(r[own] ** 2)) for r in R)  # zero off the residual set
+    g = oracle.grad(*args, dloss=M_slab / M_full, bc_mode=bc_mode)  # scale 2 / M_full
+    return ss, [x[own] for x in g]
+
+
+def oracle_all_cores(wl, bc_mode, cores, min_s=5.0):
+    """Whole-grid loss + gradient passes with `cores` threads, each calling the
+    unchanged single-threaded oracle on an overlapping slab of axis 0 (the
+    oracle is a C library; ctypes releases the interpreter lock during the
+    call).  Repeated for at least min_s.  Returns (grid-points/s, passes,
+    seconds, (loss, grads) of the last pass)."""
+    import numpy as np  # noqa: PLC0415
+    from concurrent.futures import ThreadPoolExecutor  # noqa: PLC0415
+
+    import oracle  # noqa: PLC0415  (CPU baseline leg only)
+    n0 = wl.shape[0]
+    nsl = max(1, min(cores, n0))
+    cuts = [round(i * n0 / nsl) for i in range(nsl + 1)]
+    M_full = wl.n_points if bc_mode == 1 else wl.n_residual_points
+    out = None
+    with ThreadPoolExecutor(max_workers=cores) as ex:
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            parts = list(ex.map(lambda i: _slab_pass(oracle, wl, bc_mode, cuts[i], cuts[i + 1]),
+                                range(nsl)))
+            reps += 1
+            dt = time.perf_counter() - t0
+            if dt >= min_s:
+                break
+    L = sum(p[0] for p in parts) / M_full
+    grads = [np.concatenate([p[1][f] for p in parts], axis=0) for f in range(len(wl.fields))]
+    out = (L, grads)
+    return wl.n_points * reps / dt, reps, dt, out
+
+
+def oracle_one_core(wl, bc_mode, path, seed, W, min_s=10.0):
+    """Whole-grid passes of the unchanged oracle on one thread, for at least
+    min_s.  Returns (grid-points/s, passes, seconds, oracle outputs of the last pass)."""
     reps, t0 = 0, time.perf_counter()
     while True:
-        out = one()
+        ref = _oracle_whole(wl, bc_mode, path, seed, W)
         reps += 1
         dt = time.perf_counter() - t0
         if dt >= min_s:
             break
-    npts = int(np.prod(sshape))
-    res = {"value": npts * reps / dt, "unit": "grid-points/s", "cores": 1, "kind": "oracle",
-           "sample": f"{cfg} seed {seed}: first {planes} planes along axis 0 "
-                     f"({'x'.join(map(str, sshape))} = {npts} nodes), {what}, "
-                     f"float64, single thread, {reps} passes in {dt:.2f} s"}
-    if gpu is not None and out is not None and planes == shape[0]:
-        L_ref, g_ref = out
-        L_gpu, g_gpu = gpu
-        res["parity"] = {
-            "loss_rel_err": abs(L_gpu - L_ref) / abs(L_ref),
-            "grad_max_rel_err": [float(np.abs(a.astype(np.float64) - b).max() / np.abs(b).max())
-                                 for a, b in zip(g_gpu, g_ref)],
-            "bars": {"loss": 1e-5, "grad": 1e-4}}
+    return wl.n_points * reps / dt, reps, dt, ref
+
+
+def host_cores():
+    """Host cores this process may use, at most 16 (one GPU's share of the box)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(n, 16))
+
+
+def cpu_baseline(case, W, seed, gpu_out):
+    """The oracle timed on the host beside the GPU run: all cores (the figure)
+    and one core, both whole-grid passes; the one-core pass also checks the
+    GPU's outputs of the timed steps."""
+    wl, bcm, path = case.wl, case.bc_mode, case.path
+    cores = host_cores()
+    what = {"loss": "loss + full gradient", "fused": "loss + full gradient",
+            "residual": "residuals + transposed-Jacobian action"}[path]
+    res = {"unit": "grid-points/s", "kind": "oracle"}
+    if path != "residual":
+        v, reps, dt, _ = oracle_all_cores(wl, bcm, cores)
+        res.update({"value": v, "cores": cores,
+                    "sample": f"{case.cfg} seed {seed}: the whole grid "
+                              f"({'x'.join(map(str, wl.shape))} = {wl.n_points} nodes), {what}, "
+                              f"float64; {cores} threads each running the single-threaded oracle "
+                              f"on an overlapping slab of axis 0; {reps} passes in {dt:.2f} s"})
+    v1, reps1, dt1, ref = oracle_one_core(wl, bcm, path, seed, W)
+    one = {"value": v1, "unit": "grid-points/s", "cores": 1, "kind": "oracle",
+           "sample": f"{case.cfg} seed {seed}: the whole grid ({wl.n_points} nodes), {what}, "
+                     f"float64, one thread, {reps1} passes in {dt1:.2f} s"}
+    if path == "residual":  # the all-core split is for the loss and its gradient only
+        res.update(one)
+    else:
+        res["single_core"] = one
+    res["parity"] = parity_of(gpu_out, ref)
     return res
+
+
+# --------------------------------------------------------------------------- main
+
+
+def measure(case, K, runs, warmup):
+    """Warm-up, the median-of-runs step time and the per-kernel medians."""
+    w = case.warm(steps=warmup)
+    run_ms = case.runs(K, runs)
+    kus = case.kernel_medians(K)
+    q1, med, q3 = _quartiles(run_ms)
+    return w, run_ms, med, q1, q3, kus
+
+
+def workloads_object(torch, B, W, seed, K, runs):
+    """The other workloads and paths: median-of-runs step time, grid-points/s,
+    byte-model bandwidth and whole-grid parity against the oracle."""
+    out = {}
+    for cfg, path, bcm in EXTRA_CASES:
+        key = f"{cfg}/{path}/bc{bcm}"
+        case = Case(torch, B, W, cfg, seed, path, bcm)
+        # small grids: more steps per run so that a run spans at least ~20 ms
+        k = K
+        w, run_ms, med, q1, q3, kus = measure(case, k, runs, None)
+        if med * k < 20.0:
+            k = int(min(2000, max(K, 20.0 / med)))
+            w2, run_ms, med, q1, q3, kus = measure(case, k, runs, 0)
+        gpu_out = case.outputs()
+        bm = case.bm
+        t0 = time.perf_counter()
+        ref = _oracle_whole(case.wl, bcm, path, seed, W)
+        rec = {"grid": list(case.wl.shape), "nodes": case.wl.n_points, "steps": k,
+               "warmup": w, "ms_per_step": round(med, 5), "ms_q1": round(q1, 5),
+               "ms_q3": round(q3, 5), "ms_per_step_runs": [round(x, 5) for x in run_ms],
+               "grid_points_per_s": case.wl.n_points / (med * 1e-3),
+               "bytes_per_step": bm["step"], "hbm_gbps": round(bm["step"] / (med * 1e-3) / 1e9, 1),
+               "hbm_frac_of_peak": round(bm["step"] / (med * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+               "kernel_us": {n: round(v, 2) for n, v in kus.items()},
+               "parity": parity_of(gpu_out, ref), "oracle_s": round(time.perf_counter() - t0, 2)}
+        out[key] = rec
+        case.release()
+        print(f"bench: {key} {med:.4f} ms/step, parity ok={rec['parity']['ok']}",
+              file=sys.stderr, flush=True)
+    return out
 
 
 def main():
@@ -256,139 +527,51 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     B.lib()
-    cfg = args.config
-    wl = W.make(cfg, seed=args.seed)
-    dev = torch.device("cuda:0")
-    fields = [torch.from_numpy(f).to(dev) for f in wl.fields]
-    consts = [torch.from_numpy(c).to(dev) for c in wl.consts]
-    grads = [torch.empty_like(f) for f in fields]
-    loss = torch.empty((), dtype=torch.float64, device=dev)
-    dl = torch.ones((), dtype=torch.float64, device=dev)
-    stream = torch.cuda.current_stream()
-    op, h, co = wl.op, wl.h, wl.coeffs
-
-    bcm = args.bc_mode
-
-    # the entry points bound once to the resident tensors: each step issues only
-    # the C calls (marshalling them in Python every time costs more host time
-    # than a small grid's GPU time)
-    kw = dict(bc_mode=bcm, stream=stream)
-    fwd = B.bind("fwd", op, fields, consts, h, co, loss=loss, **kw)
-    bwd = B.bind("bwd", op, fields, consts, h, co, dloss=dl, grads=grads, **kw)
-    bc = B.bind("bc", op, fields, consts, h, co, dloss=dl, grads=grads, **kw)
-    kernels = (("fwd", fwd), ("bwd", bwd), ("bc", bc))
-    if args.path == "residual":
-        R = [torch.empty_like(fields[0]) for _ in wl.spec.residuals]
-        sens = [torch.from_numpy(g).to(dev) for g in W.sensitivities(op, wl.shape, args.seed + 1)]
-        fwd_r = B.bind("fwd", op, fields, consts, h, co, residual_out=R, loss=loss, **kw)
-        vjp = B.bind("vjp", op, fields, None, h, co, sens=sens, grads=grads, **kw)
-        kernels = (("fwd", fwd_r), ("vjp", vjp))
-    if args.path == "fused":
-        value_and_grad = B.bind("value_and_grad", op, fields, consts, h, co, dloss=dl, loss=loss,
-                                grads=grads, **kw)
-        kernels = (("value_and_grad", value_and_grad),)  # (fill and march: one call)
-    names = [n for n, _ in kernels]
-
-    def step():
-        for _, fn in kernels:
-            fn()
-
-    if args.warmup is not None:
-        for _ in range(args.warmup):
-            step()
-        warmup = args.warmup
-    else:  # steps in batches of 50 until 0.5 s of them have run
-        warmup, t0 = 0, time.perf_counter()
-        while warmup < 50 or time.perf_counter() - t0 < 0.5:
-            for _ in range(50):
-                step()
-            warmup += 50
-            torch.cuda.synchronize()
-    torch.cuda.synchronize()
-
-    # Timed region: K steps between two events.  A timestamp between two kernels
-    # costs several microseconds of queue time, so per-kernel events sit on every
-    # n-th step only; their averages give the per-kernel durations.
-    K = args.steps
-    every = max(1, args.sample_every)
-    sampled = [k for k in range(K) if k % every == every - 1] or [K - 1]
-    ev = {k: [torch.cuda.Event(enable_timing=True) for _ in range(len(kernels) + 1)]
-          for k in sampled}
-    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_start.record(stream)
-    for k in range(K):
-        e = ev.get(k)
-        if e is None:
-            step()
-            continue
-        e[0].record(stream)
-        for i, (_, fn) in enumerate(kernels):
-            fn()
-            e[i + 1].record(stream)
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    total_s = t_start.elapsed_time(t_end) / 1e3
-    per = {n: sum(ev[k][i].elapsed_time(ev[k][i + 1]) for k in sampled) / len(sampled) * 1e3
-           for i, n in enumerate(names)}  # microseconds
-    L = float(loss.item())
+    cfg, bcm, K = args.config, args.bc_mode, args.steps
+    case = Case(torch, B, W, cfg, args.seed, args.path, bcm)
+    warmup, run_ms, med, q1, q3, kus = measure(case, K, args.runs, args.warmup)
+    L = float(case.loss.item())
     if not (L == L) or L <= 0:
         raise RuntimeError(f"bad loss {L}")
-
-    bm = byte_model(wl, bcm, args.path)
-    N = wl.n_points
-    ms = total_s / K * 1e3
-    gbps = bm["step"] * K / total_s / 1e9
-    dom = max((n for n in names if n in bm), key=lambda n: per[n])
-    achieved = bm[dom] / (per[dom] * 1e-6) / 1e9
+    bm, N = case.bm, case.wl.n_points
+    gbps = bm["step"] / (med * 1e-3) / 1e9
+    dom = max((n for n in case.names if n in bm), key=lambda n: kus[n])
+    achieved = bm[dom] / (kus[dom] * 1e-6) / 1e9
     roofline = {"bound": "hbm", "kernel": f"{dom} ({cfg})", "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                "traffic": measured_traffic(cfg, wl.op, TRAFFIC_KERNELS.get(dom, (dom,)), args.path),
-                "algorithmic_bytes_per_launch": bm[dom], "avg_launch_us": round(per[dom], 2)}
-    # the same K steps timed again (no per-kernel events), for a median and
-    # quartiles over runs beside the one figure the line reports
-    run_ms = [ms]
-    for _ in range(max(0, args.runs - 1)):
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        a.record(stream)
-        for _ in range(K):
-            step()
-        b.record(stream)
-        b.synchronize()
-        run_ms.append(a.elapsed_time(b) / K)
-    import statistics  # noqa: PLC0415
-    q = statistics.quantiles(run_ms, n=4) if len(run_ms) > 1 else [ms] * 3
-    runs = {"n": len(run_ms), "ms_per_step_median": round(q[1], 5), "ms_q1": round(q[0], 5),
-            "ms_q3": round(q[2], 5), "ms_per_step": [round(x, 5) for x in run_ms]}
+                "traffic": measured_traffic(cfg, case.wl.op, TRAFFIC_KERNELS.get(dom, (dom,)),
+                                            args.path),
+                "algorithmic_bytes_per_launch": bm[dom], "avg_launch_us": round(kus[dom], 2),
+                "timing": f"median over {K} steps, HIP events around this kernel only"}
+    ksum = sum(kus.values())
     flushed = flushed_dirty = None
     if args.flushed_steps > 0:
-        flushed = flushed_steps(torch, step, stream, args.flushed_steps)
-        flushed["grid_points_per_s"] = N / (flushed["ms_per_step_median"] * 1e-3)
-        flushed_dirty = flushed_steps(torch, step, stream, args.flushed_steps, dirty=True)
-        flushed_dirty["grid_points_per_s"] = N / (flushed_dirty["ms_per_step_median"] * 1e-3)
+        flushed = case.flushed(args.flushed_steps)
+        flushed_dirty = case.flushed(args.flushed_steps, dirty=True)
+    gpu_out = case.outputs()
+    cgbps = round(copy_gbps(torch), 1)
+    extra = None
+    if not args.no_workloads and cfg == DEFAULT_CONFIG and args.path == "loss" and bcm == 0:
+        extra = workloads_object(torch, B, W, args.seed, K, args.runs)
     cpu = None
     if not args.no_cpu_baseline:
-        gpu_out = None
-        if args.path in ("loss", "fused"):  # the last timed step's loss and gradient
-            gpu_out = (float(loss.item()), [g.cpu().numpy() for g in grads])
-        cpu = cpu_baseline(W, wl, cfg, args.seed, args.cpu_planes, bcm, args.path, gpu=gpu_out)
+        cpu = cpu_baseline(case, W, args.seed, gpu_out)
     out = {
         "metric": METRIC,
-        "value": N * K / total_s,
+        "value": N / (med * 1e-3),
         "unit": "grid-points/s",
         "n_gpus": 1,
         "steps": K,
         "warmup": warmup,
-        "ms_per_step": ms,
+        "ms_per_step": med,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": f"{cfg}: {W.CONFIGS[cfg].description}",
-                   "grid": list(wl.shape), "nodes": N,
-                   "fields": list(wl.spec.fields), "consts": list(wl.spec.consts),
+                   "grid": list(case.wl.shape), "nodes": N,
+                   "fields": list(case.wl.spec.fields), "consts": list(case.wl.spec.consts),
                    "seed": args.seed,
                    "step": {"loss": "fwd+loss, bwd, bc on one stream",
                             "residual": "fwd writing residuals, explicit-sensitivity vjp",
@@ -398,16 +581,24 @@ def main():
         "hbm_gbps": round(gbps, 1),
         "hbm_frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4),
         "bytes_per_step": bm["step"],
-        "kernel_us": {k: round(v, 2) for k, v in per.items()},
-        "kernel_us_sampled_steps": len(sampled),
-        "copy_gbps": round(copy_gbps(torch), 1),
-        "runs": runs,
+        "runs": {"n": len(run_ms), "statistic": "median", "ms_per_step": [round(x, 5) for x in run_ms],
+                 "ms_q1": round(q1, 5), "ms_q3": round(q3, 5)},
+        "kernel_us": {k: round(v, 2) for k, v in kus.items()},
+        "kernel_us_check": {"sum_us": round(ksum, 2), "step_us": round(med * 1e3, 2),
+                            "sum_le_step": bool(ksum <= med * 1e3)},
+        "copy_gbps": cgbps,
         "flushed": flushed,
         "flushed_dirty": flushed_dirty,
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "workloads": extra,
     }
     print(json.dumps(out), flush=True)
+    checks = ([cpu["parity"]["ok"]] if cpu else []) + \
+        ([r["parity"]["ok"] for r in extra.values()] if extra else [])
+    if not all(checks):
+        print("bench.py: a parity check exceeded its bar", file=sys.stderr)
+        sys.exit(3)
 
 
 if __name__ == "__main__":

@@ -301,9 +301,27 @@ int check_outputs(const Req& r, const fpde_grid*, const float* const* fields,
     return FPDE_OK;
 }
 
-int hip_status() {
-    const hipError_t e = hipGetLastError();
-    return e == hipSuccess ? FPDE_OK : FPDE_ERR_HIP;
+template <class T>
+struct ident {
+    using type = T;
+};
+
+// Queues kernel k on stream s and returns the status of that launch alone:
+// hipLaunchKernel's own return value.  The thread's last-error state, which the
+// caller may have left set by an earlier call, is neither read nor cleared.
+// (The arguments take the kernel's parameter types, so each is passed in the
+// layout the kernel expects.)
+template <class... P>
+int launch(void (*k)(P...), dim3 grid, dim3 block, hipStream_t s,
+           typename ident<P>::type... args) {
+    void* a[] = {(void*)&args...};
+    return hipLaunchKernel(reinterpret_cast<const void*>(k), grid, block, a, 0, s) == hipSuccess
+               ? FPDE_OK
+               : FPDE_ERR_HIP;
+}
+
+int zero_loss(const Req& r, double* loss) {
+    return launch(fill_f64_kernel, dim3(1), dim3(1), r.stream, loss, 0.0);
 }
 
 // ---- launches, per op type
@@ -319,46 +337,48 @@ void with_flag(bool v, F&& f) {
 template <class OP, int TX, int TY>
 int launch_fwd(const Req& r, bool store, double* loss, int zc) {
     const Dims dm = tile_dims(r.dims, TX, TY, zc);
-    hipLaunchKernelGGL(fill_f64_kernel, dim3(1), dim3(1), 0, r.stream, loss, 0.0);
-    with_flag(store, [&](auto st) {
+    int st = zero_loss(r, loss);
+    if (st != FPDE_OK) return st;
+    with_flag(store, [&](auto sr) {
         with_flag(dm.per, [&](auto per) {
-            hipLaunchKernelGGL((fwd_kernel<OP, TX, TY, decltype(st)::value, decltype(per)::value>),
-                               dim3(dm.nblocks), dim3(TX * TY), 0, r.stream, r.P, dm, r.K, r.inv_M,
-                               loss);
+            st = launch(fwd_kernel<OP, TX, TY, decltype(sr)::value, decltype(per)::value>,
+                        dim3(dm.nblocks), dim3(TX * TY), r.stream, r.P, dm, r.K, r.inv_M, loss);
         });
     });
-    return hip_status();
+    return st;
 }
 
 // the register-queue forward (no LDS, no barrier)
 template <class OP, int TX, int TY>
 int launch_fwdq(const Req& r, bool store, double* loss, int zc) {
     const Dims dm = tile_dims(r.dims, TX, TY, zc);
-    hipLaunchKernelGGL(fill_f64_kernel, dim3(1), dim3(1), 0, r.stream, loss, 0.0);
-    with_flag(store, [&](auto st) {
+    int st = zero_loss(r, loss);
+    if (st != FPDE_OK) return st;
+    with_flag(store, [&](auto sr) {
         with_flag(dm.per, [&](auto per) {
-            hipLaunchKernelGGL(
-                (fwdq_kernel<OP, TX, TY, FPDE_FWD2_Q, decltype(st)::value, decltype(per)::value>),
-                dim3(dm.nblocks), dim3(TX * TY), 0, r.stream, r.P, dm, r.K, r.inv_M, loss);
+            st = launch(fwdq_kernel<OP, TX, TY, FPDE_FWD2_Q, decltype(sr)::value,
+                                    decltype(per)::value>,
+                        dim3(dm.nblocks), dim3(TX * TY), r.stream, r.P, dm, r.K, r.inv_M, loss);
         });
     });
-    return hip_status();
+    return st;
 }
 
 template <class OP, int TX, int TY>
 int launch_bwd(const Req& r, const double* dloss, int zc, double* loss) {
     const Dims dm = tile_dims(r.dims, TX, TY, zc);
     // value and gradient in one pass when loss is given
-    if (loss) hipLaunchKernelGGL(fill_f64_kernel, dim3(1), dim3(1), 0, r.stream, loss, 0.0);
+    int st = loss ? zero_loss(r, loss) : FPDE_OK;
+    if (st != FPDE_OK) return st;
     with_flag(loss != nullptr, [&](auto lo) {
         with_flag(dm.per, [&](auto per) {
-            hipLaunchKernelGGL(
-                (bwd_kernel<OP, TX, TY, kBwdReverse, decltype(lo)::value, decltype(per)::value>),
-                dim3(dm.nblocks), dim3(TX * TY), 0, r.stream, r.P, dm, r.K, dloss, r.two_over_M,
-                r.inv_M, loss);
+            st = launch(bwd_kernel<OP, TX, TY, kBwdReverse, decltype(lo)::value,
+                                   decltype(per)::value>,
+                        dim3(dm.nblocks), dim3(TX * TY), r.stream, r.P, dm, r.K, dloss,
+                        r.two_over_M, r.inv_M, loss);
         });
     });
-    return hip_status();
+    return st;
 }
 
 // 3-D: the chunk length shared by the forward and the backward
@@ -373,9 +393,8 @@ int launch_bc(const Req& r, const double* dloss) {
     // the two end planes of axis 0: one workgroup per 256-node segment of each row
     // (fewer than 2^31 of them: the node count of a plane is below 2^29)
     const long long nb = 2LL * r.dims.ny * ((r.dims.nx + 255) / 256);
-    hipLaunchKernelGGL((bc_kernel<OP>), dim3((unsigned)nb), dim3(256), 0, r.stream, r.P, r.dims,
-                       r.K, dloss, r.two_over_M);
-    return hip_status();
+    return launch(bc_kernel<OP>, dim3((unsigned)nb), dim3(256), r.stream, r.P, r.dims, r.K, dloss,
+                  r.two_over_M);
 }
 
 // Explicit-sensitivity backward: every plane of axis 0 is marched (zlo = 0).
@@ -384,13 +403,14 @@ int launch_vjp(const Req& r, bool acc, int target) {
     Dims base = r.dims;
     base.zlo = 0;
     const Dims dm = tile_dims(base, TX, TY, chunk_planes(base, TX, TY, target));
+    int st = FPDE_OK;
     with_flag(acc, [&](auto ac) {
         with_flag(dm.per, [&](auto per) {
-            hipLaunchKernelGGL((vjp_kernel<OP, TX, TY, decltype(ac)::value, decltype(per)::value>),
-                               dim3(dm.nblocks), dim3(TX * TY), 0, r.stream, r.P, dm, r.K);
+            st = launch(vjp_kernel<OP, TX, TY, decltype(ac)::value, decltype(per)::value>,
+                        dim3(dm.nblocks), dim3(TX * TY), r.stream, r.P, dm, r.K);
         });
     });
-    return hip_status();
+    return st;
 }
 
 int run_vjp(const Req& r, bool acc) {

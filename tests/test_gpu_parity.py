@@ -1,11 +1,9 @@
 """GPU parity: the HIP path (through the C ABI) against the CPU oracle.
 
-Small and ragged grids are compared element by element over every node
-(residuals on the residual set, the loss, and the gradient on every node,
+Small, ragged and full-size grids are compared element by element over every
+node (residuals on the residual set, the loss, and the gradient on every node,
 boundary shell included).  Full-size grids run in the same launch
-configuration the benchmark times; there the loss is compared with the oracle
-on the whole grid, and residuals and gradients on windows that the oracle
-evaluates on a sub-grid (corners, edges, faces and the middle of the domain).
+configuration the benchmark times.
 """
 from __future__ import annotations
 
@@ -186,72 +184,18 @@ def test_autograd_function_matches_abi(oracle_mod):
 # --------------------------------------------------------------------------- full size
 
 
-def _windows(shape, w):
-    """Sub-grid boxes: every corner, the middle of every edge/face, the centre."""
-    picks = []
-    for n in shape:
-        picks.append(sorted({0, max(0, n // 2 - w // 2), n - w}))
-    boxes = []
-    import itertools  # noqa: PLC0415
-    for starts in itertools.product(*picks):
-        boxes.append(tuple(slice(s, s + w) for s in starts))
-    return boxes
-
-
-def _window_check(oracle_mod, wl, R, g, dloss, w):
-    M_full = wl.n_residual_points
-    for box in _windows(wl.shape, w):
-        sub_f = [np.ascontiguousarray(f[box]) for f in wl.fields]
-        sub_c = [np.ascontiguousarray(c[box]) for c in wl.consts]
-        sshape = sub_f[0].shape
-        Rs = oracle_mod.residual(wl.op, sshape, wl.h, wl.coeffs, sub_f, sub_c)
-        # residuals on the sub-grid interior equal the full-grid residuals there
-        for b in range(len(Rs)):
-            e = H.max_rel_err(H.interior(R[b][box]), H.interior(Rs[b]))
-            assert e <= H.TOL_RES, (box, b, e)
-        # gradients: G = 2 dloss R / M with the full-grid M; exact on nodes at least
-        # two nodes away from every cut (non-boundary) face of the box
-        Gs = [2.0 * dloss * r / M_full for r in Rs]
-        gs = oracle_mod.vjp(wl.op, sshape, wl.h, wl.coeffs, sub_f, sub_c, Gs)
-        valid = []
-        for a, sl in enumerate(box):
-            lo = 0 if sl.start == 0 else 2
-            hi = sshape[a] if sl.stop == wl.shape[a] else sshape[a] - 2
-            valid.append(slice(lo, hi))
-        valid = tuple(valid)
-        for f in range(len(gs)):
-            e = H.max_rel_err(g[f][box][valid], gs[f][valid])
-            assert e <= H.TOL_GRAD, (box, f, e)
-
-
 # the paper's seeds (App. A.7); each draws a new synthetic workload
 SEEDS = [42, 43, 44, 45, 46]
 
 
 @pytest.mark.parametrize("seed", SEEDS)
-@pytest.mark.parametrize("cfg", ["burgers_1dt", "helmholtz_2d", "heat_3d", "ns_2d"])
+@pytest.mark.parametrize("cfg", ["burgers_1dt", "helmholtz_2d", "heat_3d", "ns_2d", "ns_3d_tgv"])
 def test_parity_full_size_every_node(oracle_mod, cfg, seed):
-    """Full-size grids the oracle finishes in seconds: compared node by node."""
+    """Every workload at full size, in the launch configuration the benchmark
+    times (the 256^3 Taylor-Green grid included: 16.8M nodes x 4 residuals and
+    4 gradients), compared with the whole-grid oracle node by node."""
     wl = W.make(cfg, seed=seed)
     print(f"case full {cfg} {wl.shape} seed {seed}", flush=True)
     R, L, g = H.run_gpu(wl, dloss=1.0)
     Rr, Lr, gr = oracle_mod.on_workload(wl, dloss=1.0)
     H.assert_parity(wl, R, L, g, Rr, Lr, gr, what=f"full {cfg}")
-
-
-@pytest.mark.parametrize("seed", SEEDS)
-def test_parity_full_size_ns3d_windows(oracle_mod, seed):
-    """3D TGV at 256^3: the loss against the oracle on the whole grid; residuals
-    and gradients against the oracle on 27 sub-grid windows, each scaled by the
-    window's own max|ref| (stricter than the whole-array scale)."""
-    wl = W.make("ns_3d_tgv", seed=seed)
-    print(f"case full ns_3d_tgv {wl.shape} seed {seed}", flush=True)
-    R, L, g = H.run_gpu(wl, dloss=1.0)
-    Lr = oracle_mod.loss(wl.op, wl.shape, wl.h, wl.coeffs, wl.fields, wl.consts)
-    assert abs(L - Lr) <= H.TOL_RES * abs(Lr), (L, Lr)
-    sm = H.shell_mask(wl.shape)
-    for r in R:
-        assert np.all(r[sm] == 0)
-    for x in g:
-        assert np.all(np.isfinite(x))
-    _window_check(oracle_mod, wl, R, g, 1.0, w=24)
