@@ -21,7 +21,7 @@
 #include <stdlib.h>
 #include <string.h>
 
-#define ORC_MAXD 3
+#define ORC_MAXD 4
 
 typedef struct {
     int ndim;
@@ -49,6 +49,7 @@ static int op_shape(int op, int* ndim, int* nf, int* nc, int* nr) {
     case 7: *ndim = 2; *nf = 1; *nc = 1; *nr = 1; return 0; /* Poisson 2D: u ; f        */
     case 8: *ndim = 3; *nf = 1; *nc = 1; *nr = 1; return 0; /* Poisson 3D: u ; f        */
     case 9: *ndim = 3; *nf = 3; *nc = 0; *nr = 3; return 0; /* NS 2D+t: u,v,p (t,x,y)   */
+    case 10: *ndim = 4; *nf = 4; *nc = 0; *nr = 4; return 0; /* NS 3D+t: u,v,w,p (t,x,y,z) */
     default: return -1;
     }
 }
@@ -207,9 +208,10 @@ static void res_poisson(const grid_t* g, const coef_t* c, const double* const* F
 }
 
 /* Unsteady incompressible NS on a space-time grid: array axis 0 is t, velocity
- * component b lives on array axis b+1 (u<->1, v<->2), pressure after the
+ * component b lives on array axis b+1 (u<->1, v<->2[, w<->3]), pressure after the
  * velocities; every derivative, the time derivative included, is a centred
- * difference (the time step is the grid spacing h_0):
+ * difference (the time step is the grid spacing h_0).  The 2D+t grid (op 9)
+ * has ndim 3, the 3D+t grid (op 10) ndim 4; d = ndim - 1 spatial components:
  *   R_b = D1_0 c_b + sum_a c_a D1_{a+1} c_b + D1_{b+1} p - nu sum_a D2_{a+1} c_b
  *   R_div = sum_a D1_{a+1} c_a              (a, b over the spatial components) */
 static void res_ns_t(const grid_t* g, const coef_t* c, const double* const* F,
@@ -239,7 +241,7 @@ static void residual_at(int op, const grid_t* g, const coef_t* c, const double* 
     case 5: res_ns(g, c, F, C, m, iv, R, 1); break;
     case 6: res_ns(g, c, F, C, m, iv, R, 0); break;
     case 7: case 8: res_poisson(g, c, F, C, m, iv, R); break;
-    case 9: res_ns_t(g, c, F, C, m, iv, R); break;
+    case 9: case 10: res_ns_t(g, c, F, C, m, iv, R); break;
     }
 }
 
@@ -406,7 +408,7 @@ static void jt_at(int op, const grid_t* g, const coef_t* c, const double* const*
     case 5: jt_ns(g, c, F, C, m, iv, G, gr, 1); break;
     case 6: jt_ns(g, c, F, C, m, iv, G, gr, 0); break;
     case 7: case 8: jt_poisson(g, c, F, C, m, iv, G, gr); break;
-    case 9: jt_ns_t(g, c, F, C, m, iv, G, gr); break;
+    case 9: case 10: jt_ns_t(g, c, F, C, m, iv, G, gr); break;
     }
 }
 

@@ -15,7 +15,8 @@
  * Arrays are C-contiguous with shape n[0..ndim-1] (last axis fastest).
  * Op ids: 1 Burgers 1D+t, 2 Helmholtz 2D, 3 heat 3D (one implicit step),
  *         4 steady NS 2D, 5 backward-Euler NS 3D, 6 steady NS 3D,
- *         7 Poisson 2D, 8 Poisson 3D, 9 unsteady NS 2D+t (space-time grid).
+ *         7 Poisson 2D, 8 Poisson 3D, 9 unsteady NS 2D+t (space-time grid,
+ *         ndim 3), 10 unsteady NS 3D+t (space-time grid, ndim 4: t, x, y, z).
  * coef = {nu, k, dt, alpha}; members an op does not use are ignored.
  * bc_mode 0: residuals on interior nodes only (1 <= i_a <= n_a-2 on every axis).
  * bc_mode 1: periodic wrap on every axis, residuals on all nodes.

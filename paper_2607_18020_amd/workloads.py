@@ -31,6 +31,7 @@ NS_3D_STEADY = 6
 POISSON_2D = 7
 POISSON_3D = 8
 NS_2DT = 9
+NS_3DT = 10
 
 OP_NAMES = {
     BURGERS_1DT: "burgers_1dt",
@@ -42,6 +43,7 @@ OP_NAMES = {
     POISSON_2D: "poisson_2d",
     POISSON_3D: "poisson_3d",
     NS_2DT: "ns_2dt",
+    NS_3DT: "ns_3dt",
 }
 
 
@@ -68,6 +70,8 @@ OPS: Dict[int, OpSpec] = {
     POISSON_3D: OpSpec(POISSON_3D, 3, ("u",), ("f",), ("R",)),
     # space-time grid (t, x, y): velocity component b on array axis b + 1
     NS_2DT: OpSpec(NS_2DT, 3, ("u", "v", "p"), (), ("R_u", "R_v", "R_c")),
+    # space-time grid (t, x, y, z): velocity component b on array axis b + 1
+    NS_3DT: OpSpec(NS_3DT, 4, ("u", "v", "w", "p"), (), ("R_u", "R_v", "R_w", "R_c")),
 }
 
 # the operators of the five benchmark workloads; the others are the adjacent
@@ -150,10 +154,20 @@ CONFIGS: Dict[str, Config] = {
     "ns_2dt": Config("ns_2dt", NS_2DT, (64, 512, 512), Coeffs(nu=0.01),
                      "2D+t unsteady incompressible NS (u,v,p) on a space-time grid 64 x 512^2, "
                      "t in [0,1], (x,y) on [0,2pi)^2, nu=0.01, central time differences"),
+    # the paper's 3D Taylor-Green operator on its space-time grid (32^3 x 10 points),
+    # and on ~42M space-time points, the largest grid of its kernel-scaling study
+    "ns_3dt": Config("ns_3dt", NS_3DT, (10, 32, 32, 32), Coeffs(nu=0.01),
+                     "3D+t unsteady incompressible NS (u,v,w,p) on a space-time grid 10 x 32^3, "
+                     "t in [0,1], (x,y,z) on [0,2pi)^3, nu=0.01, central time differences"),
+    "ns_3dt_large": Config("ns_3dt_large", NS_3DT, (20, 128, 128, 128), Coeffs(nu=0.01),
+                           "3D+t unsteady incompressible NS (u,v,w,p) on a space-time grid "
+                           "20 x 128^3 (41.9M points), t in [0,1], (x,y,z) on [0,2pi)^3, "
+                           "nu=0.01, central time differences"),
 }
 
 CONFIG_ORDER = ("burgers_1dt", "helmholtz_2d", "heat_3d", "ns_2d", "ns_3d_tgv")
-ADJACENT_CONFIGS = ("ns_3d_steady", "poisson_2d", "poisson_3d", "ns_2dt")
+ADJACENT_CONFIGS = ("ns_3d_steady", "poisson_2d", "poisson_3d", "ns_2dt", "ns_3dt",
+                    "ns_3dt_large")
 
 
 def spacing(cfg_name: str, shape: Sequence[int]) -> Tuple[float, ...]:
@@ -163,7 +177,8 @@ def spacing(cfg_name: str, shape: Sequence[int]) -> Tuple[float, ...]:
     Helmholtz, heat, 2D NS, 3D steady NS, Poisson: endpoint-inclusive nodes on
     [0,1] per axis.
     3D TGV: periodic sampling x_i = 2*pi*i/n on [0,2pi).
-    2D+t NS: axis 0 is t on [0,1] endpoint-inclusive; x, y periodic on [0,2pi).
+    2D+t and 3D+t NS: axis 0 is t on [0,1] endpoint-inclusive; the spatial
+    axes periodic on [0,2pi).
     """
     if cfg_name == "burgers_1dt":
         return (1.0 / (shape[0] - 1), 2.0 / (shape[1] - 1))
@@ -172,7 +187,7 @@ def spacing(cfg_name: str, shape: Sequence[int]) -> Tuple[float, ...]:
         return tuple(1.0 / (s - 1) for s in shape)
     if cfg_name == "ns_3d_tgv":
         return tuple(2.0 * math.pi / s for s in shape)
-    if cfg_name == "ns_2dt":
+    if cfg_name in ("ns_2dt", "ns_3dt", "ns_3dt_large"):
         return (1.0 / (shape[0] - 1),) + tuple(2.0 * math.pi / s for s in shape[1:])
     raise KeyError(cfg_name)
 
@@ -309,6 +324,21 @@ def make(cfg_name: str, seed: int = 42, shape: Optional[Sequence[int]] = None) -
         p = 0.25 * (np.cos(2.0 * x) + np.cos(2.0 * y)) * e2
         fields = [_f32(np.broadcast_to(q, shape) + noise()) for q in (u, v, p)]
         consts = []
+    elif cfg_name in ("ns_3dt", "ns_3dt_large"):
+        # the 3D Taylor-Green vortex (the initial condition of the TGV workload)
+        # decaying in time at the viscous rates of its velocity (3 nu) and
+        # pressure (6 nu) modes, + N(0, 0.01^2) on every field
+        t, x, y, z = X
+        nu = cfg.coeffs.nu
+        e1, e2 = np.exp(-3.0 * nu * t), np.exp(-6.0 * nu * t)
+        u = np.sin(x) * np.cos(y) * np.cos(z) * e1
+        v = -np.cos(x) * np.sin(y) * np.cos(z) * e1
+        w = np.zeros(shape)
+        p = (np.cos(2.0 * x) + np.cos(2.0 * y)) * (np.cos(2.0 * z) + 2.0) / 16.0 * e2
+        fields = []
+        for q in (u, v, w, p):  # (one at a time: the large grid is 168 MB per array)
+            fields.append(_f32(np.broadcast_to(q, shape) + noise()))
+        consts = []
     else:  # pragma: no cover
         raise KeyError(cfg_name)
 
@@ -331,7 +361,8 @@ def normal_fields(op: int, shape: Sequence[int], seed: int,
         coeffs = {BURGERS_1DT: Coeffs(nu=0.01 / math.pi), HELMHOLTZ_2D: Coeffs(k=4 * math.pi),
                   HEAT_3D_BE: Coeffs(dt=1e-3, alpha=0.1), NS_2D_STEADY: Coeffs(nu=0.01),
                   NS_3D_BE: Coeffs(nu=0.01, dt=1e-2), NS_3D_STEADY: Coeffs(nu=0.01),
-                  POISSON_2D: Coeffs(), POISSON_3D: Coeffs(), NS_2DT: Coeffs(nu=0.01)}[op]
+                  POISSON_2D: Coeffs(), POISSON_3D: Coeffs(), NS_2DT: Coeffs(nu=0.01),
+                  NS_3DT: Coeffs(nu=0.01)}[op]
     return Workload(f"normal_{OP_NAMES[op]}", op, shape, tuple(float(x) for x in h), coeffs,
                     fields, consts)
 

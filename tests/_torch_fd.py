@@ -40,14 +40,15 @@ def residuals(op, h, co, F, C):
     if op in (7, 8):  # Poisson
         u, f = F[0], C[0]
         return [sum(_d2(u, a, h) for a in range(d)) - c0(f)]
-    if op == 9:  # NS on a space-time grid: axis 0 = t, velocity component b on axis b + 1
-        vel, p = F[:2], F[2]
+    if op in (9, 10):  # NS on a space-time grid: axis 0 = t, velocity component b on axis b + 1
+        ds = d - 1  # spatial components
+        vel, p = F[:ds], F[ds]
         out = []
-        for b in range(2):
-            r = _d1(vel[b], 0, h) + sum(c0(vel[a]) * _d1(vel[b], a + 1, h) for a in range(2)) \
-                + _d1(p, b + 1, h) - co.nu * sum(_d2(vel[b], a + 1, h) for a in range(2))
+        for b in range(ds):
+            r = _d1(vel[b], 0, h) + sum(c0(vel[a]) * _d1(vel[b], a + 1, h) for a in range(ds)) \
+                + _d1(p, b + 1, h) - co.nu * sum(_d2(vel[b], a + 1, h) for a in range(ds))
             out.append(r)
-        out.append(sum(_d1(vel[a], a + 1, h) for a in range(2)))
+        out.append(sum(_d1(vel[a], a + 1, h) for a in range(ds)))
         return out
     if op in (4, 5, 6):  # incompressible NS, velocity component b on axis b
         vel, p = F[:d], F[d]

@@ -21,19 +21,20 @@ static double uni(void) { /* xorshift64, in [-1, 1) */
 int main(void) {
     const long shapes2[][2] = {{3, 3}, {4, 7}, {9, 5}};
     const long shapes3[][3] = {{3, 3, 3}, {4, 5, 7}, {6, 3, 5}};
+    const long shapes4[][4] = {{3, 3, 3, 3}, {4, 3, 5, 6}, {5, 4, 3, 4}};
     const double coef[4] = {0.01, 2.0, 0.1, 0.3};
     int bad = 0, calls = 0;
-    for (int op = 1; op <= 9; ++op) {
+    for (int op = 1; op <= 10; ++op) {
         int ndim, nf, nc, nr;
         if (orc_op_info(op, &ndim, &nf, &nc, &nr) != 0) {
             printf("oracle-sanitize: op_info %d failed\n", op);
             return 1;
         }
         for (int si = 0; si < 3; ++si) {
-            const long* n = ndim == 2 ? shapes2[si] : shapes3[si];
+            const long* n = ndim == 2 ? shapes2[si] : ndim == 3 ? shapes3[si] : shapes4[si];
             long N = 1;
             for (int a = 0; a < ndim; ++a) N *= n[a];
-            const double h[3] = {0.5, 0.25, 0.125};
+            const double h[4] = {0.5, 0.25, 0.125, 0.375};
             double *f[4], *c[3], *G[4], *R[4], *g[4];
             for (int i = 0; i < nf; ++i) {
                 f[i] = malloc(N * sizeof(double));

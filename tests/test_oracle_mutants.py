@@ -36,6 +36,11 @@ MUTANTS = {
     "ns_dropped_time_term": ("if (unsteady) gr[b][m] += gm / c->dt;", ""),
     "periodic_wrap_off_by_one": ("if (i >= g->n[a]) i -= g->n[a];",
                                  "if (i >= g->n[a]) i -= g->n[a] - 1;"),
+    # the space-time NS operators (2D+t, 3D+t)
+    "spacetime_time_adjoint_sign": ("gr[b][nb(g, iv, m, 0, +1)] += gm / (2.0 * g->h[0]);",
+                                    "gr[b][nb(g, iv, m, 0, +1)] -= gm / (2.0 * g->h[0]);"),
+    "spacetime_last_axis_dropped": ("for (a = 0; a < d; a++) R[d] += D1(g, F[a], iv, m, a + 1);",
+                                    "for (a = 0; a + 1 < d; a++) R[d] += D1(g, F[a], iv, m, a + 1);"),
 }
 
 

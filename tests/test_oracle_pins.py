@@ -26,8 +26,8 @@ from tests import _torch_fd
 
 OPS = sorted(W.OPS)
 
-SHAPES = {2: (9, 12), 3: (8, 11, 10)}
-H = {2: (0.11, 0.07), 3: (0.13, 0.09, 0.06)}
+SHAPES = {2: (9, 12), 3: (8, 11, 10), 4: (5, 7, 6, 8)}
+H = {2: (0.11, 0.07), 3: (0.13, 0.09, 0.06), 4: (0.13, 0.09, 0.06, 0.11)}
 COEF = {
     W.BURGERS_1DT: W.Coeffs(nu=0.03),
     W.HELMHOLTZ_2D: W.Coeffs(k=2.5),
@@ -38,6 +38,7 @@ COEF = {
     W.POISSON_2D: W.Coeffs(),
     W.POISSON_3D: W.Coeffs(),
     W.NS_2DT: W.Coeffs(nu=0.05),
+    W.NS_3DT: W.Coeffs(nu=0.04),
 }
 
 
@@ -99,11 +100,12 @@ def _symbol_residuals(op, co, modes, consts):
     if op in (W.POISSON_2D, W.POISSON_3D):
         (u, d1, d2), = modes
         return [sum(d2) - consts[0]]
-    if op == W.NS_2DT:  # axis 0 = t; velocity component b on axis b + 1
-        vel, p = modes[:2], modes[2]
-        out = [vel[b][1][0] + sum(vel[a][0] * vel[b][1][a + 1] for a in range(2)) + p[1][b + 1]
-               - co.nu * (vel[b][2][1] + vel[b][2][2]) for b in range(2)]
-        out.append(sum(vel[a][1][a + 1] for a in range(2)))
+    if op in (W.NS_2DT, W.NS_3DT):  # axis 0 = t; velocity component b on axis b + 1
+        d = len(modes) - 1
+        vel, p = modes[:d], modes[d]
+        out = [vel[b][1][0] + sum(vel[a][0] * vel[b][1][a + 1] for a in range(d)) + p[1][b + 1]
+               - co.nu * sum(vel[b][2][a + 1] for a in range(d)) for b in range(d)]
+        out.append(sum(vel[a][1][a + 1] for a in range(d)))
         return out
     d = len(modes) - 1
     vel, p = modes[:d], modes[d]
@@ -162,6 +164,12 @@ def _mms_problem(op):
         x, y = xs
         pool = [s(1.3 * x + 0.4) * c(0.7 * y - 0.2) + 0.3, c(0.9 * x - 0.5) * s(1.1 * y + 0.3),
                 s(0.8 * x + 1.1 * y) + 0.2 * x * y, c(1.7 * x) * c(0.6 * y + 0.8)]
+    elif ndim == 4:  # (t, x, y, z)
+        t, x, y, z = xs
+        pool = [s(1.3 * x + 0.4 + 0.5 * t) * c(0.7 * y - 0.2) * c(0.5 * z) + 0.3,
+                c(0.9 * x - 0.5) * s(1.1 * y + 0.3 - 0.7 * t) * s(0.8 * z + 0.1),
+                s(0.8 * x + 1.1 * y - 0.6 * z + 0.9 * t) + 0.2 * x * z * t,
+                c(1.7 * x) * c(0.6 * y + 0.8) + s(z) * c(1.2 * t)]
     else:
         x, y, z = xs
         pool = [s(1.3 * x + 0.4) * c(0.7 * y - 0.2) * c(0.5 * z) + 0.3,
@@ -191,12 +199,13 @@ def _mms_problem(op):
     elif op in (W.POISSON_2D, W.POISSON_3D):
         u, = F
         R = [sum(D(u, xi, 2) for xi in xs) - C[0]]
-    elif op == W.NS_2DT:  # xs = (t, x, y)
-        vel, p = F[:2], F[2]
-        R = [D(vel[b], xs[0]) + sum(vel[a] * D(vel[b], xs[a + 1]) for a in range(2))
+    elif op in (W.NS_2DT, W.NS_3DT):  # xs = (t, x, y[, z])
+        d = ndim - 1
+        vel, p = F[:d], F[d]
+        R = [D(vel[b], xs[0]) + sum(vel[a] * D(vel[b], xs[a + 1]) for a in range(d))
              + D(p, xs[b + 1]) - co.nu * sum(D(vel[b], xi, 2) for xi in xs[1:])
-             for b in range(2)]
-        R.append(sum(D(vel[a], xs[a + 1]) for a in range(2)))
+             for b in range(d)]
+        R.append(sum(D(vel[a], xs[a + 1]) for a in range(d)))
     else:
         vel, p = F[:ndim], F[ndim]
         R = []
@@ -215,8 +224,8 @@ def _mms_problem(op):
 def test_manufactured_solution_second_order(oracle_mod, op):
     ndim = W.OPS[op].ndim
     xs, F, C, R = _mms_problem(op)
-    ns = (12, 24, 48, 96) if ndim == 2 else (10, 20, 40)
-    lengths = (1.0, 1.4, 0.8)[:ndim]
+    ns = {2: (12, 24, 48, 96), 3: (10, 20, 40), 4: (10, 20, 40)}[ndim]
+    lengths = (1.0, 1.4, 0.8, 1.1)[:ndim]
     errs = []
     for n in ns:
         shape = tuple(n + 2 * a for a in range(ndim))  # non-square
@@ -280,8 +289,8 @@ class _FastLoss:
 def test_gradient_matches_finite_differences(oracle_mod, op, bc_mode):
     """Every node of every field, boundary shell included, on 8-16-point grids."""
     ndim = W.OPS[op].ndim
-    shape = (8, 13) if ndim == 2 else (8, 9, 10)
-    h = (0.21, 0.17, 0.13)[:ndim]
+    shape = {2: (8, 13), 3: (8, 9, 10), 4: (5, 6, 5, 6)}[ndim]
+    h = (0.21, 0.17, 0.13, 0.19)[:ndim]
     F, C = _rand_inputs(op, shape, 300 + op)
     co = COEF[op]
     dloss = 0.75
@@ -369,8 +378,8 @@ def test_matches_eager_torch_fd_autograd(oracle_mod, op, seed):
     """The paper's verification protocol (App. A.7): N(0,1) inputs, seeds 42-46,
     float64 eager FD reference differentiated by autograd."""
     ndim = W.OPS[op].ndim
-    shape = (17, 23) if ndim == 2 else (11, 13, 12)
-    wl = W.normal_fields(op, shape, seed, h=(0.05, 0.04, 0.03)[:ndim], coeffs=COEF[op])
+    shape = {2: (17, 23), 3: (11, 13, 12), 4: (7, 8, 6, 9)}[ndim]
+    wl = W.normal_fields(op, shape, seed, h=(0.05, 0.04, 0.03, 0.045)[:ndim], coeffs=COEF[op])
     Rt, Lt, gt = _torch_fd.loss_and_grad(op, wl.h, wl.coeffs, [f.astype(np.float64) for f in wl.fields],
                                          [c.astype(np.float64) for c in wl.consts])
     R = oracle_mod.residual(op, wl.shape, wl.h, wl.coeffs, wl.fields, wl.consts)
@@ -420,7 +429,7 @@ def test_ns2d_u_gradient_matches_paper_equation(oracle_mod):
 # --------------------------------------------------------------------------- invariants
 
 
-@pytest.mark.parametrize("op", [W.NS_2D_STEADY, W.NS_3D_BE, W.NS_3D_STEADY, W.NS_2DT])
+@pytest.mark.parametrize("op", [W.NS_2D_STEADY, W.NS_3D_BE, W.NS_3D_STEADY, W.NS_2DT, W.NS_3DT])
 def test_pressure_gradient_sums_to_zero(oracle_mod, op):
     ndim = W.OPS[op].ndim
     F, C = _rand_inputs(op, SHAPES[ndim], 600 + op)
