@@ -62,7 +62,7 @@ DEFAULT_CONFIG = "ns_3d_tgv"
 # (config, path, bc_mode) of the "workloads" object, beside the headline case
 EXTRA_CASES = (("burgers_1dt", "loss", 0), ("helmholtz_2d", "loss", 0), ("heat_3d", "loss", 0),
                ("ns_2d", "loss", 0), ("ns_3d_tgv", "fused", 0), ("ns_3d_tgv", "residual", 0),
-               ("ns_3d_tgv", "loss", 1))
+               ("ns_3d_tgv", "loss", 1), ("ns_3dt", "loss", 0), ("ns_3dt_large", "loss", 0))
 
 
 def parse():
@@ -95,7 +95,7 @@ def parse():
 # fields the residual Jacobian depends on (what the explicit-sensitivity backward
 # reads besides G): none for the linear operators, the velocity but not the
 # pressure for NS
-JAC_FIELDS = {1: 1, 2: 0, 3: 0, 4: 2, 5: 3, 6: 3, 7: 0, 8: 0, 9: 2}
+JAC_FIELDS = {1: 1, 2: 0, 3: 0, 4: 2, 5: 3, 6: 3, 7: 0, 8: 0, 9: 2, 10: 3}
 
 
 def byte_model(wl, bc_mode=0, path="loss"):
@@ -292,7 +292,7 @@ def copy_gbps(torch, nbytes=1 << 30, reps=20):
 TRAFFIC_KERNELS = {"value_and_grad": ("fill_f64", "bwd")}
 OP_KERNEL_TAG = {1: "OpBurgers", 2: "OpHelmholtz", 3: "OpHeat", 4: "OpNS<2, false>",
                  5: "OpNS<3, true>", 6: "OpNS<3, false>", 7: "OpPoisson<2>", 8: "OpPoisson<3>",
-                 9: "OpNST"}
+                 9: "OpNST", 10: "OpNS3T"}
 
 
 def measured_traffic(cfg, op, kernels, path="loss"):

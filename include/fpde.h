@@ -52,6 +52,14 @@
  *                                                         fields {u, v, p}  consts {}
  *       R_b = D1_0 c_b + sum_a c_a D1_{a+1} c_b + D1_{b+1} p - nu sum_a D2_{a+1} c_b
  *       R_div = sum_a D1_{a+1} c_a            (a, b = 0, 1; the time step is h[0])
+ *   FPDE_NS_3DT       (ndim 4; space-time grid: axis 0 = t, axes 1, 2, 3 = x, y, z;
+ *                      velocity component b on array axis b + 1; the paper's
+ *                      3d_ns_unsteady operator with a centred time difference)
+ *                                                         fields {u, v, w, p}  consts {}
+ *       R_b = D1_0 c_b + sum_a c_a D1_{a+1} c_b + D1_{b+1} p - nu sum_a D2_{a+1} c_b
+ *       R_div = sum_a D1_{a+1} c_a            (a, b = 0, 1, 2; the time step is h[0])
+ *     Four-axis grids are described by fpde_grid4 and served by the entry
+ *     points ending in 4 (which take every op); fpde_grid holds three axes.
  *
  * Common argument rules:
  *   - `fields`, `consts`, `residual_out`, `sens`, `grads` are HOST arrays holding
@@ -97,7 +105,8 @@ typedef enum fpde_op {
     FPDE_NS_3D_STEADY = 6,
     FPDE_POISSON_2D = 7,
     FPDE_POISSON_3D = 8,
-    FPDE_NS_2DT = 9
+    FPDE_NS_2DT = 9,
+    FPDE_NS_3DT = 10
 } fpde_op;
 
 /* Grid: rank, residual-set mode, sizes per array axis, spacings per axis.
@@ -112,6 +121,17 @@ typedef struct fpde_grid {
     int64_t n[3];
     double h[3];
 } fpde_grid;
+
+/* The grid with up to four axes (a versioned fpde_grid: same members, one more
+ * axis), taken by the entry points ending in 4.  Rules as fpde_grid; for
+ * ndim 4 the limits are every n_a >= 3, n_a < 2^31, and a time level of the
+ * last three axes (n[1]*n[2]*n[3]) below 2^29 nodes. */
+typedef struct fpde_grid4 {
+    int32_t ndim;
+    int32_t bc_mode;
+    int64_t n[4];
+    double h[4];
+} fpde_grid4;
 
 /* PDE coefficients in float64; an op ignores the members it does not use.
  * The library derives 1/(2h), 1/h^2, nu/h^2, ... in float64 and rounds them
@@ -210,6 +230,41 @@ int fpde_residual_value_and_grad(int op, const fpde_grid* grid, const fpde_coeff
 int fpde_residual_vjp(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
                       const float* const* fields, const float* const* sens, int accumulate,
                       float* const* grads, void* stream);
+
+/* The same five calls for grids described by fpde_grid4: every op, four-axis
+ * grids included.  Arguments, write sets and errors as the calls above, with
+ * "the planes of array axis 0" read for a four-axis grid as its time levels
+ * (3-D volumes).  For FPDE_NS_3DT:
+ *   - fpde_residual_fwd4 queues the loss fill and one march over every interior
+ *     time level; with residual_out, also a fill of zeros on the end levels
+ *     (3 kernels);
+ *   - fpde_residual_bwd4 writes every node of the levels 1 .. n[0] - 2 with two
+ *     kernels: a march over each level (the spatial part of the transposed
+ *     stencil, boundary nodes of the level included), then a march along the
+ *     time axis that adds the time part (R_q(t-1) - R_q(t+1)) / (2 h_t) at every
+ *     node of the spatial residual set, recomputing those residuals;
+ *   - fpde_bc_correct4 writes the end levels 0 and n[0] - 1 (1 kernel);
+ *   - fpde_residual_value_and_grad4 queues the fill, the level march with the
+ *     loss, the time march and (bc_mode 0) the end-level kernel;
+ *   - fpde_residual_vjp4 queues one march over every level; the time part comes
+ *     from the sensitivities of the neighbouring levels at the node itself.
+ * Queues nothing and returns an error status on invalid arguments, as above. */
+int fpde_residual_fwd4(int op, const fpde_grid4* grid, const fpde_coeffs* coeffs,
+                       const float* const* fields, const float* const* consts,
+                       float* const* residual_out, double* loss, void* stream);
+int fpde_residual_bwd4(int op, const fpde_grid4* grid, const fpde_coeffs* coeffs,
+                       const float* const* fields, const float* const* consts,
+                       const double* dloss, float* const* grads, void* stream);
+int fpde_bc_correct4(int op, const fpde_grid4* grid, const fpde_coeffs* coeffs,
+                     const float* const* fields, const float* const* consts,
+                     const double* dloss, float* const* grads, void* stream);
+int fpde_residual_value_and_grad4(int op, const fpde_grid4* grid, const fpde_coeffs* coeffs,
+                                  const float* const* fields, const float* const* consts,
+                                  const double* dloss, double* loss, float* const* grads,
+                                  void* stream);
+int fpde_residual_vjp4(int op, const fpde_grid4* grid, const fpde_coeffs* coeffs,
+                       const float* const* fields, const float* const* sens, int accumulate,
+                       float* const* grads, void* stream);
 
 /* Static string naming a status code (never NULL). */
 const char* fpde_status_string(int status);

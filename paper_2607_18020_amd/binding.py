@@ -24,14 +24,22 @@ FPDE_OK = 0
 STATUS_NAMES = {0: "FPDE_OK", -1: "FPDE_ERR_ARG", -2: "FPDE_ERR_SHAPE", -3: "FPDE_ERR_SPACING",
                 -4: "FPDE_ERR_COEFF", -5: "FPDE_ERR_ALIGN", -6: "FPDE_ERR_HIP",
                 -7: "FPDE_ERR_UNSUPPORTED"}
-EXPORTED = ("fpde_op_info", "fpde_residual_fwd", "fpde_residual_bwd", "fpde_bc_correct",
-            "fpde_residual_vjp", "fpde_residual_value_and_grad", "fpde_status_string",
-            "fpde_version")
+# the compute entry points; each also exists with a 4 suffix taking fpde_grid4
+CALLS = ("fpde_residual_fwd", "fpde_residual_bwd", "fpde_bc_correct", "fpde_residual_vjp",
+         "fpde_residual_value_and_grad")
+EXPORTED = ("fpde_op_info",) + CALLS + tuple(c + "4" for c in CALLS) + \
+    ("fpde_status_string", "fpde_version")
 
 
 class FpdeGrid(ctypes.Structure):
     _fields_ = [("ndim", ctypes.c_int32), ("bc_mode", ctypes.c_int32),
                 ("n", ctypes.c_int64 * 3), ("h", ctypes.c_double * 3)]
+
+
+class FpdeGrid4(ctypes.Structure):
+    """fpde_grid4: the grid with up to four axes (space-time 3D+t grids)."""
+    _fields_ = [("ndim", ctypes.c_int32), ("bc_mode", ctypes.c_int32),
+                ("n", ctypes.c_int64 * 4), ("h", ctypes.c_double * 4)]
 
 
 class FpdeCoeffs(ctypes.Structure):
@@ -56,16 +64,20 @@ def _load():
         lib = ctypes.CDLL(LIB_PATH)
         vp = ctypes.c_void_p
         pp = ctypes.POINTER(ctypes.c_void_p)
-        gp, cp = ctypes.POINTER(FpdeGrid), ctypes.POINTER(FpdeCoeffs)
+        cp = ctypes.POINTER(FpdeCoeffs)
         lib.fpde_op_info.argtypes = [ctypes.c_int] + [ctypes.POINTER(ctypes.c_int)] * 4
-        lib.fpde_residual_fwd.argtypes = [ctypes.c_int, gp, cp, pp, pp, pp, vp, vp]
-        lib.fpde_residual_bwd.argtypes = [ctypes.c_int, gp, cp, pp, pp, vp, pp, vp]
-        lib.fpde_bc_correct.argtypes = [ctypes.c_int, gp, cp, pp, pp, vp, pp, vp]
-        lib.fpde_residual_vjp.argtypes = [ctypes.c_int, gp, cp, pp, pp, ctypes.c_int, pp, vp]
-        lib.fpde_residual_value_and_grad.argtypes = [ctypes.c_int, gp, cp, pp, pp, vp, vp, pp, vp]
-        for name in ("fpde_op_info", "fpde_residual_fwd", "fpde_residual_bwd", "fpde_bc_correct",
-                     "fpde_residual_vjp", "fpde_residual_value_and_grad"):
-            getattr(lib, name).restype = ctypes.c_int
+        lib.fpde_op_info.restype = ctypes.c_int
+        for sfx, grid in (("", FpdeGrid), ("4", FpdeGrid4)):
+            gp = ctypes.POINTER(grid)
+            sig = {"fpde_residual_fwd": [ctypes.c_int, gp, cp, pp, pp, pp, vp, vp],
+                   "fpde_residual_bwd": [ctypes.c_int, gp, cp, pp, pp, vp, pp, vp],
+                   "fpde_bc_correct": [ctypes.c_int, gp, cp, pp, pp, vp, pp, vp],
+                   "fpde_residual_vjp": [ctypes.c_int, gp, cp, pp, pp, ctypes.c_int, pp, vp],
+                   "fpde_residual_value_and_grad": [ctypes.c_int, gp, cp, pp, pp, vp, vp, pp, vp]}
+            for name, args in sig.items():
+                fn = getattr(lib, name + sfx)
+                fn.argtypes = args
+                fn.restype = ctypes.c_int
         lib.fpde_status_string.argtypes = [ctypes.c_int]
         lib.fpde_status_string.restype = ctypes.c_char_p
         lib.fpde_version.argtypes = []
@@ -101,14 +113,20 @@ def op_info(op: int):
     return tuple(x.value for x in v)  # ndim, n_fields, n_consts, n_residuals
 
 
-def make_grid(shape: Sequence[int], h: Sequence[float], bc_mode: int = 0) -> FpdeGrid:
-    g = FpdeGrid()
+def make_grid(shape: Sequence[int], h: Sequence[float], bc_mode: int = 0):
+    """fpde_grid for up to three axes, fpde_grid4 for four."""
+    g = FpdeGrid4() if len(shape) == 4 else FpdeGrid()
     g.ndim = len(shape)
     g.bc_mode = int(bc_mode)
     for a, (n, hh) in enumerate(zip(shape, h)):
         g.n[a] = int(n)
         g.h[a] = float(hh)
     return g
+
+
+def _entry(name: str, shape):
+    """The C entry point for a grid of this rank (the 4-suffixed one for four axes)."""
+    return getattr(_load(), name + ("4" if len(shape) == 4 else ""))
 
 
 def make_coeffs(c) -> FpdeCoeffs:
@@ -169,7 +187,7 @@ def fpde_residual_fwd(op: int, fields, consts, h, coeffs, *, residual_out=None,
         _check_tensors(residual_out, shape, "fpde_residual_fwd residual_out")
         res_arr = _ptr_array(residual_out)
     g, c = make_grid(shape, h, bc_mode), make_coeffs(coeffs)
-    st = _load().fpde_residual_fwd(int(op), ctypes.byref(g), ctypes.byref(c), _ptr_array(fields),
+    st = _entry("fpde_residual_fwd", shape)(int(op), ctypes.byref(g), ctypes.byref(c), _ptr_array(fields),
                                    _ptr_array(consts) if len(consts) else None, res_arr,
                                    loss.data_ptr(), _stream(stream))
     if st != FPDE_OK:
@@ -201,15 +219,15 @@ def _grad_call(fn, name, op, fields, consts, h, coeffs, dloss, grads, bc_mode, s
 def fpde_residual_bwd(op: int, fields, consts, h, coeffs, dloss, *, grads=None, bc_mode: int = 0,
                       stream=None):
     """Queue the interior gather-form adjoint; returns the grads list."""
-    return _grad_call(_load().fpde_residual_bwd, "fpde_residual_bwd", op, fields, consts, h,
-                      coeffs, dloss, grads, bc_mode, stream)
+    return _grad_call(_entry("fpde_residual_bwd", fields[0].shape), "fpde_residual_bwd", op,
+                      fields, consts, h, coeffs, dloss, grads, bc_mode, stream)
 
 
 def fpde_bc_correct(op: int, fields, consts, h, coeffs, dloss, *, grads=None, bc_mode: int = 0,
                     stream=None):
     """Queue the boundary-shell correction; returns the grads list."""
-    return _grad_call(_load().fpde_bc_correct, "fpde_bc_correct", op, fields, consts, h,
-                      coeffs, dloss, grads, bc_mode, stream)
+    return _grad_call(_entry("fpde_bc_correct", fields[0].shape), "fpde_bc_correct", op,
+                      fields, consts, h, coeffs, dloss, grads, bc_mode, stream)
 
 
 def fpde_residual_value_and_grad(op: int, fields, consts, h, coeffs, dloss=1.0, *,
@@ -225,7 +243,8 @@ def fpde_residual_value_and_grad(op: int, fields, consts, h, coeffs, dloss=1.0, 
                          "tensor on the fields' device")
 
     def fn(op_, g, c, fp, cp_, dl, gp, st):
-        return _load().fpde_residual_value_and_grad(op_, g, c, fp, cp_, dl, loss.data_ptr(), gp, st)
+        return _entry("fpde_residual_value_and_grad", fields[0].shape)(
+            op_, g, c, fp, cp_, dl, loss.data_ptr(), gp, st)
 
     grads = _grad_call(fn, "fpde_residual_value_and_grad", op, fields, consts, h, coeffs, dloss,
                        grads, bc_mode, stream)
@@ -246,7 +265,7 @@ def fpde_residual_vjp(op: int, fields, h, coeffs, sens, *, grads=None, accumulat
         _used_on(stream, *grads)
     _check_tensors(grads, shape, "fpde_residual_vjp grads")
     g, c = make_grid(shape, h, bc_mode), make_coeffs(coeffs)
-    st = _load().fpde_residual_vjp(int(op), ctypes.byref(g), ctypes.byref(c), _ptr_array(fields),
+    st = _entry("fpde_residual_vjp", shape)(int(op), ctypes.byref(g), ctypes.byref(c), _ptr_array(fields),
                                    _ptr_array(sens), int(bool(accumulate)), _ptr_array(grads),
                                    _stream(stream))
     if st != FPDE_OK:
@@ -307,7 +326,7 @@ def bind(entry: str, op: int, fields, consts, h, coeffs, *, dloss=None, grads=No
             ra = _ptr_array(residual_out)
             keep += [ra, list(residual_out)]
         args = (int(op), ctypes.byref(g), ctypes.byref(c), fa, ca, ra, loss.data_ptr(), sh)
-        return BoundCall("fpde_residual_fwd", lib.fpde_residual_fwd, args, keep, loss)
+        return BoundCall("fpde_residual_fwd", _entry("fpde_residual_fwd", shape), args, keep, loss)
     if grads is None:
         grads = [torch.empty_like(f) for f in fields]
         _used_on(stream, *grads)
@@ -319,7 +338,7 @@ def bind(entry: str, op: int, fields, consts, h, coeffs, *, dloss=None, grads=No
         sa = _ptr_array(sens)
         keep += [sa, list(sens)]
         args = (int(op), ctypes.byref(g), ctypes.byref(c), fa, sa, int(bool(accumulate)), ga, sh)
-        return BoundCall("fpde_residual_vjp", lib.fpde_residual_vjp, args, keep, grads)
+        return BoundCall("fpde_residual_vjp", _entry("fpde_residual_vjp", shape), args, keep, grads)
     if not isinstance(dloss, torch.Tensor):
         dloss = torch.tensor(1.0 if dloss is None else float(dloss), dtype=torch.float64,
                              device=dev)
@@ -331,12 +350,12 @@ def bind(entry: str, op: int, fields, consts, h, coeffs, *, dloss=None, grads=No
     if entry == "value_and_grad":
         args = (int(op), ctypes.byref(g), ctypes.byref(c), fa, ca, dloss.data_ptr(),
                 loss.data_ptr(), ga, sh)
-        return BoundCall("fpde_residual_value_and_grad", lib.fpde_residual_value_and_grad, args,
-                         keep, (loss, grads))
+        return BoundCall("fpde_residual_value_and_grad",
+                         _entry("fpde_residual_value_and_grad", shape), args, keep, (loss, grads))
     if entry not in ("bwd", "bc"):
         raise ValueError(f"bind: unknown entry point {entry!r}")
-    fn = lib.fpde_residual_bwd if entry == "bwd" else lib.fpde_bc_correct
     name = "fpde_residual_bwd" if entry == "bwd" else "fpde_bc_correct"
+    fn = _entry(name, shape)
     args = (int(op), ctypes.byref(g), ctypes.byref(c), fa, ca, dloss.data_ptr(), ga, sh)
     return BoundCall(name, fn, args, keep, grads)
 

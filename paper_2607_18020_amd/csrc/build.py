@@ -43,7 +43,7 @@ CHECK_FLAGS = [
     "-DFPDE_NS3_MIN_BWD_BLOCKS=512", "-DFPDE_HEAT_FWD_TX=128", "-DFPDE_HEAT_BWD_TX=128",
     "-DFPDE_HEAT_MIN_BWD_BLOCKS=256", "-DFPDE_VJP_TY3=8", "-DFPDE_VJP_HEAT_TX=64",
     "-DFPDE_TX2=128", "-DFPDE_TX2_FWD=256", "-DFPDE_TX2_VG=256", "-DFPDE_BLOCKS2=512",
-    "-DFPDE_FWD2_Q=4", "-DFPDE_HEAT_FWD_QUEUE=1",
+    "-DFPDE_FWD2_Q=4", "-DFPDE_HEAT_FWD_QUEUE=1", "-DFPDE_NS4_BWD_TX=64", "-DFPDE_NS4_BWD_TY=8",
 ]
 
 _NOISE = "is not a recognized feature for this target"

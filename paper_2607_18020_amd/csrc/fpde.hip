@@ -122,6 +122,17 @@ struct Geo2 {
 // several fields with nonlinear coupling (NS)
 using GeoNS3 = Geo3<FPDE_NS3_FWD_TX, FPDE_NS3_FWD_TY, FPDE_NS3_BWD_TX, FPDE_NS3_BWD_TY,
                     FPDE_NS3_MIN_BWD_BLOCKS, FPDE_VJP_TX3, FPDE_VJP_TY3>;
+// 3D+t NS: the level march reads six time-neighbour velocities per node besides
+// the four fields, which do not fit the 128 registers of a 1024-thread backward
+// tile: 512-thread backward tiles
+#ifndef FPDE_NS4_BWD_TX
+#define FPDE_NS4_BWD_TX 128
+#endif
+#ifndef FPDE_NS4_BWD_TY
+#define FPDE_NS4_BWD_TY 4
+#endif
+using GeoNS4 = Geo3<FPDE_NS3_FWD_TX, FPDE_NS3_FWD_TY, FPDE_NS4_BWD_TX, FPDE_NS4_BWD_TY,
+                    FPDE_NS3_MIN_BWD_BLOCKS, FPDE_VJP_TX3, FPDE_VJP_TY3>;
 // one field, a Laplacian (heat, Poisson)
 using GeoHeat = Geo3<FPDE_HEAT_FWD_TX, FPDE_HEAT_FWD_TY, FPDE_HEAT_BWD_TX, FPDE_HEAT_BWD_TY,
                      FPDE_HEAT_MIN_BWD_BLOCKS, FPDE_VJP_HEAT_TX, FPDE_VJP_HEAT_TY,
@@ -147,18 +158,23 @@ int with_op(int op, F&& f) {
     case FPDE_POISSON_2D: return f(OpTag<OpPoisson<2>, Geo2>{});
     case FPDE_POISSON_3D: return f(OpTag<OpPoisson<3>, GeoHeat>{});
     case FPDE_NS_2DT: return f(OpTag<OpNST, GeoNS3>{});
+    // 3D+t: the 3-D marches run on one time level per workgroup
+    case FPDE_NS_3DT: return f(OpTag<OpNS3T, GeoNS4>{});
     }
     return FPDE_ERR_ARG;
 }
 
 struct OpDesc {
     int ndim, nf, nc, nr;
+    bool time;  // 3D+t: the grid has a time axis 0 before the DIM axes the kernels march
 };
 
 bool op_desc(int op, OpDesc* d) {
     return with_op(op, [&](auto tag) {
         using OP = typename decltype(tag)::OP;
-        *d = {OP::DIM, OP::NF, OP::NC, OP::NR};
+        // (a 3D+t operator's consts are its own fields at the neighbouring time
+        // levels, which the kernels address themselves: the caller passes none)
+        *d = {OP::DIM + (OP::TIME ? 1 : 0), OP::NF, OP::TIME ? 0 : OP::NC, OP::NR, OP::TIME};
         return FPDE_OK;
     }) == FPDE_OK;
 }
@@ -186,7 +202,7 @@ bool finite_pos(double v) { return isfinite(v) && v > 0.0; }
 
 // Validates everything except the outputs; fills req.  need_consts: the call
 // reads the const arrays (the explicit-sensitivity backward does not).
-int validate_common(int op, const fpde_grid* g, const fpde_coeffs* c, const float* const* fields,
+int validate_common(int op, const fpde_grid4* g, const fpde_coeffs* c, const float* const* fields,
                     const float* const* consts, Req* r, bool need_consts = true) {
     if (!op_desc(op, &r->d)) return FPDE_ERR_ARG;
     if (!g || !c || !fields) return FPDE_ERR_ARG;
@@ -208,23 +224,31 @@ int validate_common(int op, const fpde_grid* g, const fpde_coeffs* c, const floa
         N *= g->n[a];
         M *= per ? g->n[a] : g->n[a] - 2;  // periodic: a residual at every node
     }
-    // plane of the last two axes (one row for 2-D grids) addressed with 32-bit byte offsets
-    if ((D == 3 ? g->n[1] * g->n[2] : g->n[1]) >= (1LL << 29)) return FPDE_ERR_SHAPE;
+    // plane of the last two axes (one row for 2-D grids) addressed with 32-bit byte
+    // offsets; a 3D+t grid's time level (the last three axes) as well
+    if ((D >= 3 ? g->n[D - 2] * g->n[D - 1] : g->n[1]) >= (1LL << 29)) return FPDE_ERR_SHAPE;
+    if (D == 4 && g->n[1] * g->n[2] * g->n[3] >= (1LL << 29)) return FPDE_ERR_SHAPE;
     for (int a = 0; a < D; ++a)
         if (!finite_pos(g->h[a])) return FPDE_ERR_SPACING;
     if (!isfinite(c->nu) || !isfinite(c->k) || !isfinite(c->dt) || !isfinite(c->alpha))
         return FPDE_ERR_COEFF;
     if (uses_dt(op) && !(c->dt > 0.0)) return FPDE_ERR_COEFF;
 
-    // float32 kernel coefficients, derived in float64
+    // float32 kernel coefficients, derived in float64; a 3D+t grid's kernel axes
+    // are its spatial axes 1..3, and its time axis 0 has a coefficient of its own
+    const int A0 = r->d.time ? 1 : 0;  // first array axis the kernels march
     KCoef K;
     memset(&K, 0, sizeof K);
-    for (int a = 0; a < D; ++a) {
-        const double h = g->h[a];
+    for (int a = 0; a < D - A0; ++a) {
+        const double h = g->h[a + A0];
         K.i2hd[a] = 1.0 / (2.0 * h);
         K.i2h[a] = (float)(1.0 / (2.0 * h));
         K.ih2[a] = (float)(1.0 / (h * h));
         if (!isfinite(K.i2h[a]) || !isfinite(K.ih2[a]) || K.ih2[a] == 0.f) return FPDE_ERR_SPACING;
+    }
+    if (r->d.time) {
+        K.i2ht = (float)(1.0 / (2.0 * g->h[0]));
+        if (!isfinite(K.i2ht)) return FPDE_ERR_SPACING;
     }
     K.nu = (float)c->nu;
     K.k2 = (float)(c->k * c->k);
@@ -249,15 +273,33 @@ int validate_common(int op, const fpde_grid* g, const fpde_coeffs* c, const floa
     for (int j = 0; j < nc; ++j) r->P.c[j] = consts[j];
 
     Dims& dm = r->dims;  // sizes only; tiles and chunks are set per launch
-    dm.nz = (int)g->n[0];
-    dm.ny = (D == 3) ? (int)g->n[1] : 1;
+    dm.nz = (int)g->n[A0];
+    dm.ny = (D - A0 == 3) ? (int)g->n[A0 + 1] : 1;
     dm.nx = (int)g->n[D - 1];
     dm.tiles_x = dm.tiles_y = dm.zc = dm.nblocks = 0;
     dm.per = per ? 1 : 0;
     dm.zlo = per ? 0 : 1;  // the marched planes: 1 .. n0-2, or all of them
+    dm.nt = r->d.time ? (int)g->n[0] : 1;
+    dm.nlev = 1;  // (set per launch for 3D+t grids)
+    dm.lev0 = 0;
+    dm.vol = r->d.time ? (long long)dm.nz * dm.ny * dm.nx : 0;
     // every launch shape used below must have fewer than 2^31 workgroups
-    if ((long long)(dm.nx / 32 + 1) * (dm.ny + 1) * (dm.nz + 1) >= (1LL << 31)) return FPDE_ERR_SHAPE;
+    if ((long long)(dm.nx / 32 + 1) * (dm.ny + 1) * (dm.nz + 1) * dm.nt >= (1LL << 31))
+        return FPDE_ERR_SHAPE;
     return FPDE_OK;
+}
+
+// The time levels a 3D+t launch covers: those with residuals (1 .. nt-2), or
+// every level (periodic grids; the explicit-sensitivity backward, which writes
+// every node).  No-op for other grids.
+Dims levels(const Dims& n, bool all) {
+    Dims dm = n;
+    if (dm.nt > 1) {
+        const bool every = all || dm.per;
+        dm.lev0 = every ? 0 : 1;
+        dm.nlev = every ? dm.nt : dm.nt - 2;
+    }
+    return dm;
 }
 
 // Tiles of TX x TY columns; chunks of zc planes along axis 0.
@@ -268,14 +310,15 @@ Dims tile_dims(const Dims& n, int TX, int TY, int zc) {
     const int nplanes = dm.nz - 2 * dm.zlo;
     dm.zc = zc;
     const long long nch = (nplanes + zc - 1) / zc;
-    dm.nblocks = (int)((long long)dm.tiles_x * dm.tiles_y * nch);
+    dm.nblocks = (int)((long long)dm.tiles_x * dm.tiles_y * nch * dm.nlev);
     return dm;
 }
 
 // Chunk length giving a launch with TX x TY tiles about `target` workgroups
-// (each chunk at least one plane).
+// (each chunk at least one plane; 3D+t grids: over all launched levels).
 int chunk_planes(const Dims& n, int TX, int TY, int target) {
-    const long long tiles = (long long)((n.nx + TX - 1) / TX) * ((n.ny + TY - 1) / TY);
+    const long long tiles =
+        (long long)((n.nx + TX - 1) / TX) * ((n.ny + TY - 1) / TY) * n.nlev;
     const int nplanes = n.nz - 2 * n.zlo;
     long long nch = (target + tiles - 1) / tiles;
     if (nch < 1) nch = 1;
@@ -283,7 +326,7 @@ int chunk_planes(const Dims& n, int TX, int TY, int target) {
     return (int)((nplanes + nch - 1) / nch);
 }
 
-int check_outputs(const Req& r, const fpde_grid*, const float* const* fields,
+int check_outputs(const Req& r, const fpde_grid4*, const float* const* fields,
                   const float* const* consts, float* const* outs, int nout, const void* extra,
                   size_t extra_bytes) {
     const size_t bytes = (size_t)r.N * sizeof(float);
@@ -339,6 +382,11 @@ int launch_fwd(const Req& r, bool store, double* loss, int zc) {
     const Dims dm = tile_dims(r.dims, TX, TY, zc);
     int st = zero_loss(r, loss);
     if (st != FPDE_OK) return st;
+    if (OP::TIME && store && !dm.per) {  // the end time levels hold no residual node
+        st = launch(zero_levels_kernel<OP::NR>, dim3((unsigned)((2 * dm.vol + 255) / 256)),
+                    dim3(256), r.stream, r.P, dm);
+        if (st != FPDE_OK) return st;
+    }
     with_flag(store, [&](auto sr) {
         with_flag(dm.per, [&](auto per) {
             st = launch(fwd_kernel<OP, TX, TY, decltype(sr)::value, decltype(per)::value>,
@@ -390,17 +438,39 @@ int zc2(const Req& r) { return chunk_planes(r.dims, kTX2, 1, kTargetBlocks2); }
 
 template <class OP>
 int launch_bc(const Req& r, const double* dloss) {
-    // the two end planes of axis 0: one workgroup per 256-node segment of each row
-    // (fewer than 2^31 of them: the node count of a plane is below 2^29)
-    const long long nb = 2LL * r.dims.ny * ((r.dims.nx + 255) / 256);
-    return launch(bc_kernel<OP>, dim3((unsigned)nb), dim3(256), r.stream, r.P, r.dims, r.K, dloss,
-                  r.two_over_M);
+    if constexpr (OP::TIME) {
+        // 3D+t: the two end time levels, one workgroup per 256-node segment of
+        // each (x, y) row (fewer than 2^31: a level holds fewer than 2^29 nodes)
+        const long long nb = 2LL * r.dims.nz * r.dims.ny * ((r.dims.nx + 255) / 256);
+        return launch(bc4_kernel<OP>, dim3((unsigned)nb), dim3(256), r.stream, r.P, r.dims, r.K,
+                      dloss, r.two_over_M);
+    } else {
+        // the two end planes of axis 0: one workgroup per 256-node segment of each row
+        // (fewer than 2^31 of them: the node count of a plane is below 2^29)
+        const long long nb = 2LL * r.dims.ny * ((r.dims.nx + 255) / 256);
+        return launch(bc_kernel<OP>, dim3((unsigned)nb), dim3(256), r.stream, r.P, r.dims, r.K,
+                      dloss, r.two_over_M);
+    }
 }
 
-// Explicit-sensitivity backward: every plane of axis 0 is marched (zlo = 0).
+// 3D+t: the time part of the backward, one lane per spatial node marching the
+// time levels (after the level march, which wrote the spatial part)
+template <class OP>
+int launch_tm(const Req& r, const double* dloss) {
+    int st = FPDE_OK;
+    with_flag(r.dims.per, [&](auto per) {
+        st = launch(tm_kernel<OP, decltype(per)::value>,
+                    dim3((unsigned)((r.dims.vol + 255) / 256)), dim3(256), r.stream, r.P, r.dims,
+                    r.K, dloss, r.two_over_M);
+    });
+    return st;
+}
+
+// Explicit-sensitivity backward: every plane of axis 0 is marched (zlo = 0),
+// on a 3D+t grid in every time level.
 template <class OP, int TX, int TY>
 int launch_vjp(const Req& r, bool acc, int target) {
-    Dims base = r.dims;
+    Dims base = levels(r.dims, true);
     base.zlo = 0;
     const Dims dm = tile_dims(base, TX, TY, chunk_planes(base, TX, TY, target));
     int st = FPDE_OK;
@@ -424,7 +494,9 @@ int run_vjp(const Req& r, bool acc) {
     });
 }
 
-int run_fwd(const Req& r, bool store, double* loss) {
+int run_fwd(const Req& r0, bool store, double* loss) {
+    Req r = r0;
+    r.dims = levels(r0.dims, false);
     return with_op(r.op, [&](auto tag) {
         using OP = typename decltype(tag)::OP;
         using GEO = typename decltype(tag)::GEO;
@@ -441,13 +513,23 @@ int run_fwd(const Req& r, bool store, double* loss) {
 // writes the end planes), else also the loss (fused value and grad), marching
 // every plane: at the end planes the gather with the residuals off the residual
 // set taken as zero is their exact boundary term, so no boundary kernel follows
+//
+// 3D+t grids: the level march covers every plane of each level with residuals
+// (the boundary planes of the level included, as above), the time march then
+// adds the time part, and with the loss the end time levels follow (bc_mode 0).
 int run_bwd(const Req& r0, const double* dloss, double* loss = nullptr) {
     Req r = r0;
-    if (loss) r.dims.zlo = 0;
+    r.dims = levels(r0.dims, false);
+    if (loss || r.d.time) r.dims.zlo = 0;
     return with_op(r.op, [&](auto tag) {
         using OP = typename decltype(tag)::OP;
         using GEO = typename decltype(tag)::GEO;
-        if constexpr (GEO::D3)
+        if constexpr (OP::TIME) {
+            int st = launch_bwd<OP, GEO::TXB, GEO::TYb>(r, dloss, zc3<GEO>(r), loss);
+            if (st == FPDE_OK) st = launch_tm<OP>(r, dloss);
+            if (st == FPDE_OK && loss && !r.dims.per) st = launch_bc<OP>(r, dloss);
+            return st;
+        } else if constexpr (GEO::D3)
             return launch_bwd<OP, GEO::TXB, GEO::TYb>(r, dloss, zc3<GEO>(r), loss);
         else
             return loss ? launch_bwd<OP, kTX2V, 1>(r, dloss, zc2(r), loss)
@@ -462,7 +544,7 @@ int run_bc(const Req& r, const double* dloss) {
     });
 }
 
-int prepare_grad_call(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+int prepare_grad_call(int op, const fpde_grid4* grid, const fpde_coeffs* coeffs,
                       const float* const* fields, const float* const* consts, const double* dloss,
                       float* const* grads, void* stream, Req* r) {
     int st = validate_common(op, grid, coeffs, fields, consts, r);
@@ -491,7 +573,7 @@ extern "C" int fpde_op_info(int op, int* ndim, int* n_fields, int* n_consts, int
     return FPDE_OK;
 }
 
-extern "C" int fpde_residual_fwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+static int fwd_impl(int op, const fpde_grid4* grid, const fpde_coeffs* coeffs,
                                  const float* const* fields, const float* const* consts,
                                  float* const* residual_out, double* loss, void* stream) {
     Req r;
@@ -513,7 +595,7 @@ extern "C" int fpde_residual_fwd(int op, const fpde_grid* grid, const fpde_coeff
     return run_fwd(r, residual_out != nullptr, loss);
 }
 
-extern "C" int fpde_residual_bwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+static int bwd_impl(int op, const fpde_grid4* grid, const fpde_coeffs* coeffs,
                                  const float* const* fields, const float* const* consts,
                                  const double* dloss, float* const* grads, void* stream) {
     Req r;
@@ -522,7 +604,7 @@ extern "C" int fpde_residual_bwd(int op, const fpde_grid* grid, const fpde_coeff
     return run_bwd(r, dloss);
 }
 
-extern "C" int fpde_bc_correct(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+static int bc_impl(int op, const fpde_grid4* grid, const fpde_coeffs* coeffs,
                                const float* const* fields, const float* const* consts,
                                const double* dloss, float* const* grads, void* stream) {
     Req r;
@@ -531,7 +613,7 @@ extern "C" int fpde_bc_correct(int op, const fpde_grid* grid, const fpde_coeffs*
     return run_bc(r, dloss);
 }
 
-extern "C" int fpde_residual_value_and_grad(int op, const fpde_grid* grid,
+static int value_and_grad_impl(int op, const fpde_grid4* grid,
                                             const fpde_coeffs* coeffs, const float* const* fields,
                                             const float* const* consts, const double* dloss,
                                             double* loss, float* const* grads, void* stream) {
@@ -551,7 +633,7 @@ extern "C" int fpde_residual_value_and_grad(int op, const fpde_grid* grid,
     return run_bwd(r, dloss, loss);
 }
 
-extern "C" int fpde_residual_vjp(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+static int vjp_impl(int op, const fpde_grid4* grid, const fpde_coeffs* coeffs,
                                  const float* const* fields, const float* const* sens,
                                  int accumulate, float* const* grads, void* stream) {
     Req r;
@@ -580,6 +662,87 @@ extern "C" int fpde_residual_vjp(int op, const fpde_grid* grid, const fpde_coeff
     return run_vjp(r, accumulate == 1);
 }
 
+// fpde_grid (three axes) as fpde_grid4; ndim is checked against the op's later
+static const fpde_grid4* widen(const fpde_grid* g, fpde_grid4* w) {
+    if (!g) return nullptr;
+    memset(w, 0, sizeof *w);
+    w->ndim = g->ndim > 3 ? -1 : g->ndim;  // (four axes do not fit an fpde_grid)
+    w->bc_mode = g->bc_mode;
+    for (int a = 0; a < 3; ++a) {
+        w->n[a] = g->n[a];
+        w->h[a] = g->h[a];
+    }
+    return w;
+}
+
+extern "C" int fpde_residual_fwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+                                 const float* const* fields, const float* const* consts,
+                                 float* const* residual_out, double* loss, void* stream) {
+    fpde_grid4 w;
+    return fwd_impl(op, widen(grid, &w), coeffs, fields, consts, residual_out, loss, stream);
+}
+
+extern "C" int fpde_residual_bwd(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+                                 const float* const* fields, const float* const* consts,
+                                 const double* dloss, float* const* grads, void* stream) {
+    fpde_grid4 w;
+    return bwd_impl(op, widen(grid, &w), coeffs, fields, consts, dloss, grads, stream);
+}
+
+extern "C" int fpde_bc_correct(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+                               const float* const* fields, const float* const* consts,
+                               const double* dloss, float* const* grads, void* stream) {
+    fpde_grid4 w;
+    return bc_impl(op, widen(grid, &w), coeffs, fields, consts, dloss, grads, stream);
+}
+
+extern "C" int fpde_residual_value_and_grad(int op, const fpde_grid* grid,
+                                            const fpde_coeffs* coeffs, const float* const* fields,
+                                            const float* const* consts, const double* dloss,
+                                            double* loss, float* const* grads, void* stream) {
+    fpde_grid4 w;
+    return value_and_grad_impl(op, widen(grid, &w), coeffs, fields, consts, dloss, loss, grads,
+                               stream);
+}
+
+extern "C" int fpde_residual_vjp(int op, const fpde_grid* grid, const fpde_coeffs* coeffs,
+                                 const float* const* fields, const float* const* sens,
+                                 int accumulate, float* const* grads, void* stream) {
+    fpde_grid4 w;
+    return vjp_impl(op, widen(grid, &w), coeffs, fields, sens, accumulate, grads, stream);
+}
+
+extern "C" int fpde_residual_fwd4(int op, const fpde_grid4* grid, const fpde_coeffs* coeffs,
+                                  const float* const* fields, const float* const* consts,
+                                  float* const* residual_out, double* loss, void* stream) {
+    return fwd_impl(op, grid, coeffs, fields, consts, residual_out, loss, stream);
+}
+
+extern "C" int fpde_residual_bwd4(int op, const fpde_grid4* grid, const fpde_coeffs* coeffs,
+                                  const float* const* fields, const float* const* consts,
+                                  const double* dloss, float* const* grads, void* stream) {
+    return bwd_impl(op, grid, coeffs, fields, consts, dloss, grads, stream);
+}
+
+extern "C" int fpde_bc_correct4(int op, const fpde_grid4* grid, const fpde_coeffs* coeffs,
+                                const float* const* fields, const float* const* consts,
+                                const double* dloss, float* const* grads, void* stream) {
+    return bc_impl(op, grid, coeffs, fields, consts, dloss, grads, stream);
+}
+
+extern "C" int fpde_residual_value_and_grad4(int op, const fpde_grid4* grid,
+                                             const fpde_coeffs* coeffs, const float* const* fields,
+                                             const float* const* consts, const double* dloss,
+                                             double* loss, float* const* grads, void* stream) {
+    return value_and_grad_impl(op, grid, coeffs, fields, consts, dloss, loss, grads, stream);
+}
+
+extern "C" int fpde_residual_vjp4(int op, const fpde_grid4* grid, const fpde_coeffs* coeffs,
+                                  const float* const* fields, const float* const* sens,
+                                  int accumulate, float* const* grads, void* stream) {
+    return vjp_impl(op, grid, coeffs, fields, sens, accumulate, grads, stream);
+}
+
 extern "C" const char* fpde_status_string(int status) {
     switch (status) {
     case FPDE_OK: return "FPDE_OK";
@@ -594,4 +757,4 @@ extern "C" const char* fpde_status_string(int status) {
     }
 }
 
-extern "C" const char* fpde_version(void) { return "fpde 0.1 gfx950"; }
+extern "C" const char* fpde_version(void) { return "fpde 0.2 gfx950"; }

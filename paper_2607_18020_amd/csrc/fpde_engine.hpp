@@ -59,7 +59,7 @@ namespace fpde {
 
 struct Ptrs {
     const float* f[4];
-    const float* c[3];
+    const float* c[6];
     float* out[4];
     const float* s[4];  // caller-given residual sensitivities (explicit-sensitivity backward)
 };
@@ -72,6 +72,12 @@ struct Dims {
                             // marching kernels take it as their template argument PER
     int zlo;                // first marched plane: 1, or 0 when periodic or when the
                             // backward march also covers the end planes (value and grad)
+    // 3D+t grids (operators with TIME): the 3-D volume (nz, ny, nx) of one time
+    // level is what the kernels march; a launch covers the levels lev0 ..
+    // lev0 + nlev - 1 of the nt levels, vol nodes apart.  Other grids: nlev = nt
+    // = 1, lev0 = 0, vol = 0.
+    int nt, nlev, lev0;
+    long long vol;
 };
 
 // i in [-n, 2n) wrapped into [0, n) (periodic grids; a ragged tile reaches past n)
@@ -147,11 +153,17 @@ struct Ring {
 
 struct TileCoord {
     int gx0, gy0, z0, z1;
+    int lev;  // time level (3D+t grids; 0 otherwise)
 };
 
+// Workgroup -> (time level, x tile, y tile, chunk), the time level fastest: the
+// workgroups of neighbouring levels of one tile and chunk then run together on
+// one XCD, and the point values one reads from the other's level are in L2.
 template <int TX, int TY>
 __device__ __forceinline__ TileCoord tile_coord(const Dims& D) {
     int lb = remap_xcd(blockIdx.x, D.nblocks);
+    const int lev = D.lev0 + lb % D.nlev;
+    lb /= D.nlev;
     const int bx = lb % D.tiles_x;
     lb /= D.tiles_x;
     const int by = lb % D.tiles_y;
@@ -161,7 +173,33 @@ __device__ __forceinline__ TileCoord tile_coord(const Dims& D) {
     tc.gy0 = by * TY;
     tc.z0 = D.zlo + ch * D.zc;
     tc.z1 = min(tc.z0 + D.zc, D.nz - D.zlo);
+    tc.lev = lev;
     return tc;
+}
+
+// A 3D+t operator's arrays at time level lev: the fields, outputs and
+// sensitivities move to the level, and each const becomes the field TSRC[j] at
+// level lev + TOFF[j] (wrapped on a periodic grid).  No-op for other operators.
+template <class OP>
+__device__ __forceinline__ void time_level(Ptrs& P, const Dims& D, int lev) {
+    if constexpr (OP::TIME) {
+        const long long off = (long long)lev * D.vol;
+        const float* base[OP::NF];
+#pragma unroll
+        for (int f = 0; f < OP::NF; ++f) {
+            base[f] = P.f[f];
+            P.f[f] += off;
+            P.out[f] += off;
+        }
+#pragma unroll
+        for (int j = 0; j < OP::NC; ++j) {
+            int l = lev + OP::TOFF[j];
+            l = l < 0 ? l + D.nt : (l >= D.nt ? l - D.nt : l);
+            P.c[j] = base[OP::TSRC[j]] + (long long)l * D.vol;
+        }
+#pragma unroll
+        for (int b = 0; b < OP::NR; ++b) P.s[b] += off;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -362,6 +400,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
     FPDE_POISON_RING(sF);
     if (FPDE_LDS_POISON) __syncthreads();
     const TileCoord tc = tile_coord<TX, TY>(D);
+    time_level<OP>(P, D, tc.lev);
     const int z0 = tc.z0, z1 = tc.z1, L = z1 - z0;
     const int gx = tc.gx0 + tx, gy = (DIM == 3) ? tc.gy0 + ty : 0;
     const uint32_t pbytes = (uint32_t)D.ny * (uint32_t)D.nx * 4u;
@@ -516,6 +555,7 @@ __global__ __launch_bounds__(TX* TY) void fwdq_kernel(Ptrs P, Dims D, KCoef K, d
     constexpr uint32_t kOff = 0x80000000u;  // past every plane's range: reads 0
     const int t = threadIdx.x, tx = t % TX, ty = t / TX;
     const TileCoord tc = tile_coord<TX, TY>(D);
+    time_level<OP>(P, D, tc.lev);
     const int z0 = tc.z0, z1 = tc.z1, L = z1 - z0;
     const int gx = tc.gx0 + tx, gy = (DIM == 3) ? tc.gy0 + ty : 0;
     const uint32_t pbytes = (uint32_t)D.ny * (uint32_t)D.nx * 4u;
@@ -661,6 +701,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
     poison_lds(&sR[0][0][0], (int)(sizeof(sR) / 4));
     if (FPDE_LDS_POISON) __syncthreads();
     const TileCoord tc = tile_coord<TX, TY>(D);
+    time_level<OP>(P, D, tc.lev);
     const int z0 = tc.z0, z1 = tc.z1, L = z1 - z0;
     auto ph = [&](int w) {  // (wrapped into the grid when periodic)
         const int p = REV ? z1 - 1 - w : z0 + w;
@@ -942,12 +983,33 @@ __global__ __launch_bounds__(TX* TY, FPDE_VJP_MINW) void vjp_kernel(Ptrs P, Dims
     FPDE_POISON_RING(sF);
     if (FPDE_LDS_POISON) __syncthreads();
     const TileCoord tc = tile_coord<TX, TY>(D);  // (D.zlo = 0: every plane)
+    // 3D+t grids: the sensitivities of the velocity residuals at the own node of
+    // the neighbouring time levels (the time part of the transposed stencil),
+    // read as 0 off the residual set
+    const float* st[2][3] = {};
+    bool lok[2] = {false, false};
+    if constexpr (OP::TIME) {
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            int l = tc.lev + (k ? 1 : -1);
+            lok[k] = PER || (l >= 1 && l <= D.nt - 2);
+            l = l < 0 ? l + D.nt : (l >= D.nt ? l - D.nt : l);
+#pragma unroll
+            for (int q = 0; q < 3; ++q) st[k][q] = P.s[q] + (long long)l * D.vol;
+        }
+    }
+    time_level<OP>(P, D, tc.lev);
     const int z0 = tc.z0, z1 = tc.z1, L = z1 - z0;
     const int gx = tc.gx0 + tx, gy = (DIM == 3) ? tc.gy0 + ty : 0;
     const uint32_t pbytes = (uint32_t)D.ny * (uint32_t)D.nx * 4u;
     const bool inarr = gx < D.nx && gy < D.ny;
     const uint32_t cb = inarr ? (uint32_t)(gy * D.nx + gx) * 4u : 0u;
     auto zw = [&](int z) { return PER ? wrap_idx(z, D.nz) : z; };  // plane index
+    // own node on the residual set in the plane (the time-neighbour loads)
+    const uint32_t cbo =
+        (inarr && (PER || (gx >= 1 && gx <= D.nx - 2 && (DIM == 2 || (gy >= 1 && gy <= D.ny - 2)))))
+            ? cb
+            : 0x80000000u;
 
     // slot element -> grid position (the forward's layout); for the
     // sensitivities, positions off the residual set read as 0
@@ -976,12 +1038,15 @@ __global__ __launch_bounds__(TX* TY, FPDE_VJP_MINW) void vjp_kernel(Ptrs P, Dims
     psg.init(t, [&](int i, int& lin) { return node_at(i, lin, true); });
     // plane pz (wrapped or -1) of the fields and the sensitivities into a slot;
     // the sensitivities of a plane off the residual set read as 0
+    // (3D+t: the end time levels hold no residual node, so none of their
+    // sensitivities is read either)
+    const bool lev_om = !OP::TIME || PER || (tc.lev >= 1 && tc.lev <= D.nt - 2);
     auto load_plane = [&](int pz, auto slot) __attribute__((always_inline)) {
         float* dst[NA];
 #pragma unroll
         for (int a = 0; a < NA; ++a) dst[a] = &sF(slot)[a][0];
         if constexpr (NFG > 0) psf.template load<NFG>(P.f, pz, D.nz, pbytes, dst);
-        const bool gok = PER || (pz >= 1 && pz <= D.nz - 2);
+        const bool gok = lev_om && (PER || (pz >= 1 && pz <= D.nz - 2));
         psg.template load<NR>(P.s, gok ? pz : -1, D.nz, pbytes, dst + NFG);
     };
     float gq[2][NF];  // accumulate mode: the stored gradients of the next plane
@@ -991,26 +1056,38 @@ __global__ __launch_bounds__(TX* TY, FPDE_VJP_MINW) void vjp_kernel(Ptrs P, Dims
             for (int f = 0; f < NF; ++f) o[f] = bld(plane_rsrc_if(P.out[f], pz, pbytes, ok), cb);
         }
     };
+    float gt[2][2][3];  // 3D+t: [plane slot][t - 1, t + 1][velocity] of the next plane
+    auto load_gt = [&](int pz, bool ok, float (*o)[3]) __attribute__((always_inline)) {
+        if constexpr (OP::TIME) {
+            ok = ok && (PER || (pz >= 1 && pz <= D.nz - 2));
+#pragma unroll
+            for (int k = 0; k < 2; ++k)
+#pragma unroll
+                for (int q = 0; q < 3; ++q)
+                    o[k][q] = bld(plane_rsrc_if(st[k][q], pz, pbytes, ok && lok[k]), cbo);
+        }
+    };
 
     // plane z0 + j lives in slot (j + 1) & 3; prologue: planes z0-1, z0, z0+1
     load_plane(zw(z0 - 1), IC<0>{});
     load_plane(z0, IC<1>{});
     load_plane(zw(z0 + 1), IC<2>{});
     load_old(z0, true, gq[0]);
+    load_gt(z0, true, gt[0]);
     __syncthreads();
 
     const int own = (ty + HY) * LX + tx;  // own node in a slot
     const int xm = tx == 0 ? XG + ty : own - 1, xp = tx == TX - 1 ? XG + TY + ty : own + 1;
-    auto star = [&](auto sm, auto sc, auto sp, int a, Star& st) __attribute__((always_inline)) {
+    auto star = [&](auto sm, auto sc, auto sp, int a, Star& sv) __attribute__((always_inline)) {
         const float* c = &sF(sc)[a][0];
-        st.c = c[own];
-        st.m[0] = sF(sm)[a][own];
-        st.p[0] = sF(sp)[a][own];
-        st.m[DIM - 1] = c[xm];
-        st.p[DIM - 1] = c[xp];
+        sv.c = c[own];
+        sv.m[0] = sF(sm)[a][own];
+        sv.p[0] = sF(sp)[a][own];
+        sv.m[DIM - 1] = c[xm];
+        sv.p[DIM - 1] = c[xp];
         if (DIM == 3) {
-            st.m[1] = c[own - LX];
-            st.p[1] = c[own + LX];
+            sv.m[1] = c[own - LX];
+            sv.p[1] = c[own + LX];
         }
     };
     auto step = [&](auto jc, int w) __attribute__((always_inline)) {
@@ -1023,6 +1100,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_VJP_MINW) void vjp_kernel(Ptrs P, Dims
         load_plane(more ? zw(z + 2) : -1, IC<SQ>{});
         __builtin_amdgcn_sched_barrier(0);  // (the plane loads first, as in the forward)
         load_old(z + 1, more, gq[NXT]);
+        load_gt(zw(z + 1), more, gt[NXT]);
         Star fs[NF] = {}, gs[NR];
 #pragma unroll
         for (int f = 0; f < NFG; ++f) star(IC<SM>{}, IC<SC>{}, IC<SP>{}, f, fs[f]);
@@ -1030,6 +1108,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_VJP_MINW) void vjp_kernel(Ptrs P, Dims
         for (int b = 0; b < NR; ++b) star(IC<SM>{}, IC<SC>{}, IC<SP>{}, NFG + b, gs[b]);
         float g[NF];
         OP::gather(fs, gs, K, g);
+        if constexpr (OP::TIME) OP::add_time(gt[CUR][0], gt[CUR][1], K, g);
         const uint32_t so = inarr ? cb : kDropOff;
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
@@ -1117,6 +1196,182 @@ __global__ __launch_bounds__(256) void bc_kernel(Ptrs P, Dims D, KCoef K, const 
     }
 #pragma unroll
     for (int f = 0; f < NF; ++f) bst<kStream>(plane_rsrc(P.out[f], zn, pbytes), off, g[f]);
+}
+
+// ---------------------------------------------------------------------------
+// 3D+t grids (operators with TIME).  The marching kernels above run on one time
+// level per workgroup: their residuals read the velocities of the neighbouring
+// levels as point values, and their gather is the spatial part of the
+// transposed stencil.  The time part of the gather,
+//     dL/dc_q(n) += (R_q(n - e_t) - R_q(n + e_t)) / (2 h_t),
+// needs residuals of other time levels, which another workgroup evaluates.  So
+// tm_kernel recomputes them: one lane per spatial node marches the time levels
+// and keeps R_q of the levels t - 1, t, t + 1 in registers, so every residual is
+// evaluated once; each node's gradient is read, the time part added, and
+// written once (the march's spatial part is already there).  Only nodes on the
+// spatial residual set have a time part (R is zero off it).
+
+// The residuals of the velocity equations at one spatial node of level lev:
+// the spatial star of every field at lev and the velocities at lev -+ 1, loaded
+// through the levels' buffer descriptors (o: the node's byte offset in a level,
+// n[6]: its neighbours' at -+ one node along the three spatial axes).
+template <class OP, bool PER>
+__device__ __forceinline__ void residual_at_level(const Ptrs& P, const Dims& D, const KCoef& K,
+                                                  int lev, uint32_t vbytes, uint32_t o,
+                                                  const uint32_t* n, float* R) {
+    constexpr int NF = OP::NF, NC = OP::NC, D3 = OP::D;
+    Star st[NF];
+#pragma unroll
+    for (int f = 0; f < NF; ++f) {
+        const __amdgpu_buffer_rsrc_t r = plane_rsrc(P.f[f], lev, vbytes);
+        st[f].c = f < D3 ? bld(r, o) : 0.f;  // (the pressure's own value enters no residual)
+#pragma unroll
+        for (int a = 0; a < D3; ++a) {
+            st[f].m[a] = bld(r, n[2 * a]);
+            st[f].p[a] = bld(r, n[2 * a + 1]);
+        }
+    }
+    float c[NC];
+#pragma unroll
+    for (int j = 0; j < NC; ++j) {
+        int l = lev + OP::TOFF[j];
+        if (PER) l = l < 0 ? l + D.nt : (l >= D.nt ? l - D.nt : l);
+        c[j] = bld(plane_rsrc(P.f[OP::TSRC[j]], l, vbytes), o);
+    }
+    float Rf[OP::NR];
+    OP::residual(st, c, K, Rf);
+#pragma unroll
+    for (int q = 0; q < D3; ++q) R[q] = Rf[q];
+}
+
+template <class OP, bool PER>
+__global__ __launch_bounds__(256) void tm_kernel(Ptrs P, Dims D, KCoef K, const double* dloss,
+                                                 double two_over_M) {
+    constexpr int D3 = OP::D;
+    const int idx = (int)blockIdx.x * 256 + (int)threadIdx.x;  // spatial node (vol < 2^29)
+    if (idx >= (int)D.vol) return;
+    const int i3 = idx % D.nx, r = idx / D.nx, i2 = r % D.ny, i1 = r / D.ny;
+    if (!PER && !(i1 >= 1 && i1 <= D.nz - 2 && i2 >= 1 && i2 <= D.ny - 2 && i3 >= 1 &&
+                  i3 <= D.nx - 2))
+        return;  // off the spatial residual set: no time part
+    const uint32_t vbytes = (uint32_t)D.vol * 4u;
+    const uint32_t o = (uint32_t)idx * 4u;
+    // neighbours along x (array axis 1), y, z: -+1, wrapped on a periodic grid
+    uint32_t n[6];
+    {
+        const int sx = D.ny * D.nx, sy = D.nx;
+        auto at = [&](int a1, int a2, int a3) -> uint32_t {
+            if (PER) {
+                a1 = wrap_idx(a1, D.nz);
+                a2 = wrap_idx(a2, D.ny);
+                a3 = wrap_idx(a3, D.nx);
+            }
+            return (uint32_t)(a1 * sx + a2 * sy + a3) * 4u;
+        };
+        n[0] = at(i1 - 1, i2, i3);
+        n[1] = at(i1 + 1, i2, i3);
+        n[2] = at(i1, i2 - 1, i3);
+        n[3] = at(i1, i2 + 1, i3);
+        n[4] = at(i1, i2, i3 - 1);
+        n[5] = at(i1, i2, i3 + 1);
+    }
+    const float scale = (float)(two_over_M * (*dloss));
+    // levels whose gradient gets the time part: those the march wrote (all of
+    // them on a periodic grid, else 1 .. nt - 2, whose residual neighbours are
+    // the levels 0 .. nt - 1 with R zero at the end levels)
+    const int t0 = PER ? 0 : 1, t1 = PER ? D.nt - 1 : D.nt - 2;
+    auto R_of = [&](int lev, float* R) __attribute__((always_inline)) {
+        if (PER) lev = wrap_idx(lev, D.nt);
+        if (!PER && (lev < 1 || lev > D.nt - 2)) {
+#pragma unroll
+            for (int q = 0; q < D3; ++q) R[q] = 0.f;
+            return;
+        }
+        residual_at_level<OP, PER>(P, D, K, lev, vbytes, o, n, R);
+    };
+    float Rm[D3], Rc[D3], Rp[D3];
+    R_of(t0 - 1, Rm);
+    R_of(t0, Rc);
+    for (int t = t0; t <= t1; ++t) {
+        R_of(t + 1, Rp);
+        float tp[D3] = {};
+        OP::add_time(Rm, Rp, K, tp);
+#pragma unroll
+        for (int q = 0; q < D3; ++q) {
+            const __amdgpu_buffer_rsrc_t rg = plane_rsrc(P.out[q], t, vbytes);
+            const float g = bld(rg, o);
+            bst<kStream>(rg, o, fmaf(scale, tp[q], g));
+            Rm[q] = Rc[q];
+            Rc[q] = Rp[q];
+        }
+    }
+}
+
+// Boundary-gradient correction on a 3D+t grid: the end time levels t = 0 and
+// t = nt - 1 (the end planes of array axis 0), which the level marches do not
+// visit.  A node whose only boundary coordinate is t receives the time term of
+// its inward neighbour's residuals (level 1 or nt - 2); a node on the spatial
+// boundary as well touches no residual node and gets 0.  One workgroup per
+// 256-node segment of each (x, y) row of the two levels.
+template <class OP>
+__global__ __launch_bounds__(256) void bc4_kernel(Ptrs P, Dims D, KCoef K, const double* dloss,
+                                                  double two_over_M) {
+    constexpr int NF = OP::NF, NC = OP::NC, D3 = OP::D;
+    const int segs = (D.nx + 255) / 256;
+    int blk = blockIdx.x;
+    const int seg = blk % segs;
+    blk /= segs;
+    const int i2 = blk % D.ny;
+    blk /= D.ny;
+    const int i1 = blk % D.nz;
+    const bool low = blk / D.nz == 0;
+    const int i3 = seg * 256 + (int)threadIdx.x;
+    if (i3 >= D.nx) return;
+    const int tn = low ? 0 : D.nt - 1;  // the node's level
+    const int tm = low ? 1 : D.nt - 2;  // its inward neighbour's (the residual's)
+    const uint32_t vbytes = (uint32_t)D.vol * 4u;
+    const int sx = D.ny * D.nx, sy = D.nx;
+    const uint32_t off = (uint32_t)(i1 * sx + i2 * sy + i3) * 4u;
+    float g[NF];
+#pragma unroll
+    for (int f = 0; f < NF; ++f) g[f] = 0.f;
+    if (i1 >= 1 && i1 <= D.nz - 2 && i2 >= 1 && i2 <= D.ny - 2 && i3 >= 1 && i3 <= D.nx - 2 &&
+        D.nt >= 3) {
+        const uint32_t d[3] = {(uint32_t)sx * 4u, (uint32_t)sy * 4u, 4u};
+        Star st[NF];
+#pragma unroll
+        for (int f = 0; f < NF; ++f) {
+            const __amdgpu_buffer_rsrc_t r = plane_rsrc(P.f[f], tm, vbytes);
+            st[f].c = bld(r, off);
+#pragma unroll
+            for (int a = 0; a < D3; ++a) {
+                st[f].m[a] = bld(r, off - d[a]);
+                st[f].p[a] = bld(r, off + d[a]);
+            }
+        }
+        float c[NC];
+#pragma unroll
+        for (int j = 0; j < NC; ++j)
+            c[j] = bld(plane_rsrc(P.f[OP::TSRC[j]], tm + OP::TOFF[j], vbytes), off);
+        OP::bc_time(st, c, K, low ? -1.f : 1.f, g);
+        const float scale = (float)(two_over_M * (*dloss));
+#pragma unroll
+        for (int f = 0; f < NF; ++f) g[f] *= scale;
+    }
+#pragma unroll
+    for (int f = 0; f < NF; ++f) bst<kStream>(plane_rsrc(P.out[f], tn, vbytes), off, g[f]);
+}
+
+// Zeros of the residual arrays on the end time levels of a 3D+t grid (no
+// residual node there), for the forward that stores the residuals: the level
+// marches write every other node.
+template <int NR>
+__global__ __launch_bounds__(256) void zero_levels_kernel(Ptrs P, Dims D) {
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (i >= 2 * D.vol) return;
+    const long long at = i < D.vol ? i : i - D.vol + (long long)(D.nt - 1) * D.vol;
+#pragma unroll
+    for (int b = 0; b < NR; ++b) P.out[b][at] = 0.f;
 }
 
 }  // namespace fpde

@@ -55,6 +55,7 @@ struct KCoef {
     float k2;        // k^2
     float inv_dt;    // 1 / dt
     float alpha;
+    float i2ht;      // 1 / (2 h_t): the time axis of a 3D+t grid (axes a above are spatial)
 };
 
 __device__ __forceinline__ float d1(const Star& s, int a, const KCoef& K) {
@@ -74,6 +75,7 @@ __device__ __forceinline__ float lap(const Star& s, const KCoef& K) {
 //   R = u_t + u u_x - nu u_xx
 struct OpBurgers {
     static constexpr int DIM = 2, NF = 1, NC = 0, NR = 1, NG = 0, NFG = 1;
+    static constexpr bool TIME = false;  // (see OpNS3T)
 
     __device__ __forceinline__ static void residual(const Star* f, const float*, const KCoef& K, float* R) {
         const Star& u = f[0];
@@ -111,6 +113,7 @@ struct OpBurgers {
 // Helmholtz: R = lap u + k^2 u - f   (self-adjoint: dL/du = k^2 R + lap R).
 struct OpHelmholtz {
     static constexpr int DIM = 2, NF = 1, NC = 1, NR = 1, NG = 0, NFG = 0;
+    static constexpr bool TIME = false;  // (see OpNS3T)
 
     __device__ __forceinline__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
         R[0] = lap<2>(f[0], K) + K.k2 * f[0].c - c[0];
@@ -136,6 +139,7 @@ struct OpHelmholtz {
 // One implicit heat step: R = (u - u0)/dt - alpha lap u.
 struct OpHeat {
     static constexpr int DIM = 3, NF = 1, NC = 1, NR = 1, NG = 0, NFG = 0;
+    static constexpr bool TIME = false;  // (see OpNS3T)
 
     __device__ __forceinline__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
         R[0] = (f[0].c - c[0]) * K.inv_dt - K.alpha * lap<3>(f[0], K);
@@ -165,6 +169,7 @@ struct OpHeat {
 template <int D, bool UNSTEADY>
 struct OpNS {
     static constexpr int DIM = D, NF = D + 1, NC = UNSTEADY ? D : 0, NR = D + 1, NG = D, NFG = D;
+    static constexpr bool TIME = false;  // (see OpNS3T)
 
     __device__ __forceinline__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
         float cs[D];  // c_a / (2 h_a), shared by the D momentum equations
@@ -248,6 +253,7 @@ using OpNS3S = OpNS<3, false>;  // steady 3D NS
 template <int D>
 struct OpPoisson {
     static constexpr int DIM = D, NF = 1, NC = 1, NR = 1, NG = 0, NFG = 0;
+    static constexpr bool TIME = false;  // (see OpNS3T)
 
     __device__ __forceinline__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
         R[0] = lap<D>(f[0], K) - c[0];
@@ -278,6 +284,7 @@ struct OpPoisson {
 struct OpNST {
     static constexpr int D = 2;  // spatial dimensions
     static constexpr int DIM = 3, NF = D + 1, NC = 0, NR = D + 1, NG = D, NFG = D;
+    static constexpr bool TIME = false;  // (see OpNS3T)
 
     __device__ __forceinline__ static float lap_xy(const Star& s, const KCoef& K) {
         float l = 0.f;
@@ -360,6 +367,112 @@ struct OpNST {
             }
             g[D] = R[S_] * t * K.i2h[AX];
         }
+    }
+};
+
+// ---------------------------------------------------------------------------
+// Unsteady incompressible NS on a 3D+t space-time grid (t, x, y, z): array
+// axis 0 is t (a centred difference in time, step h_t), velocity component b
+// on array axis b + 1, pressure last.
+//   R_b = D1_t c_b + sum_a c_a D1_a c_b + D1_b p - nu lap c_b      (a, b over x, y, z)
+//   R_div = sum_a D1_a c_a
+// The kernels run the 3-D engine on one time level t at a time (TIME): the
+// stars here are spatial (index a = spatial axis a, array axis a + 1) and the
+// velocities at the neighbouring time levels enter as point values, the consts
+// c[0..2] = c_b(t - 1) and c[3..5] = c_b(t + 1) (TSRC / TOFF: the field and
+// the time offset each const is read from).  The gather below is the spatial
+// part of the transposed stencil; its time part, (R_q(t-1) - R_q(t+1)) / (2 h_t),
+// needs the residuals of other time levels and is added by the time-march
+// kernel (or, from given sensitivities, by the explicit-sensitivity backward).
+struct OpNS3T {
+    static constexpr int D = 3;  // spatial dimensions
+    static constexpr int DIM = 3, NF = D + 1, NC = 2 * D, NR = D + 1, NG = D, NFG = D;
+    static constexpr bool TIME = true;
+    static constexpr int TSRC[2 * D] = {0, 1, 2, 0, 1, 2};
+    static constexpr int TOFF[2 * D] = {-1, -1, -1, 1, 1, 1};
+
+    __device__ __forceinline__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
+        float cs[D];  // c_a / (2 h_a), shared by the momentum equations
+#pragma unroll
+        for (int a = 0; a < D; ++a) cs[a] = f[a].c * K.i2h[a];
+        double div = 0.0;
+#pragma unroll
+        for (int b = 0; b < D; ++b) {
+            float r = (c[D + b] - c[b]) * K.i2ht;  // time derivative
+#pragma unroll
+            for (int a = 0; a < D; ++a) r = fmaf(cs[a], f[b].p[a] - f[b].m[a], r);
+            r = fmaf(f[D].p[b] - f[D].m[b], K.i2h[b], r);
+            R[b] = fmaf(-K.nu, lap<D>(f[b], K), r);
+            div = fma((double)f[b].p[b] - (double)f[b].m[b], K.i2hd[b], div);
+        }
+        R[D] = (float)div;
+    }
+
+    // spatial part of dL/dc_q(n): sum_b R_b(n) D1_q c_b(n)
+    //   + sum_a (R_q(n-e_a) c_a(n-e_a) - R_q(n+e_a) c_a(n+e_a)) / (2 h_a)
+    //   + (R_div(n-e_q) - R_div(n+e_q)) / (2 h_q) - nu lap R_q(n);
+    // dL/dp(n) = sum_b (R_b(n-e_b) - R_b(n+e_b)) / (2 h_b)
+    __device__ __forceinline__ static void gather_self(const Star* f, const float* R, const KCoef& K, float* S) {
+#pragma unroll
+        for (int q = 0; q < D; ++q) {
+            float loc = R[0] * (f[0].p[q] - f[0].m[q]);
+#pragma unroll
+            for (int b = 1; b < D; ++b) loc = fmaf(R[b], f[b].p[q] - f[b].m[q], loc);
+            S[q] = loc * K.i2h[q];
+        }
+    }
+
+    __device__ __forceinline__ static void gather_rest(const Star* f, const Star* r, const float* S, const KCoef& K, float* g) {
+        float gp = 0.f;
+#pragma unroll
+        for (int q = 0; q < D; ++q) {
+            float acc = S[q];
+#pragma unroll
+            for (int a = 0; a < D; ++a)
+                acc = fmaf(fmaf(r[q].m[a], f[a].m[a], -(r[q].p[a] * f[a].p[a])), K.i2h[a], acc);
+            acc = fmaf(r[D].m[q] - r[D].p[q], K.i2h[q], acc);
+            g[q] = fmaf(-K.nu, lap<D>(r[q], K), acc);
+            gp = fmaf(r[q].m[q] - r[q].p[q], K.i2h[q], gp);
+        }
+        g[D] = gp;
+    }
+
+    __device__ __forceinline__ static void gather(const Star* f, const Star* r, const KCoef& K, float* g) {
+        float R[NR], S[D];
+#pragma unroll
+        for (int b = 0; b < NR; ++b) R[b] = r[b].c;
+        gather_self(f, R, K, S);
+        gather_rest(f, r, S, K, g);
+    }
+
+    // the time part for velocity q from the residuals (or sensitivities) of its
+    // own node at t - 1 (rm) and t + 1 (rp), added after the spatial part
+    __device__ __forceinline__ static void add_time(const float* rm, const float* rp, const KCoef& K, float* g) {
+#pragma unroll
+        for (int q = 0; q < D; ++q) g[q] = fmaf(rm[q] - rp[q], K.i2ht, g[q]);
+    }
+
+    // n = m + t e_AX on a spatial axis AX: only the neighbour terms of R_b(m) reach n
+    template <int AX>
+    __device__ __forceinline__ static void bc_term(const Star* f, const float* c, const KCoef& K, float t, float* g) {
+        float R[NR];
+        residual(f, c, K, R);
+#pragma unroll
+        for (int q = 0; q < D; ++q) {
+            float v = R[q] * (t * f[AX].c * K.i2h[AX] - K.nu * K.ih2[AX]);
+            if (q == AX) v += R[D] * t * K.i2h[AX];
+            g[q] = v;
+        }
+        g[D] = R[AX] * t * K.i2h[AX];
+    }
+
+    // n = m + t e_t (an end time level): only the time derivative of R_q(m) reaches n
+    __device__ __forceinline__ static void bc_time(const Star* f, const float* c, const KCoef& K, float t, float* g) {
+        float R[NR];
+        residual(f, c, K, R);
+#pragma unroll
+        for (int q = 0; q < D; ++q) g[q] = R[q] * t * K.i2ht;
+        g[D] = 0.f;
     }
 };
 

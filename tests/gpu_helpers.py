@@ -8,6 +8,13 @@ TOL_RES = 1e-5
 TOL_GRAD = 1e-4
 
 
+def normal_shape(op):
+    """A ragged grid for the paper's N(0,1) verification inputs, by operator rank:
+    several tiles and chunks with ragged tails (four axes: several time levels)."""
+    from paper_2607_18020_amd import workloads as W  # noqa: PLC0415
+    return {2: (37, 291), 3: (13, 19, 75), 4: (6, 9, 11, 75)}[W.OPS[op].ndim]
+
+
 def interior(a):
     return a[tuple(slice(1, n - 1) for n in a.shape)]
 

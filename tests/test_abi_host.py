@@ -8,6 +8,7 @@ from __future__ import annotations
 import ctypes
 import os
 import re
+import types
 
 import pytest
 
@@ -43,14 +44,12 @@ def test_library_exports_every_declared_symbol(B):
 
 def test_op_info_matches_workload_registry(B):
     for op, spec in W.OPS.items():
-        if op == W.NS_3DT:  # the oracle's 4-D operator; the library's comes with its kernels
-            continue
         ndim, nf, nc, nr = B.op_info(op)
         assert (ndim, nf, nc, nr) == (spec.ndim, len(spec.fields), len(spec.consts), len(spec.residuals))
     with pytest.raises(B.FpdeError):
         B.op_info(0)
     with pytest.raises(B.FpdeError):
-        B.op_info(len(W.OPS) + 2)
+        B.op_info(len(W.OPS) + 1)
 
 
 def test_status_strings_and_version(B):
@@ -79,11 +78,21 @@ def _arr(vals):
 
 def _call(B, fn, op, shape, h=None, coef=W.Coeffs(nu=0.01, k=1.0, dt=0.1, alpha=0.1),
           fields=None, consts=None, outs=None, scalar=None, bc_mode=0, ndim=None, sens=None,
-          accumulate=0, loss=None):
-    lib = B.lib()
+          accumulate=0, loss=None, four=False):
+    """One call of entry point `fn`; four-axis grids (or four=True) go through
+    the entry points taking fpde_grid4."""
     spec = W.OPS[op]
     h = h if h is not None else (0.1,) * len(shape)
+    four = four or len(shape) == 4
     g = B.make_grid(shape, h, bc_mode)
+    if four and len(shape) < 4:
+        g4 = B.FpdeGrid4()
+        g4.ndim, g4.bc_mode = g.ndim, g.bc_mode
+        for a in range(len(shape)):
+            g4.n[a], g4.h[a] = g.n[a], g.h[a]
+        g = g4
+    lib = types.SimpleNamespace(**{n: getattr(B.lib(), n + ("4" if four else ""))
+                                   for n in B.CALLS})
     if ndim is not None:
         g.ndim = ndim
     c = B.make_coeffs(coef)
@@ -151,6 +160,31 @@ def test_validation_status_codes(B, fn):
     # every launch shape stays below 2^31 workgroups (so the node count below 2^36)
     assert _call(B, fn, op2, (1 << 26, 1 << 10)) == SHAPE
     assert _call(B, fn, op3, (1 << 20, 1 << 10, 1 << 10)) == SHAPE
+
+
+@pytest.mark.parametrize("fn", ["fwd", "bwd", "bc", "vjp", "vg"])
+def test_validation_four_axis_grids(B, fn):
+    """fpde_grid4 and the entry points ending in 4: the 3D+t operator's grid,
+    and every other op through the same calls."""
+    op = W.NS_3DT
+    s4 = (6, 7, 8, 9)
+    assert _call(B, fn, op, s4, ndim=3) == SHAPE
+    assert _call(B, fn, op, (2, 7, 8, 9)) == SHAPE
+    assert _call(B, fn, op, (6, 7, 8, 2)) == SHAPE
+    assert _call(B, fn, op, s4, h=(0.0, 0.1, 0.1, 0.1)) == SPACING  # the time step
+    assert _call(B, fn, op, s4, h=(0.1, 0.1, 0.1, float("inf"))) == SPACING
+    assert _call(B, fn, op, s4, coef=W.Coeffs(nu=float("nan"))) == COEFF
+    assert _call(B, fn, op, s4, fields=[_addr(0), _addr(1), 0, _addr(3)]) == ARG
+    assert _call(B, fn, op, s4, fields=[_addr(0), _addr(1), _addr(2, 2), _addr(3)]) == ALIGN
+    assert _call(B, fn, op, s4, bc_mode=2) == ARG
+    # a time level (the last three axes) below 2^29 nodes; the launches below 2^31 workgroups
+    assert _call(B, fn, op, (3, 1 << 10, 1 << 10, 1 << 9)) == SHAPE
+    assert _call(B, fn, op, (1 << 20, 1 << 8, 1 << 8, 1 << 8)) == SHAPE
+    # the three-axis ops through fpde_grid4, and four axes refused by fpde_grid
+    assert _call(B, fn, W.NS_3D_BE, (8, 9, 10), ndim=2, four=True) == SHAPE
+    assert _call(B, fn, W.NS_3D_BE, (8, 9, 10), h=(0.1, 0.0, 0.1), four=True) == SPACING
+    assert _call(B, fn, W.NS_2D_STEADY, (9, 2), four=True) == SHAPE
+    assert _call(B, fn, W.NS_3D_BE, (8, 9, 10), ndim=4) == SHAPE
 
 
 def test_output_checks(B):

@@ -1,5 +1,5 @@
 """GPU parity of the adjacent operators (steady 3D NS, 2D and 3D Poisson,
-unsteady 2D NS on a space-time grid): every entry point against the oracle,
+unsteady 2D and 3D NS on space-time grids): every entry point against the oracle,
 node by node, in both boundary modes, on small, ragged and multi-chunk grids
 and on the full-size workloads."""
 from __future__ import annotations
@@ -21,6 +21,9 @@ CASES = [
     ("poisson_3d", (9, 10, 300)), ("poisson_3d", (42, 256, 256)),
     ("ns_2dt", (3, 3, 3)), ("ns_2dt", (4, 9, 66)), ("ns_2dt", (19, 21, 70)),
     ("ns_2dt", (40, 17, 129)), ("ns_2dt", (7, 9, 300)), ("ns_2dt", (42, 256, 256)),
+    # 3D+t: several time levels, several tiles and chunks of each level, ragged tails
+    ("ns_3dt", (3, 3, 3, 3)), ("ns_3dt", (4, 5, 9, 66)), ("ns_3dt", (6, 19, 21, 70)),
+    ("ns_3dt", (5, 12, 17, 129)), ("ns_3dt", (4, 7, 9, 300)), ("ns_3dt", (9, 40, 20, 33)),
 ]
 IDS = [f"{c}-{'x'.join(map(str, s))}" for c, s in CASES]
 
@@ -93,10 +96,10 @@ def test_adjacent_vjp_and_value_and_grad(oracle_mod, cfg, shape, bc_mode):
                  oracle_mod.grad(*args, dloss=0.6, bc_mode=bc_mode), "value_and_grad " + what)
 
 
-@pytest.mark.parametrize("op", [W.NS_3D_STEADY, W.POISSON_2D, W.POISSON_3D, W.NS_2DT])
+@pytest.mark.parametrize("op", [W.NS_3D_STEADY, W.POISSON_2D, W.POISSON_3D, W.NS_2DT, W.NS_3DT])
 def test_adjacent_normal_inputs(oracle_mod, op):
     """N(0,1) fields (the paper's verification inputs), seeds 42-46."""
-    shape = (37, 291) if W.OPS[op].ndim == 2 else (13, 19, 75)
+    shape = H.normal_shape(op)
     for seed in (42, 43, 44, 45, 46):
         wl = W.normal_fields(op, shape, seed)
         print(f"case adjacent normal op={op} seed={seed}", flush=True)

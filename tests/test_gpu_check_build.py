@@ -26,7 +26,8 @@ CASES = [
     ("ns_3d_tgv", (42, 256, 256)), ("heat_3d", (19, 21, 70)), ("heat_3d", (9, 10, 300)),
     ("ns_2d", (71, 600)), ("ns_2d", (13400, 40)), ("burgers_1dt", (41, 300)),
     ("helmholtz_2d", (67, 513)), ("ns_3d_steady", (19, 21, 70)), ("poisson_3d", (33, 40, 130)),
-    ("poisson_2d", (30, 700)), ("ns_2dt", (9, 20, 70)),
+    ("poisson_2d", (30, 700)), ("ns_2dt", (9, 20, 70)), ("ns_3dt", (6, 19, 21, 70)),
+    ("ns_3dt", (5, 12, 17, 300)),
 ]
 
 

@@ -73,7 +73,7 @@ def test_value_and_grad_parity(oracle_mod, cfg, shape, bc_mode):
 
 @pytest.mark.parametrize("op", sorted(W.OPS))
 def test_value_and_grad_normal_inputs(oracle_mod, op):
-    shape = (37, 291) if W.OPS[op].ndim == 2 else (13, 19, 75)
+    shape = H.normal_shape(op)
     wl = W.normal_fields(op, shape, 45)
     print(f"case value_and_grad normal op={op} {shape}", flush=True)
     _check(oracle_mod, wl, 1.0, 0, f"vg normal op{op}")

@@ -61,7 +61,7 @@ def test_parity_small_and_ragged(oracle_mod, cfg, shape):
 @pytest.mark.parametrize("seed", [42, 43, 44, 45, 46])
 def test_parity_normal_inputs_seeds(oracle_mod, op, seed):
     """The paper's verification inputs (App. A.7): N(0,1) fields, seeds 42-46."""
-    shape = (37, 291) if W.OPS[op].ndim == 2 else (13, 19, 75)
+    shape = H.normal_shape(op)
     wl = W.normal_fields(op, shape, seed)
     print(f"case op={op} seed={seed} {shape}", flush=True)
     R, L, g = H.run_gpu(wl, dloss=1.0)

@@ -60,7 +60,7 @@ def test_periodic_parity(oracle_mod, cfg, shape):
 @pytest.mark.parametrize("op", sorted(W.OPS))
 def test_periodic_normal_inputs(oracle_mod, op):
     """The paper's N(0,1) verification inputs, on a wrapped grid."""
-    shape = (37, 291) if W.OPS[op].ndim == 2 else (13, 19, 75)
+    shape = H.normal_shape(op)
     wl = W.normal_fields(op, shape, 44)
     print(f"case periodic op={op} {shape}", flush=True)
     _compare(oracle_mod, wl, 1.0, f"periodic normal op{op}")

@@ -74,7 +74,7 @@ def test_vjp_parity(oracle_mod, cfg, shape, bc_mode):
 @pytest.mark.parametrize("op", sorted(W.OPS))
 def test_vjp_normal_inputs(oracle_mod, op, bc_mode):
     """N(0,1) fields and sensitivities (the paper's verification inputs)."""
-    shape = (37, 291) if W.OPS[op].ndim == 2 else (13, 19, 75)
+    shape = H.normal_shape(op)
     wl = W.normal_fields(op, shape, 42)
     G = W.sensitivities(op, shape, 46)
     print(f"case vjp normal op={op} {shape} bc_mode={bc_mode}", flush=True)
@@ -87,7 +87,7 @@ def test_vjp_ignores_sensitivities_off_the_residual_set():
     """Entries of G on the boundary shell are never read: NaN or huge values
     there give bitwise the result of zeros there."""
     for cfg, shape in (("ns_3d_tgv", (9, 12, 70)), ("ns_2d", (9, 260)), ("heat_3d", (5, 67, 3)),
-                       ("burgers_1dt", (3, 300))):
+                       ("burgers_1dt", (3, 300)), ("ns_3dt", (5, 6, 12, 70))):
         wl = W.make(cfg, seed=49, shape=shape)
         G = W.sensitivities(wl.op, shape, 50)
         sm = H.shell_mask(shape)
