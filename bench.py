@@ -297,16 +297,18 @@ OP_KERNEL_TAG = {1: "OpBurgers", 2: "OpHelmholtz", 3: "OpHeat", 4: "OpNS<2, fals
 
 def measured_traffic(cfg, op, kernels, path="loss"):
     """HBM bytes per launch from the committed rocprofv3 counter summary of this
-    bench path, summed over `kernels` (name stems such as "bwd", "fill_f64"), if
-    it was taken on this workload with the current kernel sources; else None."""
+    workload and bench path (profiles/traffic_*.json), summed over `kernels`
+    (name stems such as "bwd", "fill_f64"), if it was taken with the current
+    kernel sources; else None."""
+    import glob  # noqa: PLC0415
+
     from paper_2607_18020_amd import profiling  # noqa: PLC0415
-    fn = os.path.join(ROOT, "profiles", f"traffic_{path}.json")
-    if not os.path.exists(fn):
-        return None
-    rec = json.load(open(fn))
-    if rec.get("source_hash") != profiling.source_hash() or not rec.get("workload", "").startswith(cfg):
-        return None
-    if rec.get("path") != path:
+    rec = None
+    for fn in sorted(glob.glob(os.path.join(ROOT, "profiles", "traffic_*.json"))):
+        r = json.load(open(fn))
+        if r.get("path") == path and r.get("workload", "").split(" ")[0] == cfg:
+            rec = r
+    if rec is None or rec.get("source_hash") != profiling.source_hash():
         return None
     total = 0.0
     for stem in kernels:

@@ -11,9 +11,10 @@ file name.)
 Traffic calibration: FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are scaled by
 what the same counters read for the benchmark's stream kernel (y = 1 * x over
 1 GiB: 1 GiB read, 1 GiB written), so the figures are bytes, whatever the
-counters' own unit and coverage.  ``traffic_<PATH>.json`` records a hash of the kernel
-sources (comments and whitespace ignored); ``bench.py`` reports the traffic
-only while that hash still matches.
+counters' own unit and coverage.  ``traffic_<STEM>.json`` records the workload,
+the bench path and a hash of the kernel sources (comments and whitespace
+ignored); ``bench.py`` reports the traffic of the record for its workload and
+path only while that hash still matches.
 """
 from __future__ import annotations
 
@@ -31,6 +32,9 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = ("csrc/fpde.hip", "csrc/fpde_engine.hpp", "csrc/fpde_ops.hpp")
 STREAM_KERNEL = "MulFunctor"  # the benchmark's 1 GiB y = 1 * x kernel
 STREAM_BYTES = 1 << 30
+# the library's kernels (name stems)
+KERNELS = ("fwd_kernel", "fwdq_kernel", "bwd_kernel", "bc_kernel", "bc4_kernel", "vjp_kernel",
+           "tm_kernel", "zero_levels_kernel", "fill_f64")
 
 
 def _code_only(text: str) -> str:
@@ -87,7 +91,7 @@ def calibrated(pmc_dir: str, counter: str) -> Dict[str, dict]:
     factor = STREAM_BYTES / ref_kib  # bytes per counted KiB
     out = {"_calibration": {"stream_kib": ref_kib, "bytes_per_kib": factor}}
     for k, vs in vals.items():
-        if k.startswith(("fwd_kernel", "bwd_kernel", "bc_kernel", "vjp_kernel", "fill_f64")):
+        if k.startswith(KERNELS):
             avg = sum(vs) / len(vs)
             out[k] = {"dispatches": len(vs), "avg_kib": avg, "bytes": avg * factor}
     return out
@@ -115,8 +119,7 @@ def main():
     sha = source_hash()
     os.makedirs(a.out, exist_ok=True)
 
-    kern = sorted(k for k in stats
-                  if k.startswith(("fwd_kernel", "bwd_kernel", "bc_kernel", "vjp_kernel", "fill")))
+    kern = sorted(k for k in stats if k.startswith(KERNELS))
     lines = [f"# Kernel timings and HBM traffic, {a.workload}, bench.py --path {a.path}", "",
              "Commands (run from the repository root on one MI355X):", "", "```", cmds, "```", "",
              f"Kernel sources hash (comments and whitespace ignored): `{sha}`.", "",
@@ -145,7 +148,7 @@ def main():
         traffic[k] = {"fetch_bytes": fb, "write_bytes": wb}
     with open(os.path.join(a.out, a.name + ".md"), "w") as f:
         f.write("\n".join(lines) + "\n")
-    with open(os.path.join(a.out, f"traffic_{a.path}.json"), "w") as f:
+    with open(os.path.join(a.out, f"traffic_{a.name}.json"), "w") as f:
         json.dump({"source_hash": sha, "workload": a.workload, "path": a.path, "kernels": traffic,
                    "calibration": {"fetch": fetch["_calibration"], "write": write["_calibration"]}},
                   f, indent=1)
