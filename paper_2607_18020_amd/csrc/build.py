@@ -2,7 +2,8 @@
 
 Usage: python -m paper_2607_18020_amd.csrc.build [--save-temps]
 Writes paper_2607_18020_amd/libfpde.so.  Packed-FP32 VALU ops are disabled
-for all device code; float64 atomics use the native global_atomic_add_f64.
+for all device code; float64 atomics use the native global_atomic_add_f64;
+floating-point contraction is off (the operators' fmaf are explicit).
 """
 from __future__ import annotations
 
@@ -24,6 +25,9 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
     "-munsafe-fp-atomics",
+    # no implicit fusing of a multiply and an add: the operators write their fmaf
+    # explicitly, so each one is the same instruction sequence in every kernel
+    "-ffp-contract=off",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-command-line-argument",
     "-I", os.path.join(ROOT, "include"), "-I", HERE,
@@ -44,6 +48,7 @@ CHECK_FLAGS = [
     "-DFPDE_HEAT_MIN_BWD_BLOCKS=256", "-DFPDE_VJP_TY3=8", "-DFPDE_VJP_HEAT_TX=64",
     "-DFPDE_TX2=128", "-DFPDE_TX2_FWD=256", "-DFPDE_TX2_VG=256", "-DFPDE_BLOCKS2=512",
     "-DFPDE_FWD2_Q=4", "-DFPDE_HEAT_FWD_QUEUE=1", "-DFPDE_NS4_BWD_TX=64", "-DFPDE_NS4_BWD_TY=8",
+    "-DFPDE_BWD2_QUEUE=1", "-DFPDE_NS4_MIN_BLOCKS=700",
 ]
 
 _NOISE = "is not a recognized feature for this target"

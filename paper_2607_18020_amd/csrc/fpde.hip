@@ -74,6 +74,20 @@ namespace {
 #ifndef FPDE_HEAT_FWD_QUEUE
 #define FPDE_HEAT_FWD_QUEUE 0
 #endif
+// 2-D backward: the LDS march (bwd_kernel with one-row tiles); the checking
+// build takes the register-queue march (bwdq_kernel: no LDS, no barrier; NW
+// waves of 62 output columns, Q rows in registers) as a second algorithm whose
+// gradients must match bit for bit.  (The queue march is no faster for the
+// product: NS-2D 2048^2 37.8 against 36.7 us per step.)
+#ifndef FPDE_BWD2_QUEUE
+#define FPDE_BWD2_QUEUE 0
+#endif
+#ifndef FPDE_BWD2_NW
+#define FPDE_BWD2_NW 4
+#endif
+#ifndef FPDE_BWD2_Q
+#define FPDE_BWD2_Q 7
+#endif
 // 2-D one-pass value and gradient (the backward with the loss atomics)
 #ifndef FPDE_TX2_VG
 #define FPDE_TX2_VG 512
@@ -131,8 +145,14 @@ using GeoNS3 = Geo3<FPDE_NS3_FWD_TX, FPDE_NS3_FWD_TY, FPDE_NS3_BWD_TX, FPDE_NS3_
 #ifndef FPDE_NS4_BWD_TY
 #define FPDE_NS4_BWD_TY 4
 #endif
+// workgroups per launch: a time level is a 3-D volume of its own, so whole-level
+// chunks leave few workgroups (and a last round of them mostly idle) on the
+// smaller volumes of space-time grids; chunks are cut for many rounds instead
+#ifndef FPDE_NS4_MIN_BLOCKS
+#define FPDE_NS4_MIN_BLOCKS 2048
+#endif
 using GeoNS4 = Geo3<FPDE_NS3_FWD_TX, FPDE_NS3_FWD_TY, FPDE_NS4_BWD_TX, FPDE_NS4_BWD_TY,
-                    FPDE_NS3_MIN_BWD_BLOCKS, FPDE_VJP_TX3, FPDE_VJP_TY3>;
+                    FPDE_NS4_MIN_BLOCKS, FPDE_VJP_TX3, FPDE_VJP_TY3>;
 // one field, a Laplacian (heat, Poisson)
 using GeoHeat = Geo3<FPDE_HEAT_FWD_TX, FPDE_HEAT_FWD_TY, FPDE_HEAT_BWD_TX, FPDE_HEAT_BWD_TY,
                      FPDE_HEAT_MIN_BWD_BLOCKS, FPDE_VJP_HEAT_TX, FPDE_VJP_HEAT_TY,
@@ -315,12 +335,17 @@ Dims tile_dims(const Dims& n, int TX, int TY, int zc) {
 }
 
 // Chunk length giving a launch with TX x TY tiles about `target` workgroups
-// (each chunk at least one plane; 3D+t grids: over all launched levels).
+// (each chunk at least one plane; 3D+t grids: over all launched levels, and at
+// least kMinChunkT planes, as a chunk of a few planes re-reads its halo planes
+// and its march prologue for little work).
+constexpr int kMinChunkT = 8;
 int chunk_planes(const Dims& n, int TX, int TY, int target) {
     const long long tiles =
         (long long)((n.nx + TX - 1) / TX) * ((n.ny + TY - 1) / TY) * n.nlev;
     const int nplanes = n.nz - 2 * n.zlo;
     long long nch = (target + tiles - 1) / tiles;
+    if (n.nt > 1 && nch > (nplanes + kMinChunkT - 1) / kMinChunkT)
+        nch = (nplanes + kMinChunkT - 1) / kMinChunkT;
     if (nch < 1) nch = 1;
     if (nch > nplanes) nch = nplanes;
     return (int)((nplanes + nch - 1) / nch);
@@ -429,6 +454,19 @@ int launch_bwd(const Req& r, const double* dloss, int zc, double* loss) {
     return st;
 }
 
+// 2-D register-queue backward (the gradient alone)
+template <class OP>
+int launch_bwdq(const Req& r, const double* dloss, int zc) {
+    constexpr int NW = FPDE_BWD2_NW;
+    const Dims dm = tile_dims(r.dims, 62 * NW, 1, zc);
+    int st = FPDE_OK;
+    with_flag(dm.per, [&](auto per) {
+        st = launch(bwdq_kernel<OP, NW, FPDE_BWD2_Q, decltype(per)::value>, dim3(dm.nblocks),
+                    dim3(64 * NW), r.stream, r.P, dm, r.K, dloss, r.two_over_M);
+    });
+    return st;
+}
+
 // 3-D: the chunk length shared by the forward and the backward
 template <class GEO>
 int zc3(const Req& r) {
@@ -439,9 +477,9 @@ int zc2(const Req& r) { return chunk_planes(r.dims, kTX2, 1, kTargetBlocks2); }
 template <class OP>
 int launch_bc(const Req& r, const double* dloss) {
     if constexpr (OP::TIME) {
-        // 3D+t: the two end time levels, one workgroup per 256-node segment of
-        // each (x, y) row (fewer than 2^31: a level holds fewer than 2^29 nodes)
-        const long long nb = 2LL * r.dims.nz * r.dims.ny * ((r.dims.nx + 255) / 256);
+        // 3D+t: the two end time levels, 256 consecutive nodes of a level per
+        // workgroup (fewer than 2^31: a level holds fewer than 2^29 nodes)
+        const long long nb = 2 * ((r.dims.vol + 255) / 256);
         return launch(bc4_kernel<OP>, dim3((unsigned)nb), dim3(256), r.stream, r.P, r.dims, r.K,
                       dloss, r.two_over_M);
     } else {
@@ -488,7 +526,8 @@ int run_vjp(const Req& r, bool acc) {
         using OP = typename decltype(tag)::OP;
         using GEO = typename decltype(tag)::GEO;
         if constexpr (GEO::D3)
-            return launch_vjp<OP, GEO::TXV, GEO::TYV>(r, acc, FPDE_VJP_TARGET3);
+            return launch_vjp<OP, GEO::TXV, GEO::TYV>(
+                r, acc, OP::TIME ? GEO::MIN_BWD_BLOCKS : FPDE_VJP_TARGET3);
         else
             return launch_vjp<OP, kTX2, 1>(r, acc, kTargetBlocks2);
     });
@@ -531,9 +570,12 @@ int run_bwd(const Req& r0, const double* dloss, double* loss = nullptr) {
             return st;
         } else if constexpr (GEO::D3)
             return launch_bwd<OP, GEO::TXB, GEO::TYb>(r, dloss, zc3<GEO>(r), loss);
+        else if (loss)
+            return launch_bwd<OP, kTX2V, 1>(r, dloss, zc2(r), loss);
+        else if (FPDE_BWD2_QUEUE)
+            return launch_bwdq<OP>(r, dloss, zc2(r));
         else
-            return loss ? launch_bwd<OP, kTX2V, 1>(r, dloss, zc2(r), loss)
-                        : launch_bwd<OP, kTX2, 1>(r, dloss, zc2(r), loss);
+            return launch_bwd<OP, kTX2, 1>(r, dloss, zc2(r), loss);
     });
 }
 

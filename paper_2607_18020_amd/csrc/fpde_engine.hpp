@@ -954,6 +954,150 @@ __global__ __launch_bounds__(TX* TY, FPDE_BWD_MINW) void bwd_kernel(Ptrs P, Dims
 }
 
 // ---------------------------------------------------------------------------
+// 2-D backward with a register queue: no LDS and no barrier.  A row of a 2-D
+// grid is a few kilobytes, so the LDS march above waits once per row for a
+// barrier and that row's loads.  Here each lane marches one column down its
+// chunk of rows, keeping for every field the values at x - 1, x, x + 1 of Q
+// rows in registers (each row loaded Q - 5 steps before its first use), and
+// its own residuals R of the rows z - 1, z, z + 1.  The gather at (z, x) needs
+// R at x -+ 1 as well: the neighbouring lanes hold them, and a DPP wavefront
+// shift by one lane brings them over.  So that every lane has both neighbours,
+// the two edge lanes of each wave evaluate residuals only (at the columns
+// before and after the wave's 62 output columns), and a workgroup of NW waves
+// writes 62 NW columns.  Every node of the marched rows is written once, the
+// boundary columns included (R is zero off the residual set); no atomics.
+
+// v of lane i - 1 (wave_shr:1) or of lane i + 1 (wave_shl:1); the lanes at the
+// wave's ends receive 0
+__device__ __forceinline__ float lane_prev(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x138, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float lane_next(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x130, 0xF, 0xF, false));
+}
+
+template <class OP, int NW, int Q, bool PER>
+__global__ __launch_bounds__(NW * 64) void bwdq_kernel(Ptrs P, Dims D, KCoef K, const double* dloss,
+                                                     double two_over_M) {
+    constexpr int NF = OP::NF, NC = OP::NC, NR = OP::NR, NG = OP::NG;
+    constexpr int NC1 = NC > 0 ? NC : 1, NG1 = NG > 0 ? NG : 1;
+    constexpr int TXO = 62 * NW;  // output columns per workgroup
+    static_assert(OP::DIM == 2, "rows of a 2-D grid");
+    static_assert(Q >= 6, "rows z - 1 .. z + 2 in use and at least one row in flight");
+    constexpr uint32_t kOff = 0x80000000u;  // past every row's range: reads 0
+    const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+    const TileCoord tc = tile_coord<TXO, 1>(D);
+    const int z0 = tc.z0, z1 = tc.z1, L = z1 - z0;
+    const int c = tc.gx0 + wv * 62 + lane - 1;  // this lane's column (-1 .. past the grid)
+    const bool out_lane = lane >= 1 && lane <= 62 && c < D.nx;  // writes a gradient
+    // the lane's residual is that of its column, or of the wrapped column on a
+    // periodic grid (the edge lanes hold the x -+ 1 residuals of the output lanes)
+    const bool own_om = PER ? (c >= -D.nx && c < 2 * D.nx) : (c >= 1 && c <= D.nx - 2);
+    const uint32_t pbytes = (uint32_t)D.nx * 4u;
+    auto at = [&](int x) -> uint32_t {
+        if (PER) return (uint32_t)wrap_idx(x, D.nx) * 4u;
+        return (x >= 0 && x < D.nx) ? (uint32_t)x * 4u : kOff;
+    };
+    const uint32_t off[3] = {at(c - 1), at(c), at(c + 1)};
+    const uint32_t so = out_lane ? (uint32_t)c * 4u : kDropOff;
+    const float scale = (float)(two_over_M * (*dloss));
+
+    // the queue: row z0 - 2 + k lives in slot k % Q; rows z0 - 2 .. z1 + 1 are read
+    float qv[Q][NF][3], qk[Q][NC1];
+    auto load_row = [&](int k, auto slot) __attribute__((always_inline)) {
+        constexpr int S_ = decltype(slot)::value;
+        const int z = z0 - 2 + k;
+        const bool ok = z <= z1 + 1 && (PER || (z >= 0 && z < D.nz));
+        const int zr = PER ? wrap_idx(z, D.nz) : z;
+#pragma unroll
+        for (int f = 0; f < NF; ++f) {
+            const __amdgpu_buffer_rsrc_t r = plane_rsrc_if(P.f[f], zr, pbytes, ok);
+#pragma unroll
+            for (int v = 0; v < 3; ++v) qv[S_][f][v] = bld(r, off[v]);
+        }
+#pragma unroll
+        for (int j = 0; j < NC; ++j) qk[S_][j] = bld(plane_rsrc_if(P.c[j], zr, pbytes, ok), off[1]);
+    };
+    // R at the row of slot K1 from the rows of slots K0, K1, K2 (zero off the
+    // residual set), and the gather's self terms there
+    auto r_row = [&](auto k0, auto k1, auto k2, int z, float* R, float* S) __attribute__((always_inline)) {
+        constexpr int A = decltype(k0)::value, B = decltype(k1)::value, C = decltype(k2)::value;
+        Star s[NF];
+#pragma unroll
+        for (int f = 0; f < NF; ++f) {
+            s[f].c = qv[B][f][1];
+            s[f].m[0] = qv[A][f][1];
+            s[f].p[0] = qv[C][f][1];
+            s[f].m[1] = qv[B][f][0];
+            s[f].p[1] = qv[B][f][2];
+        }
+        OP::residual(s, qk[B], K, R);
+        const bool om = own_om && (PER || (z >= 1 && z <= D.nz - 2));
+#pragma unroll
+        for (int b = 0; b < NR; ++b) R[b] = om ? R[b] : 0.f;
+        OP::gather_self(s, R, K, S);
+    };
+
+    unroll_seq([&](auto k) __attribute__((always_inline)) {
+        load_row(decltype(k)::value, k);
+    }, std::make_integer_sequence<int, Q - 1>{});
+    float Rm[NR], Rc[NR], Sm[NG1], Sc[NG1];
+    r_row(IC<0>{}, IC<1>{}, IC<2>{}, z0 - 1, Rm, Sm);
+    r_row(IC<1>{}, IC<2>{}, IC<3>{}, z0, Rc, Sc);
+
+    auto step = [&](auto jc, int w) __attribute__((always_inline)) {
+        constexpr int J = decltype(jc)::value;  // w % Q
+        // slots of the rows z - 1, z, z + 1, z + 2 (k = w + 1 .. w + 4), and of the row
+        // loaded now (k = w + Q - 1, in the slot of row z - 3, last read a step ago)
+        constexpr int K1 = (J + 1) % Q, K2 = (J + 2) % Q, K3 = (J + 3) % Q, K4 = (J + 4) % Q;
+        constexpr int KN = (J + Q - 1) % Q;
+        const int z = z0 + w;
+        load_row(w + Q - 1, IC<KN>{});
+        float Rp[NR], Sp[NG1];
+        r_row(IC<K2>{}, IC<K3>{}, IC<K4>{}, z + 1, Rp, Sp);
+        Star fs[NF], rs[NR];
+#pragma unroll
+        for (int f = 0; f < NF; ++f) {
+            fs[f].c = qv[K2][f][1];
+            fs[f].m[0] = qv[K1][f][1];
+            fs[f].p[0] = qv[K3][f][1];
+            fs[f].m[1] = qv[K2][f][0];
+            fs[f].p[1] = qv[K2][f][2];
+        }
+#pragma unroll
+        for (int b = 0; b < NR; ++b) {
+            rs[b].c = Rc[b];
+            rs[b].m[0] = Rm[b];
+            rs[b].p[0] = Rp[b];
+            rs[b].m[1] = lane_prev(Rc[b]);
+            rs[b].p[1] = lane_next(Rc[b]);
+        }
+        float g[NF];
+        OP::gather_rest(fs, rs, Sc, K, g);
+        const int zr = PER ? wrap_idx(z, D.nz) : z;
+#pragma unroll
+        for (int f = 0; f < NF; ++f) bst<kStream>(plane_rsrc(P.out[f], zr, pbytes), so, scale * g[f]);
+#pragma unroll
+        for (int b = 0; b < NR; ++b) {
+            Rm[b] = Rc[b];
+            Rc[b] = Rp[b];
+        }
+#pragma unroll
+        for (int q = 0; q < NG; ++q) Sc[q] = Sp[q];
+        (void)Sm;
+    };
+
+    int w = 0;
+    for (; w + Q <= L; w += Q)  // slot indices are constants in each copy
+        unroll_seq([&](auto j) __attribute__((always_inline)) {
+            step(j, w + decltype(j)::value);
+        }, std::make_integer_sequence<int, Q>{});
+    unroll_seq([&](auto j) __attribute__((always_inline)) {
+        if (w + decltype(j)::value < L) step(j, w + decltype(j)::value);
+    }, std::make_integer_sequence<int, Q - 1>{});
+}
+
+// ---------------------------------------------------------------------------
 // Explicit-sensitivity backward: grads (=, or += when ACC) J^T G for caller-given
 // residual sensitivities G_b = dL/dR_b (Sec. 2.2).  The gather is the one above
 // with G in place of the recomputed residuals, so no residual, const or ring is
@@ -1248,7 +1392,11 @@ template <class OP, bool PER>
 __global__ __launch_bounds__(256) void tm_kernel(Ptrs P, Dims D, KCoef K, const double* dloss,
                                                  double two_over_M) {
     constexpr int D3 = OP::D;
-    const int idx = (int)blockIdx.x * 256 + (int)threadIdx.x;  // spatial node (vol < 2^29)
+    // spatial node (vol < 2^29), blocks in launch order: each lane marches the
+    // time levels on its own, so neighbouring rows are shared in L2 only by
+    // workgroups that run at the same time; an XCD-contiguous order (as the
+    // end-level kernel uses) fetched 27% more here
+    const int idx = (int)blockIdx.x * 256 + (int)threadIdx.x;
     if (idx >= (int)D.vol) return;
     const int i3 = idx % D.nx, r = idx / D.nx, i2 = r % D.ny, i1 = r / D.ny;
     if (!PER && !(i1 >= 1 && i1 <= D.nz - 2 && i2 >= 1 && i2 <= D.ny - 2 && i3 >= 1 &&
@@ -1311,22 +1459,18 @@ __global__ __launch_bounds__(256) void tm_kernel(Ptrs P, Dims D, KCoef K, const 
 // t = nt - 1 (the end planes of array axis 0), which the level marches do not
 // visit.  A node whose only boundary coordinate is t receives the time term of
 // its inward neighbour's residuals (level 1 or nt - 2); a node on the spatial
-// boundary as well touches no residual node and gets 0.  One workgroup per
-// 256-node segment of each (x, y) row of the two levels.
+// boundary as well touches no residual node and gets 0.  One workgroup per 256
+// consecutive nodes of a level (the first half of the workgroups covers level 0).
 template <class OP>
 __global__ __launch_bounds__(256) void bc4_kernel(Ptrs P, Dims D, KCoef K, const double* dloss,
                                                   double two_over_M) {
     constexpr int NF = OP::NF, NC = OP::NC, D3 = OP::D;
-    const int segs = (D.nx + 255) / 256;
-    int blk = blockIdx.x;
-    const int seg = blk % segs;
-    blk /= segs;
-    const int i2 = blk % D.ny;
-    blk /= D.ny;
-    const int i1 = blk % D.nz;
-    const bool low = blk / D.nz == 0;
-    const int i3 = seg * 256 + (int)threadIdx.x;
-    if (i3 >= D.nx) return;
+    const int per_level = (int)((D.vol + 255) / 256);
+    const int blk = remap_xcd((int)blockIdx.x, 2 * per_level);  // (neighbours through one L2)
+    const bool low = blk < per_level;
+    const int idx = (blk - (low ? 0 : per_level)) * 256 + (int)threadIdx.x;
+    if (idx >= (int)D.vol) return;
+    const int i3 = idx % D.nx, rr = idx / D.nx, i2 = rr % D.ny, i1 = rr / D.ny;
     const int tn = low ? 0 : D.nt - 1;  // the node's level
     const int tm = low ? 1 : D.nt - 2;  // its inward neighbour's (the residual's)
     const uint32_t vbytes = (uint32_t)D.vol * 4u;

@@ -31,6 +31,11 @@
 // algebraically equal grouped form (q+ - 2q + q-) or coefficient grouping such as
 // g * (u_x + 2 nu/h^2) loses several digits on fine grids.
 //
+// Every multiply that feeds an add is written as fmaf, and the library is built
+// with floating-point contraction off: an operator's arithmetic is then the same
+// instruction sequence whichever kernel evaluates it, so two kernels that
+// evaluate the same residual or gather agree bit for bit.
+//
 // The divergence residual sum_a D1_a c_a of a nearly divergence-free velocity is
 // a near-total cancellation of terms far larger than the result, so it is summed
 // in float64 (differences widened exactly, float64 1/(2h_a)) and rounded once.
@@ -66,7 +71,7 @@ template <int DIM>
 __device__ __forceinline__ float lap(const Star& s, const KCoef& K) {
     float l = 0.f;
 #pragma unroll
-    for (int a = 0; a < DIM; ++a) l += ((s.p[a] - s.c) + (s.m[a] - s.c)) * K.ih2[a];
+    for (int a = 0; a < DIM; ++a) l = fmaf((s.p[a] - s.c) + (s.m[a] - s.c), K.ih2[a], l);
     return l;
 }
 
@@ -80,7 +85,7 @@ struct OpBurgers {
     __device__ __forceinline__ static void residual(const Star* f, const float*, const KCoef& K, float* R) {
         const Star& u = f[0];
         const float uxx = ((u.p[1] - u.c) + (u.m[1] - u.c)) * K.ih2[1];
-        R[0] = d1(u, 0, K) + u.c * d1(u, 1, K) - K.nu * uxx;
+        R[0] = fmaf(-K.nu, uxx, fmaf(u.c, d1(u, 1, K), d1(u, 0, K)));
     }
 
     // dL/du(n): time neighbours (R(n-e_t) - R(n+e_t))/(2dt); advective
@@ -89,10 +94,9 @@ struct OpBurgers {
         const Star& u = f[0];
         const Star& R = r[0];
         float acc = (R.m[0] - R.p[0]) * K.i2h[0];
-        acc += R.c * d1(u, 1, K);
-        acc += (R.m[1] * u.m[1] - R.p[1] * u.p[1]) * K.i2h[1];
-        acc -= K.nu * (((R.p[1] - R.c) + (R.m[1] - R.c)) * K.ih2[1]);
-        g[0] = acc;
+        acc = fmaf(R.c, d1(u, 1, K), acc);
+        acc = fmaf(fmaf(R.m[1], u.m[1], -(R.p[1] * u.p[1])), K.i2h[1], acc);
+        g[0] = fmaf(-K.nu, ((R.p[1] - R.c) + (R.m[1] - R.c)) * K.ih2[1], acc);
     }
 
     __device__ __forceinline__ static void gather_self(const Star*, const float*, const KCoef&, float*) {}
@@ -105,7 +109,7 @@ struct OpBurgers {
         float R[1];
         residual(f, c, K, R);
         g[0] = (AX == 0) ? R[0] * t * K.i2h[0]
-                         : R[0] * (t * f[0].c * K.i2h[1] - K.nu * K.ih2[1]);
+                         : R[0] * fmaf(t * f[0].c, K.i2h[1], -K.nu * K.ih2[1]);
     }
 };
 
@@ -116,11 +120,11 @@ struct OpHelmholtz {
     static constexpr bool TIME = false;  // (see OpNS3T)
 
     __device__ __forceinline__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
-        R[0] = lap<2>(f[0], K) + K.k2 * f[0].c - c[0];
+        R[0] = fmaf(K.k2, f[0].c, lap<2>(f[0], K)) - c[0];
     }
 
     __device__ __forceinline__ static void gather(const Star*, const Star* r, const KCoef& K, float* g) {
-        g[0] = K.k2 * r[0].c + lap<2>(r[0], K);
+        g[0] = fmaf(K.k2, r[0].c, lap<2>(r[0], K));
     }
     __device__ __forceinline__ static void gather_self(const Star*, const float*, const KCoef&, float*) {}
     __device__ __forceinline__ static void gather_rest(const Star* f, const Star* r, const float*, const KCoef& K, float* g) {
@@ -142,11 +146,11 @@ struct OpHeat {
     static constexpr bool TIME = false;  // (see OpNS3T)
 
     __device__ __forceinline__ static void residual(const Star* f, const float* c, const KCoef& K, float* R) {
-        R[0] = (f[0].c - c[0]) * K.inv_dt - K.alpha * lap<3>(f[0], K);
+        R[0] = fmaf(-K.alpha, lap<3>(f[0], K), (f[0].c - c[0]) * K.inv_dt);
     }
 
     __device__ __forceinline__ static void gather(const Star*, const Star* r, const KCoef& K, float* g) {
-        g[0] = r[0].c * K.inv_dt - K.alpha * lap<3>(r[0], K);
+        g[0] = fmaf(-K.alpha, lap<3>(r[0], K), r[0].c * K.inv_dt);
     }
     __device__ __forceinline__ static void gather_self(const Star*, const float*, const KCoef&, float*) {}
     __device__ __forceinline__ static void gather_rest(const Star* f, const Star* r, const float*, const KCoef& K, float* g) {
@@ -236,8 +240,8 @@ struct OpNS {
         residual(f, c, K, R);
 #pragma unroll
         for (int q = 0; q < D; ++q) {
-            float v = R[q] * (t * f[AX].c * K.i2h[AX] - K.nu * K.ih2[AX]);
-            if (q == AX) v += R[D] * t * K.i2h[AX];
+            float v = R[q] * fmaf(t * f[AX].c, K.i2h[AX], -K.nu * K.ih2[AX]);
+            if (q == AX) v = fmaf(R[D] * t, K.i2h[AX], v);
             g[q] = v;
         }
         g[D] = R[AX] * t * K.i2h[AX];
@@ -289,7 +293,7 @@ struct OpNST {
     __device__ __forceinline__ static float lap_xy(const Star& s, const KCoef& K) {
         float l = 0.f;
 #pragma unroll
-        for (int a = 1; a <= D; ++a) l += ((s.p[a] - s.c) + (s.m[a] - s.c)) * K.ih2[a];
+        for (int a = 1; a <= D; ++a) l = fmaf((s.p[a] - s.c) + (s.m[a] - s.c), K.ih2[a], l);
         return l;
     }
 
@@ -361,8 +365,8 @@ struct OpNST {
             constexpr int S_ = AX - 1;  // the velocity component along AX
 #pragma unroll
             for (int q = 0; q < D; ++q) {
-                float v = R[q] * (t * f[S_].c * K.i2h[AX] - K.nu * K.ih2[AX]);
-                if (q == S_) v += R[D] * t * K.i2h[AX];
+                float v = R[q] * fmaf(t * f[S_].c, K.i2h[AX], -K.nu * K.ih2[AX]);
+                if (q == S_) v = fmaf(R[D] * t, K.i2h[AX], v);
                 g[q] = v;
             }
             g[D] = R[S_] * t * K.i2h[AX];
@@ -459,8 +463,8 @@ struct OpNS3T {
         residual(f, c, K, R);
 #pragma unroll
         for (int q = 0; q < D; ++q) {
-            float v = R[q] * (t * f[AX].c * K.i2h[AX] - K.nu * K.ih2[AX]);
-            if (q == AX) v += R[D] * t * K.i2h[AX];
+            float v = R[q] * fmaf(t * f[AX].c, K.i2h[AX], -K.nu * K.ih2[AX]);
+            if (q == AX) v = fmaf(R[D] * t, K.i2h[AX], v);
             g[q] = v;
         }
         g[D] = R[AX] * t * K.i2h[AX];

@@ -26,7 +26,7 @@ from typing import Dict, List
 
 from paper_2607_18020_amd.csrc import build as B
 
-KERNEL_PREFIXES = ("fwd_kernel", "fwdq_kernel", "bwd_kernel", "vjp_kernel", "bc_kernel",
+KERNEL_PREFIXES = ("fwd_kernel", "fwdq_kernel", "bwd_kernel", "bwdq_kernel", "vjp_kernel", "bc_kernel",
                    "bc4_kernel", "tm_kernel", "zero_levels_kernel", "fill_f64_kernel")
 
 

@@ -33,7 +33,7 @@ KERNEL_SOURCES = ("csrc/fpde.hip", "csrc/fpde_engine.hpp", "csrc/fpde_ops.hpp")
 STREAM_KERNEL = "MulFunctor"  # the benchmark's 1 GiB y = 1 * x kernel
 STREAM_BYTES = 1 << 30
 # the library's kernels (name stems)
-KERNELS = ("fwd_kernel", "fwdq_kernel", "bwd_kernel", "bc_kernel", "bc4_kernel", "vjp_kernel",
+KERNELS = ("fwd_kernel", "fwdq_kernel", "bwd_kernel", "bwdq_kernel", "bc_kernel", "bc4_kernel", "vjp_kernel",
            "tm_kernel", "zero_levels_kernel", "fill_f64")
 
 
