@@ -62,7 +62,8 @@ DEFAULT_CONFIG = "ns_3d_tgv"
 # (config, path, bc_mode) of the "workloads" object, beside the headline case
 EXTRA_CASES = (("burgers_1dt", "loss", 0), ("helmholtz_2d", "loss", 0), ("heat_3d", "loss", 0),
                ("ns_2d", "loss", 0), ("ns_3d_tgv", "fused", 0), ("ns_3d_tgv", "residual", 0),
-               ("ns_3d_tgv", "loss", 1), ("ns_3dt", "loss", 0), ("ns_3dt_large", "loss", 0))
+               ("ns_3d_tgv", "loss", 1), ("ns_3dt", "loss", 0), ("ns_3dt_large", "loss", 0),
+               ("ns_3dt_large", "residual", 0))
 
 
 def parse():

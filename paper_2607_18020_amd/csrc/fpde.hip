@@ -138,12 +138,12 @@ using GeoNS3 = Geo3<FPDE_NS3_FWD_TX, FPDE_NS3_FWD_TY, FPDE_NS3_BWD_TX, FPDE_NS3_
                     FPDE_NS3_MIN_BWD_BLOCKS, FPDE_VJP_TX3, FPDE_VJP_TY3>;
 // 3D+t NS: the level march reads six time-neighbour velocities per node besides
 // the four fields, which do not fit the 128 registers of a 1024-thread backward
-// tile: 512-thread backward tiles
+// tile: 768-thread backward tiles (at 20 x 128^3, 5% faster than 512 threads)
 #ifndef FPDE_NS4_BWD_TX
 #define FPDE_NS4_BWD_TX 128
 #endif
 #ifndef FPDE_NS4_BWD_TY
-#define FPDE_NS4_BWD_TY 4
+#define FPDE_NS4_BWD_TY 6
 #endif
 // workgroups per launch: a time level is a 3-D volume of its own, so whole-level
 // chunks leave few workgroups (and a last round of them mostly idle) on the
@@ -495,11 +495,14 @@ int launch_bc(const Req& r, const double* dloss) {
 // time levels (after the level march, which wrote the spatial part)
 template <class OP>
 int launch_tm(const Req& r, const double* dloss) {
+    // blocks of TM_B1 x TM_B2 x TM_B3 nodes (fewer than 2^31: a level holds fewer than 2^29)
+    const Dims& d = r.dims;
+    const long long nb = (long long)((d.nx + TM_B3 - 1) / TM_B3) * ((d.ny + TM_B2 - 1) / TM_B2) *
+                         ((d.nz + TM_B1 - 1) / TM_B1);
     int st = FPDE_OK;
-    with_flag(r.dims.per, [&](auto per) {
-        st = launch(tm_kernel<OP, decltype(per)::value>,
-                    dim3((unsigned)((r.dims.vol + 255) / 256)), dim3(256), r.stream, r.P, r.dims,
-                    r.K, dloss, r.two_over_M);
+    with_flag(d.per, [&](auto per) {
+        st = launch(tm_kernel<OP, decltype(per)::value>, dim3((unsigned)nb), dim3(TM_NT),
+                    r.stream, r.P, d, r.K, dloss, r.two_over_M);
     });
     return st;
 }

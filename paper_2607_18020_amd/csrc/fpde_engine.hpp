@@ -1354,17 +1354,22 @@ __global__ __launch_bounds__(256) void bc_kernel(Ptrs P, Dims D, KCoef K, const 
 // evaluated once; each node's gradient is read, the time part added, and
 // written once (the march's spatial part is already there).  Only nodes on the
 // spatial residual set have a time part (R is zero off it).
+//
+// The residual of level L reads the stars at L and the node's velocities at
+// L -+ 1, which are the centres of the stars at L -+ 1.  The lane loads the stars
+// of each level once, one level ahead of the residual it evaluates, and keeps
+// the stars of L + 1 and the centre velocities of L - 1 in registers: a point
+// value fetched once for a residual and again, a level later, for a star would
+// come from HBM twice, since a whole level of every field passes through L2 in
+// between.
 
-// The residuals of the velocity equations at one spatial node of level lev:
-// the spatial star of every field at lev and the velocities at lev -+ 1, loaded
-// through the levels' buffer descriptors (o: the node's byte offset in a level,
-// n[6]: its neighbours' at -+ one node along the three spatial axes).
-template <class OP, bool PER>
-__device__ __forceinline__ void residual_at_level(const Ptrs& P, const Dims& D, const KCoef& K,
-                                                  int lev, uint32_t vbytes, uint32_t o,
-                                                  const uint32_t* n, float* R) {
-    constexpr int NF = OP::NF, NC = OP::NC, D3 = OP::D;
-    Star st[NF];
+// The stars of every field at one spatial node of level lev (lev in range),
+// loaded through the level's buffer descriptors (o: the node's byte offset in a
+// level, n[6]: its neighbours' at -+ one node along the three spatial axes).
+template <class OP>
+__device__ __forceinline__ void stars_at_level(const Ptrs& P, int lev, uint32_t vbytes, uint32_t o,
+                                               const uint32_t* n, Star* st) {
+    constexpr int NF = OP::NF, D3 = OP::D;
 #pragma unroll
     for (int f = 0; f < NF; ++f) {
         const __amdgpu_buffer_rsrc_t r = plane_rsrc(P.f[f], lev, vbytes);
@@ -1375,30 +1380,49 @@ __device__ __forceinline__ void residual_at_level(const Ptrs& P, const Dims& D, 
             st[f].p[a] = bld(r, n[2 * a + 1]);
         }
     }
-    float c[NC];
-#pragma unroll
-    for (int j = 0; j < NC; ++j) {
-        int l = lev + OP::TOFF[j];
-        if (PER) l = l < 0 ? l + D.nt : (l >= D.nt ? l - D.nt : l);
-        c[j] = bld(plane_rsrc(P.f[OP::TSRC[j]], l, vbytes), o);
-    }
-    float Rf[OP::NR];
-    OP::residual(st, c, K, Rf);
-#pragma unroll
-    for (int q = 0; q < D3; ++q) R[q] = Rf[q];
 }
 
+// Lanes: a workgroup of TM_B1 x TM_B2 x TM_B3 lanes covers a block of as many
+// spatial nodes (along array axes 1, 2, 3; whole 64-lane wavefronts along
+// axis 3), blocks numbered with axis 3 fastest, in launch order or (TM_REMAP)
+// XCD-contiguous.  Each lane marches the time levels on its own, so the rows
+// that neighbouring blocks share meet in L2 only while the blocks run at the
+// same time.  At 20 x 128^3 one row pair per block in launch order (the default)
+// was the fastest of the shapes from 2 x 2 x 64 to 4 x 4 x 64 lanes, and the
+// XCD-contiguous order slower by 3-4% for every shape.
+#ifndef FPDE_TM_B1
+#define FPDE_TM_B1 1
+#endif
+#ifndef FPDE_TM_B2
+#define FPDE_TM_B2 2
+#endif
+#ifndef FPDE_TM_B3
+#define FPDE_TM_B3 128
+#endif
+#ifndef FPDE_TM_REMAP
+#define FPDE_TM_REMAP 0
+#endif
+constexpr int TM_B1 = FPDE_TM_B1, TM_B2 = FPDE_TM_B2, TM_B3 = FPDE_TM_B3;
+constexpr int TM_NT = TM_B1 * TM_B2 * TM_B3;
+static_assert(TM_B3 % 64 == 0 && TM_NT <= 1024, "whole wavefronts along axis 3");
+
 template <class OP, bool PER>
-__global__ __launch_bounds__(256) void tm_kernel(Ptrs P, Dims D, KCoef K, const double* dloss,
-                                                 double two_over_M) {
-    constexpr int D3 = OP::D;
-    // spatial node (vol < 2^29), blocks in launch order: each lane marches the
-    // time levels on its own, so neighbouring rows are shared in L2 only by
-    // workgroups that run at the same time; an XCD-contiguous order (as the
-    // end-level kernel uses) fetched 27% more here
-    const int idx = (int)blockIdx.x * 256 + (int)threadIdx.x;
-    if (idx >= (int)D.vol) return;
-    const int i3 = idx % D.nx, r = idx / D.nx, i2 = r % D.ny, i1 = r / D.ny;
+__global__ __launch_bounds__(TM_NT) void tm_kernel(Ptrs P, Dims D, KCoef K, const double* dloss,
+                                                   double two_over_M) {
+    constexpr int NF = OP::NF, D3 = OP::D;
+    static_assert(OP::NC == 2 * D3, "consts: the velocities at t - 1, then at t + 1");
+    const int n3 = (D.nx + TM_B3 - 1) / TM_B3, n2 = (D.ny + TM_B2 - 1) / TM_B2;
+    int blk = (int)blockIdx.x;
+    if (FPDE_TM_REMAP) blk = remap_xcd(blk, (int)gridDim.x);
+    const int b3 = blk % n3;
+    blk /= n3;
+    const int b2 = blk % n2, b1 = blk / n2;
+    const int lt = (int)threadIdx.x;
+    const int i3 = b3 * TM_B3 + lt % TM_B3;
+    const int i2 = b2 * TM_B2 + (lt / TM_B3) % TM_B2;
+    const int i1 = b1 * TM_B1 + lt / (TM_B3 * TM_B2);
+    if (i1 >= D.nz || i2 >= D.ny || i3 >= D.nx) return;
+    const int idx = (i1 * D.ny + i2) * D.nx + i3;  // (vol < 2^29)
     if (!PER && !(i1 >= 1 && i1 <= D.nz - 2 && i2 >= 1 && i2 <= D.ny - 2 && i3 >= 1 &&
                   i3 <= D.nx - 2))
         return;  // off the spatial residual set: no time part
@@ -1426,22 +1450,59 @@ __global__ __launch_bounds__(256) void tm_kernel(Ptrs P, Dims D, KCoef K, const 
     const float scale = (float)(two_over_M * (*dloss));
     // levels whose gradient gets the time part: those the march wrote (all of
     // them on a periodic grid, else 1 .. nt - 2, whose residual neighbours are
-    // the levels 0 .. nt - 1 with R zero at the end levels)
+    // the levels 0 .. nt - 1 with R zero at the end levels); nt >= 3
     const int t0 = PER ? 0 : 1, t1 = PER ? D.nt - 1 : D.nt - 2;
-    auto R_of = [&](int lev, float* R) __attribute__((always_inline)) {
-        if (PER) lev = wrap_idx(lev, D.nt);
-        if (!PER && (lev < 1 || lev > D.nt - 2)) {
+    // the march state: the next residual is that of level L, from the stars of
+    // L (sc) and the centre velocities of L - 1 (vm) and L + 1 (loaded with the
+    // stars of L + 1, which become sc for the next level)
+    int L;
+    Star sc[NF];
+    float vm[D3];
+    auto next_R = [&](float* R) __attribute__((always_inline)) {
+        if (!PER && L > D.nt - 2) {  // level nt - 1: R = 0 and no level beyond it
 #pragma unroll
             for (int q = 0; q < D3; ++q) R[q] = 0.f;
+            ++L;
             return;
         }
-        residual_at_level<OP, PER>(P, D, K, lev, vbytes, o, n, R);
+        Star sn[NF];
+        stars_at_level<OP>(P, PER ? wrap_idx(L + 1, D.nt) : L + 1, vbytes, o, n, sn);
+        float c[2 * D3], Rf[OP::NR];
+#pragma unroll
+        for (int b = 0; b < D3; ++b) {
+            c[b] = vm[b];
+            c[D3 + b] = sn[b].c;
+        }
+        OP::residual(sc, c, K, Rf);
+#pragma unroll
+        for (int q = 0; q < D3; ++q) {
+            R[q] = Rf[q];
+            vm[q] = sc[q].c;
+        }
+#pragma unroll
+        for (int f = 0; f < NF; ++f) sc[f] = sn[f];
+        ++L;
     };
     float Rm[D3], Rc[D3], Rp[D3];
-    R_of(t0 - 1, Rm);
-    R_of(t0, Rc);
+    if (PER) {  // from level -1 (= nt - 1): the residual of t0 - 1 is evaluated too
+        L = -1;
+        stars_at_level<OP>(P, D.nt - 1, vbytes, o, n, sc);
+        const int l2 = D.nt - 2;
+#pragma unroll
+        for (int b = 0; b < D3; ++b) vm[b] = bld(plane_rsrc(P.f[b], l2, vbytes), o);
+        next_R(Rm);
+    } else {  // R(0) = 0; the march starts at level 1 with the velocities of level 0
+        L = 1;
+        stars_at_level<OP>(P, 1, vbytes, o, n, sc);
+#pragma unroll
+        for (int b = 0; b < D3; ++b) {
+            vm[b] = bld(plane_rsrc(P.f[b], 0, vbytes), o);
+            Rm[b] = 0.f;
+        }
+    }
+    next_R(Rc);
     for (int t = t0; t <= t1; ++t) {
-        R_of(t + 1, Rp);
+        next_R(Rp);  // R of level t + 1
         float tp[D3] = {};
         OP::add_time(Rm, Rp, K, tp);
 #pragma unroll
