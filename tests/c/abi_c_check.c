@@ -1,8 +1,10 @@
 /*
  * abi_c_check.c -- the C ABI of libfpde used from C alone (no Python, no
  * torch): device buffers from the HIP runtime, every entry point called on a
- * small 3-D backward-Euler Navier-Stokes grid, results compared with the CPU
- * oracle (test infrastructure, linked by this test program only).
+ * small 3-D backward-Euler Navier-Stokes grid (fpde_grid) and every four-axis
+ * entry point on a small 3D+t Navier-Stokes space-time grid (fpde_grid4),
+ * results compared with the CPU oracle (test infrastructure, linked by this
+ * test program only).
  * Exit status 0 and a line "c-abi: ok" when every comparison holds.
  */
 #include <hip/hip_runtime_api.h>
@@ -46,7 +48,7 @@ static double rel_err(const float* got, const double* ref, long n) {
     return s > 0 ? e / s : e;
 }
 
-int main(void) {
+static int check_ns3d(void) {
     const long n[3] = {20, 24, 70};
     const long N = n[0] * n[1] * n[2];
     const double pi = 3.14159265358979323846;
@@ -192,6 +194,155 @@ int main(void) {
         snprintf(what, sizeof what, "grad %s (vjp)", names[a]);
         check(what, rel_err(buf, oj[a], N), 1e-4);
     }
+    return 0;
+}
+
+/* 3D+t NS on a t x x x y x z grid with several time levels, tiles and chunks
+ * and a ragged last tile: the four-axis entry points against the oracle.  The
+ * op has no consts (the neighbouring levels' velocities are its own fields). */
+static int check_ns3dt(void) {
+    enum { F4 = 4, R4 = 4 };
+    const long n[4] = {6, 12, 17, 70};
+    const long V = n[1] * n[2] * n[3], N = n[0] * V;
+    const double pi = 3.14159265358979323846;
+    const double h[4] = {1.0 / (n[0] - 1), 2 * pi / n[1], 2 * pi / n[2], 2 * pi / n[3]};
+    const double coef[4] = {0.01, 0.0, 0.0, 0.0}; /* nu */
+    float* hf[F4];
+    float* hg[R4];
+    for (int a = 0; a < F4; ++a) hf[a] = malloc(N * sizeof(float));
+    for (int b = 0; b < R4; ++b) hg[b] = malloc(N * sizeof(float));
+    /* a decaying Taylor-Green field, perturbed */
+    for (long t = 0; t < n[0]; ++t)
+        for (long i = 0; i < n[1]; ++i)
+            for (long j = 0; j < n[2]; ++j)
+                for (long k = 0; k < n[3]; ++k) {
+                    const long m = ((t * n[1] + i) * n[2] + j) * n[3] + k;
+                    const double x = i * h[1], y = j * h[2], z = k * h[3];
+                    const double d = exp(-3 * coef[0] * t * h[0]);
+                    const double ic[4] = {d * sin(x) * cos(y) * cos(z), -d * cos(x) * sin(y) * cos(z),
+                                          0.0, d * d * (cos(2 * x) + cos(2 * y)) * (cos(2 * z) + 2) / 16};
+                    for (int a = 0; a < F4; ++a)
+                        hf[a][m] = (float)(ic[a] + 0.01 * sin(12.9898 * m + 78.233 * a));
+                    for (int b = 0; b < R4; ++b) hg[b][m] = (float)cos(0.37 * m + 1.3 * b);
+                }
+    float *df[F4], *dR[R4], *dG[R4], *dg[F4], *dgv[F4], *dgj[F4];
+    double *dloss, *ddl, *dloss_v;
+    const size_t bytes = N * sizeof(float);
+    for (int a = 0; a < F4; ++a) {
+        CK(hipMalloc((void**)&df[a], bytes));
+        CK(hipMemcpy(df[a], hf[a], bytes, hipMemcpyHostToDevice));
+        CK(hipMalloc((void**)&dg[a], bytes));
+        CK(hipMalloc((void**)&dgv[a], bytes));
+        CK(hipMalloc((void**)&dgj[a], bytes));
+    }
+    for (int b = 0; b < R4; ++b) {
+        CK(hipMalloc((void**)&dR[b], bytes));
+        CK(hipMalloc((void**)&dG[b], bytes));
+        CK(hipMemcpy(dG[b], hg[b], bytes, hipMemcpyHostToDevice));
+    }
+    CK(hipMalloc((void**)&dloss, sizeof(double)));
+    CK(hipMalloc((void**)&dloss_v, sizeof(double)));
+    CK(hipMalloc((void**)&ddl, sizeof(double)));
+    const double dl = 0.75;
+    CK(hipMemcpy(ddl, &dl, sizeof(double), hipMemcpyHostToDevice));
+
+    fpde_grid4 grid;
+    memset(&grid, 0, sizeof grid);
+    grid.ndim = 4;
+    grid.bc_mode = 0;
+    for (int a = 0; a < 4; ++a) {
+        grid.n[a] = n[a];
+        grid.h[a] = h[a];
+    }
+    const fpde_coeffs co = {coef[0], coef[1], coef[2], coef[3]};
+    const float* cf[F4] = {df[0], df[1], df[2], df[3]};
+    const float* cG[R4] = {dG[0], dG[1], dG[2], dG[3]};
+
+    int ndim, nf, nc, nr;
+    if (fpde_op_info(FPDE_NS_3DT, &ndim, &nf, &nc, &nr) != FPDE_OK || ndim != 4 || nf != F4 ||
+        nc != 0 || nr != R4) {
+        printf("c-abi: fpde_op_info disagrees (3D+t)\n");
+        return 1;
+    }
+    /* a four-axis op through a three-axis grid, and a three-axis grid's op
+     * through fpde_grid4 with ndim 4: refused, nothing queued */
+    fpde_grid g3;
+    memset(&g3, 0, sizeof g3);
+    g3.ndim = 3;
+    for (int a = 0; a < 3; ++a) {
+        g3.n[a] = n[a + 1];
+        g3.h[a] = h[a + 1];
+    }
+    if (fpde_residual_fwd(FPDE_NS_3DT, &g3, &co, cf, NULL, NULL, dloss, NULL) != FPDE_ERR_SHAPE ||
+        fpde_residual_fwd4(FPDE_NS_3D_BE, &grid, &co, cf, cf, NULL, dloss, NULL) !=
+            FPDE_ERR_SHAPE) {
+        printf("c-abi: a grid of the wrong rank was not refused\n");
+        return 1;
+    }
+
+    int st = fpde_residual_fwd4(FPDE_NS_3DT, &grid, &co, cf, NULL, dR, dloss, NULL);
+    st |= fpde_residual_bwd4(FPDE_NS_3DT, &grid, &co, cf, NULL, ddl, dg, NULL);
+    st |= fpde_bc_correct4(FPDE_NS_3DT, &grid, &co, cf, NULL, ddl, dg, NULL);
+    st |= fpde_residual_value_and_grad4(FPDE_NS_3DT, &grid, &co, cf, NULL, ddl, dloss_v, dgv,
+                                        NULL);
+    st |= fpde_residual_vjp4(FPDE_NS_3DT, &grid, &co, cf, cG, 0, dgj, NULL);
+    if (st != FPDE_OK) {
+        printf("c-abi: a valid four-axis call failed (%d)\n", st);
+        return 1;
+    }
+    CK(hipDeviceSynchronize());
+
+    double *of[F4], *oG[R4], *oR[R4], *og[F4], *oj[F4];
+    for (int a = 0; a < F4; ++a) {
+        of[a] = malloc(N * sizeof(double));
+        og[a] = malloc(N * sizeof(double));
+        oj[a] = malloc(N * sizeof(double));
+        for (long m = 0; m < N; ++m) of[a][m] = hf[a][m];
+    }
+    for (int b = 0; b < R4; ++b) {
+        oG[b] = malloc(N * sizeof(double));
+        oR[b] = malloc(N * sizeof(double));
+        for (long m = 0; m < N; ++m) oG[b][m] = hg[b][m];
+    }
+    double L_ref;
+    const double* const* ocf = (const double* const*)of;
+    st = orc_loss(FPDE_NS_3DT, 4, n, h, 0, coef, ocf, NULL, &L_ref);
+    st |= orc_residual(FPDE_NS_3DT, 4, n, h, 0, coef, ocf, NULL, oR);
+    st |= orc_grad(FPDE_NS_3DT, 4, n, h, 0, coef, ocf, NULL, dl, og);
+    st |= orc_vjp(FPDE_NS_3DT, 4, n, h, 0, coef, ocf, NULL, (const double* const*)oG, oj);
+    if (st != 0) {
+        printf("c-abi: oracle failed on 3D+t (%d)\n", st);
+        return 1;
+    }
+    double L, Lv;
+    CK(hipMemcpy(&L, dloss, sizeof(double), hipMemcpyDeviceToHost));
+    CK(hipMemcpy(&Lv, dloss_v, sizeof(double), hipMemcpyDeviceToHost));
+    check("3D+t loss (fwd4)", fabs(L - L_ref) / fabs(L_ref), 1e-5);
+    check("3D+t loss (value_and_grad4)", fabs(Lv - L_ref) / fabs(L_ref), 1e-5);
+    float* buf = malloc(bytes);
+    const char* names[4] = {"u", "v", "w", "p"};
+    char what[64];
+    for (int b = 0; b < R4; ++b) {
+        CK(hipMemcpy(buf, dR[b], bytes, hipMemcpyDeviceToHost));
+        snprintf(what, sizeof what, "3D+t residual %d", b);
+        check(what, rel_err(buf, oR[b], N), 1e-5);
+    }
+    for (int a = 0; a < F4; ++a) {
+        CK(hipMemcpy(buf, dg[a], bytes, hipMemcpyDeviceToHost));
+        snprintf(what, sizeof what, "3D+t grad %s (bwd4 + bc4)", names[a]);
+        check(what, rel_err(buf, og[a], N), 1e-4);
+        CK(hipMemcpy(buf, dgv[a], bytes, hipMemcpyDeviceToHost));
+        snprintf(what, sizeof what, "3D+t grad %s (vg4)", names[a]);
+        check(what, rel_err(buf, og[a], N), 1e-4);
+        CK(hipMemcpy(buf, dgj[a], bytes, hipMemcpyDeviceToHost));
+        snprintf(what, sizeof what, "3D+t grad %s (vjp4)", names[a]);
+        check(what, rel_err(buf, oj[a], N), 1e-4);
+    }
+    return 0;
+}
+
+int main(void) {
+    if (check_ns3d() != 0 || check_ns3dt() != 0) return 1;
     if (fails) {
         printf("c-abi: %d comparison(s) failed\n", fails);
         return 1;
