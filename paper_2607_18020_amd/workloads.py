@@ -385,6 +385,58 @@ def normal_fields_f32(op: int, shape: Sequence[int], seed: int,
                     wl.coeffs if coeffs is None else coeffs, fields, consts)
 
 
+@dataclasses.dataclass
+class TiledWorkload:
+    """A workload too large to draw value by value (billions of nodes): each
+    array (fields, then consts) repeats one seeded draw of `period` standard
+    normal float32 values in memory order.  The period is a prime, so no row,
+    plane or time level holds its neighbour's values.  `window` rebuilds any
+    sub-box of the arrays on the host from the draws; the arrays themselves
+    are never built on the host."""
+
+    name: str
+    op: int
+    shape: Tuple[int, ...]
+    h: Tuple[float, ...]
+    coeffs: Coeffs
+    vectors: List[np.ndarray]  # float32, one draw per array
+
+    @property
+    def spec(self) -> OpSpec:
+        return OPS[self.op]
+
+    @property
+    def n_points(self) -> int:
+        return int(np.prod(self.shape))
+
+    @property
+    def n_residual_points(self) -> int:
+        return int(np.prod([s - 2 for s in self.shape]))
+
+    def window(self, box) -> Tuple[List[np.ndarray], List[np.ndarray]]:
+        """(fields, consts) on the sub-box `box` (a tuple of slices)."""
+        axes = [np.arange(*sl.indices(n)) for sl, n in zip(box, self.shape)]
+        lin = np.ravel_multi_index(np.meshgrid(*axes, indexing="ij"), self.shape)
+        arrays = [np.ascontiguousarray(v[lin % v.size]) for v in self.vectors]
+        nf = len(self.spec.fields)
+        return arrays[:nf], arrays[nf:]
+
+
+def normal_tiled_f32(op: int, shape: Sequence[int], seed: int,
+                     h: Optional[Sequence[float]] = None,
+                     coeffs: Optional[Coeffs] = None, period: int = 1_000_003) -> TiledWorkload:
+    """Standard-normal float32 inputs repeated with a prime period (TiledWorkload)."""
+    wl = normal_fields(op, (3,) * OPS[op].ndim, seed, None, coeffs)  # coefficients only
+    shape = tuple(int(s) for s in shape)
+    rng = np.random.default_rng(seed)
+    spec = OPS[op]
+    vectors = [rng.standard_normal(period, dtype=np.float32) for _ in spec.fields + spec.consts]
+    if h is None:
+        h = tuple(1.0 / (s - 1) for s in shape)
+    return TiledWorkload(f"tiled32_{OP_NAMES[op]}", op, shape, tuple(float(x) for x in h),
+                         wl.coeffs if coeffs is None else coeffs, vectors)
+
+
 def sensitivities(op: int, shape: Sequence[int], seed: int) -> List[np.ndarray]:
     """Upstream residual sensitivities G_b (one standard-normal float32 array
     per residual, full size) for the explicit-sensitivity backward."""

@@ -1,7 +1,9 @@
 """GPU parity at the size limits of the C ABI (include/fpde.h): a plane of the
 non-marching axes just below 2^29 nodes, the most the kernels' 32-bit per-plane
 byte offsets address, for a 3-D grid (heat) and a 2-D grid (Burgers, one row
-per plane).  Each array holds ~1.6 G nodes (6.4 GB), so the oracle checks
+per plane), and a 3D+t grid whose time levels hold just below 2^29 nodes (the
+time march's 32-bit offsets within a level; levels more than 4 GB from the
+array's start).  Each array holds ~1.6 G nodes (6.4 GB), so the oracle checks
 sub-grid windows (corners, edge and face middles, centre): residuals on each
 window's interior, and gradients from the oracle's transposed Jacobian applied
 to 2 R / M with the full grid's M, on the nodes at least two away from a cut.
@@ -38,12 +40,35 @@ def _boxes(shape, w):
             for starts in itertools.product(*[p for _, p in picks])]
 
 
+def _device_arrays(wl):
+    """(fields, consts) of a Workload, or of a TiledWorkload (its draws repeated
+    on the device), on cuda:0."""
+    import torch  # noqa: PLC0415
+    dev = torch.device("cuda:0")
+    if isinstance(wl, W.TiledWorkload):
+        n = wl.n_points
+        full = []
+        for v in wl.vectors:
+            vd = torch.from_numpy(v).to(dev)
+            full.append(vd.repeat(-(-n // v.size))[:n].view(wl.shape))
+        nf = len(wl.spec.fields)
+        return full[:nf], full[nf:]
+    return ([torch.from_numpy(f).to(dev) for f in wl.fields],
+            [torch.from_numpy(c).to(dev) for c in wl.consts])
+
+
+def _window(wl, box):
+    if isinstance(wl, W.TiledWorkload):
+        return wl.window(box)
+    return ([np.ascontiguousarray(f[box]) for f in wl.fields],
+            [np.ascontiguousarray(c[box]) for c in wl.consts])
+
+
 def _run_and_check(oracle_mod, wl, w=10):
     import torch  # noqa: PLC0415
     from paper_2607_18020_amd import binding as B  # noqa: PLC0415
     dev = torch.device("cuda:0")
-    fields = [torch.from_numpy(f).to(dev) for f in wl.fields]
-    consts = [torch.from_numpy(c).to(dev) for c in wl.consts]
+    fields, consts = _device_arrays(wl)
     R = [torch.full_like(fields[0], float("nan")) for _ in wl.spec.residuals]
     loss = B.fpde_residual_fwd(wl.op, fields, consts, wl.h, wl.coeffs, residual_out=R)
     dl = torch.ones((), dtype=torch.float64, device=dev)
@@ -67,16 +92,17 @@ def _run_and_check(oracle_mod, wl, w=10):
     # the fused loss against the float64 sum of the stored residuals (row blocks of
     # axis 1, to bound the float64 temporaries)
     ss = 0.0
+    ax = int(np.argmax(wl.shape))  # blocks of the longest axis
+    blk = max(1, (1 << 26) * wl.shape[ax] // int(np.prod(wl.shape)))
     for r in R:
-        for j in range(0, wl.shape[1], 1024):
-            ss += float(r[:, j:j + 1024].double().square().sum().item())
+        for j in range(0, wl.shape[ax], blk):
+            ss += float(r.narrow(ax, j, min(blk, wl.shape[ax] - j)).double().square().sum().item())
     L = float(loss.item())
     assert abs(L - ss / M) <= 1e-9 * abs(L), (L, ss / M)
     del fields, consts
 
     for box in _boxes(wl.shape, w):
-        sub_f = [np.ascontiguousarray(f[box]) for f in wl.fields]
-        sub_c = [np.ascontiguousarray(c[box]) for c in wl.consts]
+        sub_f, sub_c = _window(wl, box)
         sshape = sub_f[0].shape
         Rs = oracle_mod.residual(wl.op, sshape, wl.h, wl.coeffs, sub_f, sub_c)
         for b, rs in enumerate(Rs):
@@ -109,4 +135,19 @@ def test_largest_row_2d(oracle_mod):
     shape = (3, PLANE_LIMIT - 1)
     wl = W.normal_fields_f32(W.BURGERS_1DT, shape, 48, h=(1e-2, 1e-2))
     print(f"case limits burgers {shape}", flush=True)
+    _run_and_check(oracle_mod, wl)
+
+
+def test_largest_level_3dt(oracle_mod):
+    """3D+t NS, 3 x 3 x 16384 x 10922: a time level of 536,838,144 nodes (32,768
+    below 2^29, 2.1 GB per field), so the planes of the last level lie 4.3 to
+    6.4 GB into each array, past 4 GiB from its second plane on.  Inputs: a
+    seeded draw of a prime number of standard normals repeated through each
+    array (1.6 G values per array)."""
+    shape = (3, 3, 16384, 10922)
+    plane = shape[2] * shape[3]
+    assert shape[1] * plane < PLANE_LIMIT
+    assert ((shape[0] - 1) * shape[1] + 1) * plane * 4 > 1 << 32
+    wl = W.normal_tiled_f32(W.NS_3DT, shape, 49, h=(0.5, 1e-2, 1e-2, 1e-2))
+    print(f"case limits ns_3dt {shape}", flush=True)
     _run_and_check(oracle_mod, wl)
