@@ -61,9 +61,9 @@ BARS = {"loss": 1e-5, "residual": 1e-5, "grad": 1e-4}  # max|err| / max|ref|
 DEFAULT_CONFIG = "ns_3d_tgv"
 # (config, path, bc_mode) of the "workloads" object, beside the headline case
 EXTRA_CASES = (("burgers_1dt", "loss", 0), ("helmholtz_2d", "loss", 0), ("heat_3d", "loss", 0),
-               ("ns_2d", "loss", 0), ("ns_3d_tgv", "fused", 0), ("ns_3d_tgv", "residual", 0),
-               ("ns_3d_tgv", "loss", 1), ("ns_3dt", "loss", 0), ("ns_3dt_large", "loss", 0),
-               ("ns_3dt_large", "residual", 0))
+               ("ns_2d", "loss", 0), ("ns_2d", "fused", 0), ("ns_3d_tgv", "fused", 0),
+               ("ns_3d_tgv", "residual", 0), ("ns_3d_tgv", "loss", 1), ("ns_3dt", "loss", 0),
+               ("ns_3dt_large", "loss", 0), ("ns_3dt_large", "residual", 0))
 
 
 def parse():
