@@ -2,9 +2,10 @@
 
 Each case plants one mistake in a copy of the oracle's C source (a flipped
 sign, a transposed operand, a wrong normaliser, a dropped Jacobian term, a
-coefficient off by one part in 1e7, a spacing taken from the wrong axis),
-builds the copy on the CPU and runs the pin suite against it in a fresh
-process.  The pin suite must fail for every mutant.
+coefficient off by one part in 1e7, a spacing taken from the wrong axis, a
+derivative taken along the wrong axis, a source term's sign), builds the copy on
+the CPU and runs the pin suite (the pins and the cross-operator reductions)
+against it in a fresh process.  The pin suite must fail for every mutant.
 """
 from __future__ import annotations
 
@@ -41,6 +42,9 @@ MUTANTS = {
                                     "gr[b][nb(g, iv, m, 0, +1)] -= gm / (2.0 * g->h[0]);"),
     "spacetime_last_axis_dropped": ("for (a = 0; a < d; a++) R[d] += D1(g, F[a], iv, m, a + 1);",
                                     "for (a = 0; a + 1 < d; a++) R[d] += D1(g, F[a], iv, m, a + 1);"),
+    "spacetime_advection_axis": ("for (a = 0; a < d; a++) r += F[a][m] * D1(g, cb, iv, m, a + 1);",
+                                 "for (a = 0; a < d; a++) r += F[a][m] * D1(g, cb, iv, m, a);"),
+    "poisson_source_sign": ("R[0] = lap - C[0][m];", "R[0] = lap + C[0][m];"),
 }
 
 
@@ -57,7 +61,8 @@ def test_pins_reject_mutant(tmp_path, name):
     subprocess.run(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-o",
                     str(tmp_path / "oracle" / "libfpde_oracle.so"), str(csrc), "-lm"], check=True)
     r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
-                        str(tmp_path / "tests" / "test_oracle_pins.py"), "--rootdir", str(tmp_path)],
+                        str(tmp_path / "tests" / "test_oracle_pins.py"),
+                        str(tmp_path / "tests" / "test_oracle_reductions.py"), "--rootdir", str(tmp_path)],
                        cwd=tmp_path, capture_output=True, text=True, timeout=300)
     assert r.returncode == 1, f"pins did not catch mutant {name}:\n{r.stdout[-2000:]}"
     assert "failed" in r.stdout
