@@ -48,8 +48,7 @@ CHECK_FLAGS = [
     "-DFPDE_HEAT_MIN_BWD_BLOCKS=256", "-DFPDE_VJP_TY3=8", "-DFPDE_VJP_HEAT_TX=64",
     "-DFPDE_TX2=128", "-DFPDE_TX2_FWD=256", "-DFPDE_TX2_VG=256", "-DFPDE_BLOCKS2=512",
     "-DFPDE_FWD2_Q=4", "-DFPDE_HEAT_FWD_QUEUE=1", "-DFPDE_NS4_BWD_TX=64", "-DFPDE_NS4_BWD_TY=8",
-    "-DFPDE_BWD2_QUEUE=1", "-DFPDE_NS4_MIN_BLOCKS=700", "-DFPDE_TM_B1=2", "-DFPDE_TM_B2=4", "-DFPDE_TM_B3=64",
-    "-DFPDE_TM_REMAP=1",
+    "-DFPDE_BWD2_QUEUE=1", "-DFPDE_NS4_MIN_BLOCKS=700", "-DFPDE_TM_REMAP=1",
 ]
 
 _NOISE = "is not a recognized feature for this target"

@@ -495,14 +495,11 @@ int launch_bc(const Req& r, const double* dloss) {
 // time levels (after the level march, which wrote the spatial part)
 template <class OP>
 int launch_tm(const Req& r, const double* dloss) {
-    // blocks of TM_B1 x TM_B2 x TM_B3 nodes (fewer than 2^31: a level holds fewer than 2^29)
-    const Dims& d = r.dims;
-    const long long nb = (long long)((d.nx + TM_B3 - 1) / TM_B3) * ((d.ny + TM_B2 - 1) / TM_B2) *
-                         ((d.nz + TM_B1 - 1) / TM_B1);
     int st = FPDE_OK;
-    with_flag(d.per, [&](auto per) {
-        st = launch(tm_kernel<OP, decltype(per)::value>, dim3((unsigned)nb), dim3(TM_NT),
-                    r.stream, r.P, d, r.K, dloss, r.two_over_M);
+    with_flag(r.dims.per, [&](auto per) {
+        st = launch(tm_kernel<OP, decltype(per)::value>,
+                    dim3((unsigned)((r.dims.vol + 255) / 256)), dim3(256), r.stream, r.P, r.dims,
+                    r.K, dloss, r.two_over_M);
     });
     return st;
 }

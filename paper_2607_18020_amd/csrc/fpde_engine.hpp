@@ -1382,47 +1382,27 @@ __device__ __forceinline__ void stars_at_level(const Ptrs& P, int lev, uint32_t 
     }
 }
 
-// Lanes: a workgroup of TM_B1 x TM_B2 x TM_B3 lanes covers a block of as many
-// spatial nodes (along array axes 1, 2, 3; whole 64-lane wavefronts along
-// axis 3), blocks numbered with axis 3 fastest, in launch order or (TM_REMAP)
-// XCD-contiguous.  Each lane marches the time levels on its own, so the rows
-// that neighbouring blocks share meet in L2 only while the blocks run at the
-// same time.  At 20 x 128^3 one row pair per block in launch order (the default)
-// was the fastest of the shapes from 2 x 2 x 64 to 4 x 4 x 64 lanes, and the
-// XCD-contiguous order slower by 3-4% for every shape.
-#ifndef FPDE_TM_B1
-#define FPDE_TM_B1 1
-#endif
-#ifndef FPDE_TM_B2
-#define FPDE_TM_B2 2
-#endif
-#ifndef FPDE_TM_B3
-#define FPDE_TM_B3 128
-#endif
+// Lanes: one per spatial node of a level, 256 consecutive nodes per workgroup,
+// in launch order or (FPDE_TM_REMAP) XCD-contiguous.  Each lane marches the
+// time levels on its own, so the rows that neighbouring workgroups share meet
+// in L2 only while those workgroups run at the same time.  At 20 x 128^3 this
+// order was the fastest of the lane blocks tried (2 x 2 x 64 up to 4 x 4 x 64
+// nodes, and 128-wide blocks of 1 to 8 rows: 1-8% slower), and the
+// XCD-contiguous order 3-4% slower; unlike a block, it leaves no lane idle
+// whatever the extent of the last axis.
 #ifndef FPDE_TM_REMAP
 #define FPDE_TM_REMAP 0
 #endif
-constexpr int TM_B1 = FPDE_TM_B1, TM_B2 = FPDE_TM_B2, TM_B3 = FPDE_TM_B3;
-constexpr int TM_NT = TM_B1 * TM_B2 * TM_B3;
-static_assert(TM_B3 % 64 == 0 && TM_NT <= 1024, "whole wavefronts along axis 3");
 
 template <class OP, bool PER>
-__global__ __launch_bounds__(TM_NT) void tm_kernel(Ptrs P, Dims D, KCoef K, const double* dloss,
-                                                   double two_over_M) {
+__global__ __launch_bounds__(256) void tm_kernel(Ptrs P, Dims D, KCoef K, const double* dloss,
+                                                 double two_over_M) {
     constexpr int NF = OP::NF, D3 = OP::D;
     static_assert(OP::NC == 2 * D3, "consts: the velocities at t - 1, then at t + 1");
-    const int n3 = (D.nx + TM_B3 - 1) / TM_B3, n2 = (D.ny + TM_B2 - 1) / TM_B2;
-    int blk = (int)blockIdx.x;
-    if (FPDE_TM_REMAP) blk = remap_xcd(blk, (int)gridDim.x);
-    const int b3 = blk % n3;
-    blk /= n3;
-    const int b2 = blk % n2, b1 = blk / n2;
-    const int lt = (int)threadIdx.x;
-    const int i3 = b3 * TM_B3 + lt % TM_B3;
-    const int i2 = b2 * TM_B2 + (lt / TM_B3) % TM_B2;
-    const int i1 = b1 * TM_B1 + lt / (TM_B3 * TM_B2);
-    if (i1 >= D.nz || i2 >= D.ny || i3 >= D.nx) return;
-    const int idx = (i1 * D.ny + i2) * D.nx + i3;  // (vol < 2^29)
+    const int blk = FPDE_TM_REMAP ? remap_xcd((int)blockIdx.x, (int)gridDim.x) : (int)blockIdx.x;
+    const int idx = blk * 256 + (int)threadIdx.x;  // (vol < 2^29)
+    if (idx >= (int)D.vol) return;
+    const int i3 = idx % D.nx, r = idx / D.nx, i2 = r % D.ny, i1 = r / D.ny;
     if (!PER && !(i1 >= 1 && i1 <= D.nz - 2 && i2 >= 1 && i2 <= D.ny - 2 && i3 >= 1 &&
                   i3 <= D.nx - 2))
         return;  // off the spatial residual set: no time part
