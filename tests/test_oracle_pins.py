@@ -467,6 +467,46 @@ def test_heat_without_diffusion_is_pointwise(oracle_mod):
     np.testing.assert_allclose(g, want, rtol=1e-13, atol=1e-15)
 
 
+def _lap_numpy(u, h):
+    """The 5/7-point Laplacian on the interior by array slicing (independent of
+    the oracle's stencil code); zero on the shell."""
+    out = np.zeros_like(u)
+    inner = tuple(slice(1, n - 1) for n in u.shape)
+    for a, ha in enumerate(h):
+        lo = list(inner)
+        hi = list(inner)
+        lo[a] = slice(0, u.shape[a] - 2)
+        hi[a] = slice(2, u.shape[a])
+        out[inner] += (u[tuple(hi)] - 2.0 * u[inner] + u[tuple(lo)]) / (ha * ha)
+    return out
+
+
+@pytest.mark.parametrize("case", ["helmholtz", "poisson_2d", "poisson_3d", "heat"])
+def test_zero_residual_when_the_source_matches(oracle_mod, case):
+    """The residual vanishes on the residual set when the const is built from
+    the field by the operator's own definition: f := lap u + k^2 u (Helmholtz),
+    f := lap u (Poisson), u0 := u - dt alpha lap u (heat); and the gradient of
+    a zero loss is zero everywhere."""
+    op, nd, co = {"helmholtz": (W.HELMHOLTZ_2D, 2, W.Coeffs(k=2.5)),
+                  "poisson_2d": (W.POISSON_2D, 2, W.Coeffs()),
+                  "poisson_3d": (W.POISSON_3D, 3, W.Coeffs()),
+                  "heat": (W.HEAT_3D_BE, 3, W.Coeffs(dt=0.02, alpha=0.1))}[case]
+    shape, h = SHAPES[nd], H[nd]
+    u = np.random.default_rng(1000 + op).standard_normal(shape)
+    lap = _lap_numpy(u, h)
+    if op == W.HELMHOLTZ_2D:
+        c = lap + co.k ** 2 * u
+    elif op == W.HEAT_3D_BE:
+        c = u - co.dt * co.alpha * lap
+    else:
+        c = lap
+    R = oracle_mod.residual(op, shape, h, co, [u], [c])[0]
+    scale = np.abs(lap).max()
+    assert np.abs(R).max() <= 1e-12 * scale, np.abs(R).max() / scale
+    g = oracle_mod.grad(op, shape, h, co, [u], [c])[0]
+    assert np.abs(g).max() <= 1e-12 * scale
+
+
 @pytest.mark.parametrize("op", OPS)
 def test_edges_and_corners_have_zero_gradient(oracle_mod, op):
     """A node with two or more boundary coordinates touches no interior residual."""
