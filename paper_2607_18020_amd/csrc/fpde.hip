@@ -74,6 +74,12 @@ namespace {
 #ifndef FPDE_HEAT_FWD_QUEUE
 #define FPDE_HEAT_FWD_QUEUE 0
 #endif
+// one stencil field and almost no arithmetic per plane: the LDS march forward
+// keeps several planes in flight (an 8-slot ring), where one plane per step
+// would wait for each plane's latency in turn
+#ifndef FPDE_HEAT_FWD_RING
+#define FPDE_HEAT_FWD_RING 8
+#endif
 // 2-D backward: the LDS march (bwd_kernel with one-row tiles); the checking
 // build takes the register-queue march (bwdq_kernel: no LDS, no barrier; NW
 // waves of 62 output columns, Q rows in registers) as a second algorithm whose
@@ -121,10 +127,12 @@ constexpr bool kBwdReverse = FPDE_BWD_REVERSE != 0;
 
 // 3-D grids: forward tile TXF x TYf, backward tile TXB x TYb, explicit-sensitivity
 // backward tile TXV x TYV
-template <int TXF_, int TYF, int TXB_, int TYB, int MINB, int TXV_, int TYV_, bool QF = false>
+template <int TXF_, int TYF, int TXB_, int TYB, int MINB, int TXV_, int TYV_, bool QF = false,
+          int RF = 4>
 struct Geo3 {
     static constexpr bool D3 = true;
     static constexpr bool FWD_QUEUE = QF;  // forward: fwdq_kernel (else the LDS march)
+    static constexpr int FWD_RING = RF;    // LDS march forward: slots of its plane ring
     static constexpr int TXF = TXF_, TYf = TYF, TXB = TXB_, TYb = TYB, MIN_BWD_BLOCKS = MINB;
     static constexpr int TXV = TXV_, TYV = TYV_;
 };
@@ -156,7 +164,7 @@ using GeoNS4 = Geo3<FPDE_NS3_FWD_TX, FPDE_NS3_FWD_TY, FPDE_NS4_BWD_TX, FPDE_NS4_
 // one field, a Laplacian (heat, Poisson)
 using GeoHeat = Geo3<FPDE_HEAT_FWD_TX, FPDE_HEAT_FWD_TY, FPDE_HEAT_BWD_TX, FPDE_HEAT_BWD_TY,
                      FPDE_HEAT_MIN_BWD_BLOCKS, FPDE_VJP_HEAT_TX, FPDE_VJP_HEAT_TY,
-                     FPDE_HEAT_FWD_QUEUE != 0>;
+                     FPDE_HEAT_FWD_QUEUE != 0, FPDE_HEAT_FWD_RING>;
 
 template <class OP_, class GEO_>
 struct OpTag {
@@ -402,7 +410,7 @@ void with_flag(bool v, F&& f) {
     else f(std::false_type{});
 }
 
-template <class OP, int TX, int TY>
+template <class OP, int TX, int TY, int RD>
 int launch_fwd(const Req& r, bool store, double* loss, int zc) {
     const Dims dm = tile_dims(r.dims, TX, TY, zc);
     int st = zero_loss(r, loss);
@@ -414,7 +422,7 @@ int launch_fwd(const Req& r, bool store, double* loss, int zc) {
     }
     with_flag(store, [&](auto sr) {
         with_flag(dm.per, [&](auto per) {
-            st = launch(fwd_kernel<OP, TX, TY, decltype(sr)::value, decltype(per)::value>,
+            st = launch(fwd_kernel<OP, TX, TY, decltype(sr)::value, decltype(per)::value, RD>,
                         dim3(dm.nblocks), dim3(TX * TY), r.stream, r.P, dm, r.K, r.inv_M, loss);
         });
     });
@@ -542,7 +550,7 @@ int run_fwd(const Req& r0, bool store, double* loss) {
         if constexpr (GEO::D3 && GEO::FWD_QUEUE)
             return launch_fwdq<OP, GEO::TXF, GEO::TYf>(r, store, loss, zc3<GEO>(r));
         else if constexpr (GEO::D3)
-            return launch_fwd<OP, GEO::TXF, GEO::TYf>(r, store, loss, zc3<GEO>(r));
+            return launch_fwd<OP, GEO::TXF, GEO::TYf, GEO::FWD_RING>(r, store, loss, zc3<GEO>(r));
         else
             return launch_fwdq<OP, kTX2F, 1>(r, store, loss, zc2(r));
     });

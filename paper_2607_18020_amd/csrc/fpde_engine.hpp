@@ -212,19 +212,30 @@ __device__ __forceinline__ void time_level(Ptrs& P, const Dims& D, int lev) {
 template <int V>
 using IC = std::integral_constant<int, V>;
 
-// The LDS ring slots are four distinct __shared__ arrays, picked by a
-// compile-time index.  Distinct objects let the compiler see that a slot being
-// filled by buffer_load ... lds is not one being read, so the reads of a step
-// do not wait for the plane that the same step queues.
-#define FPDE_SLOT_RING(T, NAME, D1, D2)                                              \
-    __shared__ T NAME##0[D1][D2], NAME##1[D1][D2], NAME##2[D1][D2], NAME##3[D1][D2]; \
-    auto NAME = [&](auto sc) __attribute__((always_inline)) -> T(*)[D2] {            \
-        constexpr int S_ = decltype(sc)::value & 3;                                  \
-        if constexpr (S_ == 0) return NAME##0;                                       \
-        else if constexpr (S_ == 1) return NAME##1;                                  \
-        else if constexpr (S_ == 2) return NAME##2;                                  \
-        else return NAME##3;                                                         \
+// The LDS ring slots are N (4 or 8) distinct __shared__ arrays, picked by a
+// compile-time index modulo N.  Distinct objects let the compiler see that a
+// slot being filled by buffer_load ... lds is not one being read, so the reads
+// of a step do not wait for the plane that the same step queues.  (Slots 4..7
+// of a 4-slot ring are one-element placeholders that nothing references.)
+#define FPDE_SLOT_RING_N(T, NAME, N, D1, D2)                                              \
+    static_assert((N) == 4 || (N) == 8, "rings of 4 or 8 slots");                         \
+    __shared__ T NAME##0[D1][D2], NAME##1[D1][D2], NAME##2[D1][D2], NAME##3[D1][D2];      \
+    __shared__ T NAME##4[(N) > 4 ? (D1) : 1][(N) > 4 ? (D2) : 1],                         \
+        NAME##5[(N) > 4 ? (D1) : 1][(N) > 4 ? (D2) : 1],                                  \
+        NAME##6[(N) > 4 ? (D1) : 1][(N) > 4 ? (D2) : 1],                                  \
+        NAME##7[(N) > 4 ? (D1) : 1][(N) > 4 ? (D2) : 1];                                  \
+    auto NAME = [&](auto sc) __attribute__((always_inline)) -> T(*)[D2] {                 \
+        constexpr int S_ = decltype(sc)::value % (N);                                     \
+        if constexpr (S_ == 0) return NAME##0;                                            \
+        else if constexpr (S_ == 1) return NAME##1;                                       \
+        else if constexpr (S_ == 2) return NAME##2;                                       \
+        else if constexpr (S_ == 3) return NAME##3;                                       \
+        else if constexpr (S_ == 4) return reinterpret_cast<T(*)[D2]>(&NAME##4[0][0]);    \
+        else if constexpr (S_ == 5) return reinterpret_cast<T(*)[D2]>(&NAME##5[0][0]);    \
+        else if constexpr (S_ == 6) return reinterpret_cast<T(*)[D2]>(&NAME##6[0][0]);    \
+        else return reinterpret_cast<T(*)[D2]>(&NAME##7[0][0]);                           \
     }
+#define FPDE_SLOT_RING(T, NAME, D1, D2) FPDE_SLOT_RING_N(T, NAME, 4, D1, D2)
 
 // Checking build (FPDE_LDS_POISON): every LDS array of a marching kernel is
 // filled with NaN before the march, so that a read of a location no load or
@@ -243,6 +254,10 @@ __device__ __forceinline__ void poison_lds(float* p, int n) {
             poison_lds(&NAME##1[0][0], (int)(sizeof(NAME##1) / 4));         \
             poison_lds(&NAME##2[0][0], (int)(sizeof(NAME##2) / 4));         \
             poison_lds(&NAME##3[0][0], (int)(sizeof(NAME##3) / 4));         \
+            poison_lds(&NAME##4[0][0], (int)(sizeof(NAME##4) / 4));         \
+            poison_lds(&NAME##5[0][0], (int)(sizeof(NAME##5) / 4));         \
+            poison_lds(&NAME##6[0][0], (int)(sizeof(NAME##6) / 4));         \
+            poison_lds(&NAME##7[0][0], (int)(sizeof(NAME##7) / 4));         \
         }                                                                   \
     } while (0)
 
@@ -370,18 +385,41 @@ struct PlaneStream {
 // ---------------------------------------------------------------------------
 // Forward: residuals of one chunk of planes + fused sum of squares.  Each plane
 // (tile rows plus one row above and below, and the side-edge x-neighbours)
-// streams from memory straight into a 4-slot LDS ring; the 7-point star of
-// every field is read from the slots of planes z-1, z, z+1.  One barrier per
-// step: plane z+2 streams into the slot of plane z-2 while plane z is
-// evaluated.  The sum of squares is accumulated per thread in float64, reduced
-// with DPP across the wavefront and through LDS across waves, then added with
-// ONE float64 atomic per workgroup.
+// streams from memory straight into an LDS ring of RD slots; the 7-point star
+// of every field is read from the slots of planes z-1, z, z+1.  One barrier per
+// step: plane z + RD - 2 streams into the slot of plane z-2 while plane z is
+// evaluated, and the consts come CD - 1 planes ahead into registers.  The sum
+// of squares is accumulated per thread in float64, reduced with DPP across the
+// wavefront and through LDS across waves, then added with ONE float64 atomic
+// per workgroup.
+//
+// RD = 4: the plane queued in a step is read in the next one, and the barrier
+// waits for it (the operators with several fields, whose arithmetic per step
+// covers a plane's latency; their LDS holds no more slots anyway).  RD = 8: the
+// plane queued in a step is read five steps later, so that an operator with
+// one field and almost no arithmetic per step keeps several planes in flight;
+// the barrier waits, by an explicit count, only for the plane queued four
+// steps earlier, which the next step reads first.
 
-template <class OP, int TX, int TY, bool STORE_R, bool PER>
+template <class F, int... I>
+__device__ __forceinline__ void unroll_seq(F&& f, std::integer_sequence<int, I...>) {
+    (f(IC<I>{}), ...);
+}
+
+// Waits until at most N vector-memory operations of this wave are in flight
+// and its LDS operations are done, then the workgroup barrier.
+template <int N>
+__device__ __forceinline__ void barrier_after() {
+    static_assert(N >= 0 && N <= 63, "vmcnt counts 0 .. 63");
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
+template <class OP, int TX, int TY, bool STORE_R, bool PER, int RD = 4>
 __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims D, KCoef K,
                                                                     double inv_M, double* loss) {
     constexpr int DIM = OP::DIM, NF = OP::NF, NC = OP::NC, NR = OP::NR, NT = TX * TY;
     constexpr int NC1 = NC > 0 ? NC : 1;
+    constexpr int CD = RD / 2;  // const queue: planes z .. z + CD - 1 in registers
     constexpr int HY = (DIM == 3) ? 1 : 0;
     // A slot holds the tile's own TX columns for TY + 2 HY rows, so that every
     // wavefront's plane load is one aligned 64-node row segment (a halo column in
@@ -394,7 +432,22 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
     static_assert(2 * TY <= 64, "the side-edge neighbours fill one 64-element group");
     using PS = PlaneStream<XG + 64, NT>;
     static_assert(DIM == 3 || TY == 1, "2-D grids use one-row tiles");
-    FPDE_SLOT_RING(float, sF, NF, PS::FSZS);
+    FPDE_SLOT_RING_N(float, sF, RD, NF, PS::FSZS);
+    // vector-memory operations a wave issues per step, in this order: the plane
+    // loads (every wave the same number), the const loads, the residual stores
+    constexpr int kPlaneOps = PS::KP * NF, kStepOps = kPlaneOps + NC + (STORE_R ? NR : 0);
+    // At the end of step w, step w + 1 needs plane z + 2, queued in step
+    // w - (RD - 4), or for w < RD - 4 in the prologue (RD - 1 plane groups, then
+    // CD - 1 const groups); the operations issued after it may stay in flight:
+    //   w >= RD - 4:  (kStepOps - kPlaneOps) + (RD - 4) kStepOps
+    //   w <  RD - 4:  (RD - 5 - w) kPlaneOps + (CD - 1) NC + (w + 1) kStepOps
+    constexpr int kInFlight = (kStepOps - kPlaneOps) + (RD - 4) * kStepOps;
+    constexpr auto in_flight_early = [](int w) {
+        const int k = (RD - 5 - w) * kPlaneOps + (CD - 1) * NC + (w + 1) * kStepOps;
+        return k < kInFlight ? k : kInFlight;
+    };
+    static_assert(RD == 4 || kInFlight <= 63, "a vmcnt wait counts at most 63 operations");
+    static_assert(RD == 4 || RD == 8, "rings of 4 or 8 slots");
 
     const int t = threadIdx.x, tx = t % TX, ty = t / TX;
     FPDE_POISON_RING(sF);
@@ -435,7 +488,7 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
         for (int f = 0; f < NF; ++f) dst[f] = &sF(slot)[f][0];
         ps.template load<NF>(P.f, pz, D.nz, pbytes, dst);
     };
-    float cv[2][NC1];
+    float cv[CD][NC1];
     auto load_consts = [&](int pz, bool ok, float* c) __attribute__((always_inline)) {
 #pragma unroll
         for (int j = 0; j < NC; ++j)
@@ -455,11 +508,17 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
         }
     }
 
-    // plane z0 + j lives in slot (j + 1) & 3; prologue: planes z0-1, z0, z0+1
-    load_plane(zw(z0 - 1), IC<0>{});
-    load_plane(z0, IC<1>{});
-    load_plane(zw(z0 + 1), IC<2>{});
-    load_consts(z0, true, cv[0]);
+    // plane z0 + j lives in slot (j + 1) % RD; prologue: planes z0 - 1 .. z0 + RD - 3
+    // (planes past the chunk's stencil, or past the grid, are harmless: unread, or
+    // read as 0), consts of planes z0 .. z0 + CD - 2
+    unroll_seq([&](auto jc) __attribute__((always_inline)) {
+        constexpr int J = decltype(jc)::value;  // slot J holds plane z0 + J - 1
+        load_plane(J == 1 ? z0 : zw(z0 + J - 1), IC<J>{});
+    }, std::make_integer_sequence<int, RD - 1>{});
+    unroll_seq([&](auto jc) __attribute__((always_inline)) {
+        constexpr int J = decltype(jc)::value;
+        load_consts(z0 + J, J == 0 || J < L, cv[J]);  // (a chunk holds a plane at least)
+    }, std::make_integer_sequence<int, CD - 1>{});
     __syncthreads();
 
     const int own = (ty + HY) * LX + tx;  // own node in a slot
@@ -467,17 +526,17 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
     const int xm = tx == 0 ? XG + ty : own - 1, xp = tx == TX - 1 ? XG + TY + ty : own + 1;
     double acc = 0.0;
     auto step = [&](auto jc, int w) __attribute__((always_inline)) {
-        constexpr int J = decltype(jc)::value;  // w & 3
-        constexpr int SM = J & 3, SC = (J + 1) & 3, SP = (J + 2) & 3, SQ = (J + 3) & 3;
-        constexpr int CUR = J & 1, NXT = (J + 1) & 1;
+        constexpr int J = decltype(jc)::value;  // w % RD
+        constexpr int SM = J % RD, SC = (J + 1) % RD, SP = (J + 2) % RD, SQ = (J + RD - 1) % RD;
+        constexpr int CUR = J % CD, NXT = (J + CD - 1) % CD;
         const int z = z0 + w;
-        const bool more = w + 1 < L;
-        // plane z+2 goes to the slot of plane z-2, last read before the previous barrier
-        load_plane(more ? zw(z + 2) : -1, IC<SQ>{});
+        // plane z + RD - 2 goes to the slot of plane z - 2, last read before the
+        // previous barrier; it is in the chunk's stencil if z + RD - 2 <= z1
+        load_plane(w + RD - 3 < L ? zw(z + RD - 2) : -1, IC<SQ>{});
         // the plane loads go first: the barrier then waits for them alone, not
-        // for the const loads queued after them for the next step
+        // for the const loads queued after them for later steps
         __builtin_amdgcn_sched_barrier(0);
-        load_consts(z + 1, more, cv[NXT]);
+        load_consts(z + CD - 1, w + CD - 1 < L, cv[NXT]);
         Star s[NF];
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
@@ -507,19 +566,31 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
             for (int b = 0; b < NR; ++b)
                 bst<kStream>(plane_rsrc(P.out[b], z, pbytes), so, interior ? R[b] : 0.f);
         }
-        __syncthreads();  // (waits for the plane loads into LDS as well)
+        if constexpr (RD == 4) {
+            __syncthreads();  // (waits for the plane loads into LDS as well)
+        } else {
+            // the plane step w + 1 reads first, and every earlier operation, has
+            // landed (operations retire in order); the LDS reads of this step are
+            // done; then the workgroup's barrier (w is uniform)
+            if (w >= RD - 4) barrier_after<kInFlight>();
+            else if (w == 0) barrier_after<in_flight_early(0)>();
+            else if (w == 1) barrier_after<in_flight_early(1)>();
+            else if (w == 2) barrier_after<in_flight_early(2)>();
+            else barrier_after<in_flight_early(3)>();
+        }
     };
 
     int w = 0;
-    for (; w + 4 <= L; w += 4) {  // slot indices are constants in each copy
-        step(IC<0>{}, w);
-        step(IC<1>{}, w + 1);
-        step(IC<2>{}, w + 2);
-        step(IC<3>{}, w + 3);
-    }
-    if (w < L) step(IC<0>{}, w);
-    if (w + 1 < L) step(IC<1>{}, w + 1);
-    if (w + 2 < L) step(IC<2>{}, w + 2);
+    for (; w + RD <= L; w += RD)  // slot indices are constants in each copy
+        unroll_seq([&](auto jc) __attribute__((always_inline)) {
+            step(jc, w + decltype(jc)::value);
+        }, std::make_integer_sequence<int, RD>{});
+    unroll_seq([&](auto jc) __attribute__((always_inline)) {
+        if (w + decltype(jc)::value < L) step(jc, w + decltype(jc)::value);
+    }, std::make_integer_sequence<int, RD - 1>{});
+    // nothing still streams into LDS when the workgroup's LDS is reused below
+    // or handed to the next workgroup
+    if constexpr (RD != 4) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     block_atomic_sum<NT>(acc * inv_M, loss);
 }
 
@@ -539,10 +610,6 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
 // chunk's stencil and outside the grid are read through empty descriptors (0,
 // no access).
 
-template <class F, int... I>
-__device__ __forceinline__ void unroll_seq(F&& f, std::integer_sequence<int, I...>) {
-    (f(IC<I>{}), ...);
-}
 
 template <class OP, int TX, int TY, int Q, bool STORE_R, bool PER>
 __global__ __launch_bounds__(TX* TY) void fwdq_kernel(Ptrs P, Dims D, KCoef K, double inv_M,

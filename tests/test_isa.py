@@ -30,7 +30,7 @@ def test_design_rules(kernels):
 
 
 def test_ns3d_kernels(kernels):
-    fwd = kernels["fwd_kernel<OpNS<3, true>, 128, 4, false, false>"]
+    fwd = kernels["fwd_kernel<OpNS<3, true>, 128, 4, false, false, 4>"]
     bwd = kernels["bwd_kernel<OpNS<3, true>, 128, 8, true, false, false>"]
     vg = kernels["bwd_kernel<OpNS<3, true>, 128, 8, true, true, false>"]
     bc = kernels["bc_kernel<OpNS<3, true> >"]
