@@ -515,6 +515,8 @@ __global__ __launch_bounds__(TX* TY, FPDE_FWD_MINW) void fwd_kernel(Ptrs P, Dims
         constexpr int J = decltype(jc)::value;  // slot J holds plane z0 + J - 1
         load_plane(J == 1 ? z0 : zw(z0 + J - 1), IC<J>{});
     }, std::make_integer_sequence<int, RD - 1>{});
+    // (the plane loads first, as in the steps: the wait counts assume that order)
+    __builtin_amdgcn_sched_barrier(0);
     unroll_seq([&](auto jc) __attribute__((always_inline)) {
         constexpr int J = decltype(jc)::value;
         load_consts(z0 + J, J == 0 || J < L, cv[J]);  // (a chunk holds a plane at least)

@@ -105,6 +105,42 @@ def parse(asm: str) -> Dict[str, dict]:
     return kernels
 
 
+def memory_stream(asm: str, kernel: str) -> List[str]:
+    """The kernel's vector-memory operations, explicit barrier waits and
+    barriers in code order: "D" a load into LDS, "L" a load into registers,
+    "S" a store, "A" an atomic, "W<n>" an `s_waitcnt vmcnt(n) lgkmcnt(0)`
+    directly before an `s_barrier`, "B" the barrier.  (Code order, not
+    execution order: loops and branches are not followed.)"""
+    lines = asm.splitlines()
+    starts = [(i, m.group(1)) for i, ln in enumerate(lines)
+              for m in [re.match(r"^(_Z\w+):", ln)] if m]
+    names = _demangle([n for _, n in starts])
+    for k, (i0, mangled) in enumerate(starts):
+        if names[mangled] != kernel:
+            continue
+        i1 = starts[k + 1][0] if k + 1 < len(starts) else len(lines)
+        body = [ln.strip() for ln in lines[i0 + 1:i1]]
+        body = [s for s in body if s and not s.startswith((";", ".")) and not s.endswith(":")]
+        out: List[str] = []
+        for j, s in enumerate(body):
+            op = s.split()[0]
+            if op.startswith(("buffer_", "global_", "flat_")):
+                if "atomic" in op:
+                    out.append("A")
+                elif re.search(r"\blds\b", s):
+                    out.append("D")
+                else:
+                    out.append("L" if "load" in op else "S")
+            elif op == "s_barrier":
+                out.append("B")
+            else:
+                m = re.match(r"s_waitcnt vmcnt\((\d+)\) lgkmcnt\(0\)$", s)
+                if m and j + 1 < len(body) and body[j + 1].startswith("s_barrier"):
+                    out.append("W" + m.group(1))
+        return out
+    raise KeyError(kernel)
+
+
 def _template_args(name: str) -> List[str]:
     args = name[name.index("<") + 1:name.rindex(">")]
     out, depth, cur = [], 0, ""
