@@ -12,7 +12,8 @@ from paper_2607_18020_amd import workloads as W
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("cfg,shape", [("ns_3d_tgv", (30, 40, 130)), ("ns_2d", (200, 600))])
+@pytest.mark.parametrize("cfg,shape", [("ns_3d_tgv", (30, 40, 130)), ("ns_2d", (200, 600)),
+                                       ("heat_3d", (19, 21, 130)), ("ns_3dt", (6, 19, 21, 70))])
 def test_graph_replays_match_eager(cfg, shape):
     import torch  # noqa: PLC0415
     from paper_2607_18020_amd import binding as B  # noqa: PLC0415
