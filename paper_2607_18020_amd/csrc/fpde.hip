@@ -312,7 +312,9 @@ int validate_common(int op, const fpde_grid4* g, const fpde_coeffs* c, const flo
     dm.lev0 = 0;
     dm.vol = r->d.time ? (long long)dm.nz * dm.ny * dm.nx : 0;
     // every launch shape used below must have fewer than 2^31 workgroups
-    if ((long long)(dm.nx / 32 + 1) * (dm.ny + 1) * (dm.nz + 1) * dm.nt >= (1LL << 31))
+    // (in 64 bits: an extent of axis 0 may be up to 2^31 - 1)
+    if (((long long)dm.nx / 32 + 1) * ((long long)dm.ny + 1) * ((long long)dm.nz + 1) * dm.nt >=
+        (1LL << 31))
         return FPDE_ERR_SHAPE;
     return FPDE_OK;
 }
