@@ -160,6 +160,9 @@ def test_validation_status_codes(B, fn):
     # every launch shape stays below 2^31 workgroups (so the node count below 2^36)
     assert _call(B, fn, op2, (1 << 26, 1 << 10)) == SHAPE
     assert _call(B, fn, op3, (1 << 20, 1 << 10, 1 << 10)) == SHAPE
+    # the longest first axis the rank checks allow (the count is taken in 64 bits)
+    assert _call(B, fn, op2, ((1 << 31) - 1, 3)) == SHAPE
+    assert _call(B, fn, op3, ((1 << 31) - 1, 9, 9)) == SHAPE
 
 
 @pytest.mark.parametrize("fn", ["fwd", "bwd", "bc", "vjp", "vg"])
