@@ -1,5 +1,6 @@
-"""Host-side parts of bench.py (no GPU): the byte model and the all-core CPU
-baseline, whose slab passes must reproduce the whole-grid oracle."""
+"""Host-side parts of bench.py (no GPU): the byte model, the all-core CPU
+baseline, whose slab passes must reproduce the whole-grid oracle, the parity
+verdict and the choice of the profile record behind roofline.traffic."""
 from __future__ import annotations
 
 import numpy as np
@@ -45,3 +46,28 @@ def test_parity_verdict():
     ok = bench.parity_of((2.0 * (1 + 5e-6), [np.ones(4) * (1 + 5e-5)], None), ref)
     bad = bench.parity_of((2.0 * (1 + 2e-5), [np.ones(4)], None), ref)
     assert ok["ok"] and not bad["ok"]
+
+
+def test_measured_traffic_only_for_matching_records(tmp_path, monkeypatch):
+    """roofline.traffic comes from the profile record of the same workload and
+    bench path, summed over the named kernels, and only while the record's
+    kernel-source hash is the current one."""
+    import json  # noqa: PLC0415
+
+    from paper_2607_18020_amd import profiling  # noqa: PLC0415
+    (tmp_path / "profiles").mkdir()
+    rec = {"source_hash": "abc", "workload": "ns_3d_tgv 256^3", "path": "loss",
+           "kernels": {"bwd_kernel<OpNS<3, true>, 128, 8, true, false, false>":
+                       {"fetch_bytes": 100.0, "write_bytes": 20.0},
+                       "fill_f64_kernel": {"fetch_bytes": 1.0, "write_bytes": 0.0}}}
+    (tmp_path / "profiles" / "traffic_x.json").write_text(json.dumps(rec))
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(profiling, "source_hash", lambda root=None: "abc")
+    op = W.CONFIGS["ns_3d_tgv"].op
+    assert bench.measured_traffic("ns_3d_tgv", op, ["bwd"]) == 120
+    assert bench.measured_traffic("ns_3d_tgv", op, ["bwd", "fill_f64"]) == 121
+    assert bench.measured_traffic("ns_3d_tgv", op, ["bwd"], path="fused") is None
+    assert bench.measured_traffic("heat_3d", op, ["bwd"]) is None
+    assert bench.measured_traffic("ns_3d_tgv", op, ["fwd"]) is None  # no such kernel
+    monkeypatch.setattr(profiling, "source_hash", lambda root=None: "changed")
+    assert bench.measured_traffic("ns_3d_tgv", op, ["bwd"]) is None
