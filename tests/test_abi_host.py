@@ -241,3 +241,20 @@ def test_product_path_shares_nothing_with_the_oracle():
                 assert not re.search(r"^\s*(from|import)\s+oracle\b", src, re.M), fn
                 assert "fpde_oracle" not in src, fn
                 assert "orc_" not in src, fn
+
+
+def test_no_fallback_without_the_library_or_a_gpu(B, tmp_path):
+    """The binding has no CPU path: without the built library every entry point
+    raises ImportError, and host (CPU) tensors are refused before any call."""
+    import torch  # noqa: PLC0415
+    wl = W.make("ns_3d_tgv", seed=1, shape=(5, 6, 7))
+    f = [torch.from_numpy(x) for x in wl.fields]
+    c = [torch.from_numpy(x) for x in wl.consts]
+    with pytest.raises(ImportError):
+        with B.library(str(tmp_path / "libfpde_missing.so")):
+            pass
+    assert B.lib() is not None  # (the product library again after the block)
+    with pytest.raises(ValueError, match="CUDA"):
+        B.fpde_residual_fwd(wl.op, f, c, wl.h, wl.coeffs)
+    with pytest.raises(ValueError, match="CUDA"):
+        B.fpde_residual_vjp(wl.op, f, wl.h, wl.coeffs, [x.clone() for x in f])
