@@ -114,7 +114,10 @@ typedef enum fpde_op {
  * axis (the fully periodic reading of the Taylor-Green grid); other values are
  * rejected with FPDE_ERR_ARG.  Entries past ndim are ignored.
  * Limits: every n_a >= 3 and n_a < 2^31; a plane of the non-marching axes
- * (n[1]*n[2] for ndim 3, n[1] for ndim 2) holds fewer than 2^29 nodes. */
+ * (n[1]*n[2] for ndim 3, n[1] for ndim 2) holds fewer than 2^29 nodes; and every
+ * launch stays below 2^31 workgroups: (n[ndim-1]/32 + 1) * (n[1] + 1) * (n[0] + 1)
+ * < 2^31 for ndim 3, with 2 in place of n[1] + 1 for ndim 2 (grids up to about
+ * 2^36 nodes).  Beyond any limit: FPDE_ERR_SHAPE. */
 typedef struct fpde_grid {
     int32_t ndim;
     int32_t bc_mode;
@@ -124,8 +127,9 @@ typedef struct fpde_grid {
 
 /* The grid with up to four axes (a versioned fpde_grid: same members, one more
  * axis), taken by the entry points ending in 4.  Rules as fpde_grid; for
- * ndim 4 the limits are every n_a >= 3, n_a < 2^31, and a time level of the
- * last three axes (n[1]*n[2]*n[3]) below 2^29 nodes. */
+ * ndim 4 the limits are every n_a >= 3, n_a < 2^31, a time level of the last
+ * three axes (n[1]*n[2]*n[3]) below 2^29 nodes, and
+ * (n[3]/32 + 1) * (n[2] + 1) * (n[1] + 1) * n[0] < 2^31 (workgroups). */
 typedef struct fpde_grid4 {
     int32_t ndim;
     int32_t bc_mode;
