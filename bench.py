@@ -17,17 +17,21 @@ Protocol (the paper's: median of five runs, Sec. 4.1):
   2. --runs runs of K back-to-back steps, each between two HIP events and
      nothing else: `value` and `ms_per_step` are the MEDIAN run, all runs are
      listed under "runs";
-  3. a separate pass per kernel of the step: K steps with HIP events around
-     that kernel only; its median over the K steps is the kernel's duration
-     ("kernel_us"), from which `roofline` is computed for the dominant kernel;
-  4. "flushed": steps timed one by one after reading 512 MB between them (every
+  3. "steady_state": 0.5 s more of untimed steps, then the same runs again.  A
+     new load runs slower for its first few tens of ms, and with a short
+     warm-up the runs of step 2 fall in that time;
+  4. a separate pass per kernel of the step, after step 3: K steps with HIP
+     events around that kernel only; its median over the K steps is the
+     kernel's duration ("kernel_us"), from which `roofline` is computed for
+     the dominant kernel;
+  5. "flushed": steps timed one by one after reading 512 MB between them (every
      input then comes from HBM rather than the 256 MB memory-side cache);
      "flushed_dirty" writes the 512 MB instead, so the step also pays for
      writing back the dirty lines the write leaves in the caches;
-  5. "workloads" (default config only; --no-workloads skips it): the same
+  6. "workloads" (default config only; --no-workloads skips it): the same
      median-of-runs step time for the other workloads and paths, read-flushed
      steps, and a whole-grid parity check against the oracle for each;
-  6. "cpu_baseline": the oracle on all host cores (whole-grid passes, threads
+  7. "cpu_baseline": the oracle on all host cores (whole-grid passes, threads
      each running the unchanged single-threaded oracle on an overlapping slab
      of axis 0) and on one core, the last pass checking the GPU's loss and
      gradient ("parity").
@@ -540,7 +544,16 @@ def main():
     B.lib()
     cfg, bcm, K = args.config, args.bc_mode, args.steps
     case = Case(torch, B, W, cfg, args.seed, args.path, bcm)
-    warmup, run_ms, med, q1, q3, kus = measure(case, K, args.runs, args.warmup)
+    # the headline: W warm-up steps, then the median of the runs of K steps
+    warmup = case.warm(steps=args.warmup)
+    run_ms = case.runs(K, args.runs)
+    q1, med, q3 = _quartiles(run_ms)
+    # the same runs once the GPU has settled on this load (the first few tens of
+    # ms of a new load run slower), then the per-kernel pass in that state
+    steady_warm = case.warm(seconds=0.5)
+    steady_ms = case.runs(K, args.runs)
+    sq1, smed, sq3 = _quartiles(steady_ms)
+    kus = case.kernel_medians(K)
     L = float(case.loss.item())
     if not (L == L) or L <= 0:
         raise RuntimeError(f"bad loss {L}")
@@ -553,7 +566,8 @@ def main():
                 "traffic": measured_traffic(cfg, case.wl.op, TRAFFIC_KERNELS.get(dom, (dom,)),
                                             args.path),
                 "algorithmic_bytes_per_launch": bm[dom], "avg_launch_us": round(kus[dom], 2),
-                "timing": f"median over {K} steps, HIP events around this kernel only"}
+                "timing": f"median over {K} steps, HIP events around this kernel only, "
+                          "after the steady-state runs"}
     ksum = sum(kus.values())
     flushed = flushed_dirty = None
     if args.flushed_steps > 0:
@@ -595,8 +609,19 @@ def main():
         "runs": {"n": len(run_ms), "statistic": "median", "ms_per_step": [round(x, 5) for x in run_ms],
                  "ms_q1": round(q1, 5), "ms_q3": round(q3, 5)},
         "kernel_us": {k: round(v, 2) for k, v in kus.items()},
+        "steady_state": {"warm_steps": steady_warm, "statistic": "median",
+                         "ms_per_step": round(smed, 5),
+                         "ms_per_step_runs": [round(x, 5) for x in steady_ms],
+                         "ms_q1": round(sq1, 5), "ms_q3": round(sq3, 5),
+                         "grid_points_per_s": N / (smed * 1e-3),
+                         "hbm_frac_of_peak": round(bm["step"] / (smed * 1e-3) / 1e9
+                                                   / HBM_PEAK_GBPS, 4)},
+        # (each call's events also hold its own dispatch gap, and the forward's
+        # call launches the loss-zeroing fill too, so in the steady state the
+        # sum runs a few per cent over a back-to-back step)
         "kernel_us_check": {"sum_us": round(ksum, 2), "step_us": round(med * 1e3, 2),
-                            "sum_le_step": bool(ksum <= med * 1e3)},
+                            "sum_le_step": bool(ksum <= med * 1e3),
+                            "steady_step_us": round(smed * 1e3, 2)},
         "copy_gbps": cgbps,
         "flushed": flushed,
         "flushed_dirty": flushed_dirty,
