@@ -438,7 +438,8 @@ def oracle_one_core(wl, bc_mode, path, seed, W, min_s=10.0):
 
 
 def host_cores():
-    """Host cores this process may use, at most 16 (one GPU's share of the box)."""
+    """Host cores this process may use, at most 16 (the host's share for one GPU
+    on an eight-GPU machine)."""
     try:
         n = len(os.sched_getaffinity(0))
     except AttributeError:  # pragma: no cover
