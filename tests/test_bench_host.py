@@ -1,6 +1,7 @@
 """Host-side parts of bench.py (no GPU): the byte model, the all-core CPU
 baseline, whose slab passes must reproduce the whole-grid oracle, the parity
-verdict and the choice of the profile record behind roofline.traffic."""
+verdict, the choice of the profile record behind roofline.traffic, and the
+refusal of more than one GPU."""
 from __future__ import annotations
 
 import numpy as np
@@ -71,3 +72,16 @@ def test_measured_traffic_only_for_matching_records(tmp_path, monkeypatch):
     assert bench.measured_traffic("ns_3d_tgv", op, ["fwd"]) is None  # no such kernel
     monkeypatch.setattr(profiling, "source_hash", lambda root=None: "changed")
     assert bench.measured_traffic("ns_3d_tgv", op, ["bwd"]) is None
+
+
+def test_more_than_one_gpu_is_refused():
+    """bench.py measures one GPU: --gpus above 1 exits with status 2 and says
+    so, before touching a GPU."""
+    import os  # noqa: PLC0415
+    import subprocess  # noqa: PLC0415
+    import sys  # noqa: PLC0415
+    root = os.path.dirname(os.path.abspath(bench.__file__))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
